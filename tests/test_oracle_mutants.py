@@ -1,0 +1,75 @@
+"""Mutation check of the pins: plant one plausible mistake at a time in a copy of
+the oracle's C source (CPU only), build it, and require the pin battery to reject
+it.  A mutant that passes every pin would mean that part of the oracle is not
+pinned.  Mutations are chosen so that the broken build still stays in bounds."""
+import os
+import subprocess
+
+import pytest
+
+import oracle
+from oracle_pins import ALL_PINS
+
+SRC = os.path.join(os.path.dirname(oracle.__file__), "omnimem_oracle.c")
+
+# (name, exact text in the source, replacement)
+MUTANTS = [
+    ("pool_divides_by_B", "kbar[((int64_t)h * nb + b) * d + j] = sum / count;",
+     "kbar[((int64_t)h * nb + b) * d + j] = sum / B;"),
+    ("tail_block_drops_last_token", "int end = begin + B < S ? begin + B : S;",
+     "int end = begin + B < S ? begin + B : S - 1;"),
+    ("proxy_query_sum_not_mean", "qbar[(((int64_t)h * R) + r) * d + j] = sum / (q1 - q0);",
+     "qbar[(((int64_t)h * R) + r) * d + j] = sum;"),
+    ("group_boundary_off_by_one", "int q0 = r * G_q, q1 = q0 + G_q < Lq ? q0 + G_q : Lq;",
+     "int q0 = r * G_q, q1 = q0 + G_q < Lq ? q0 + G_q + 1 : Lq;"),
+    ("awe_chunk_threshold_strict", "return (outside_chunks >= T_out && outside_blocks >= K) ? 1 : 0;",
+     "return (outside_chunks > T_out && outside_blocks >= K) ? 1 : 0;"),
+    ("awe_block_guard_strict", "return (outside_chunks >= T_out && outside_blocks >= K) ? 1 : 0;",
+     "return (outside_chunks >= T_out && outside_blocks > K) ? 1 : 0;"),
+    ("awe_block_guard_dropped", "return (outside_chunks >= T_out && outside_blocks >= K) ? 1 : 0;",
+     "return (outside_chunks >= T_out) ? 1 : 0;"),
+    ("window_off_by_one", "int in_window = c >= n - E;", "int in_window = c > n - E;"),
+    ("window_uses_offset_not_chunk", "int c = (int)(b / Bpc);\n    int in_window", "int c = (int)(b % Bpc);\n    int in_window"),
+    ("residency_ignored_in_selection", "int is_resident = resident == NULL ? 1 : (resident[b] != 0);",
+     "int is_resident = 1;"),
+    ("ranking_reversed", "if (a->s > b->s) return -1;\n  if (a->s < b->s) return 1;",
+     "if (a->s > b->s) return 1;\n  if (a->s < b->s) return -1;"),
+    ("tie_break_reversed", "return (a->b < b->b) ? -1 : (a->b > b->b);", "return (a->b > b->b) ? -1 : (a->b < b->b);"),
+    ("output_not_sorted_by_id", "qsort(chosen, (size_t)take, sizeof(int32_t), id_cmp);", ";"),
+    ("score_unscaled", "double sb = scale * dot;", "double sb = dot;"),
+    ("logit_unscaled", "logit_buf[i] = scale * dot;", "logit_buf[i] = dot;"),
+    ("lse_missing_max", "*lse = mx + log(denom);", "*lse = log(denom);"),
+    ("values_read_from_keys", "out[j] += w * widen(V, kv_at", "out[j] += w * widen(K, kv_at"),
+    ("kv_layout_transposed", "return (((int64_t)c * S + t) * H + h) * d + j;", "return (((int64_t)c * S + t) * d + j) * H + h;"),
+    ("residency_ignored_in_attention", "if (resident != NULL && !resident[b]) return nk;", "if (0) return nk;"),
+    ("sparse_uses_first_group", "int h = hs[i], q = qs[i], r = q / G_q;", "int h = hs[i], q = qs[i], r = 0;"),
+    ("dense_drops_last_chunk", "for (int32_t b = c0 * Bpc; b < c1 * Bpc; ++b)", "for (int32_t b = c0 * Bpc; b < (c1 - 1) * Bpc; ++b)"),
+    ("softmax_not_normalised", "for (int j = 0; j < d; ++j) out[j] /= denom;", ";"),
+    ("bf16_widened_wrong", "uint32_t bits = ((uint32_t)((const uint16_t*)base)[i]) << 16;",
+     "uint32_t bits = ((uint32_t)((const uint16_t*)base)[i]) << 15;"),
+    ("union_counts_duplicates", "if (!mine[b]) { mine[b] = 1; ++count; }", "{ mine[b] = 1; ++count; }"),
+]
+
+
+@pytest.fixture(scope="module")
+def source():
+    with open(SRC) as f:
+        return f.read()
+
+
+@pytest.mark.parametrize("name,old,new", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_pins_reject_mutant(name, old, new, source, tmp_path):
+    assert source.count(old) >= 1, f"mutation site for {name} not found in the oracle source"
+    mutated = source.replace(old, new, 1)
+    src = tmp_path / "mutant.c"
+    src.write_text(mutated)
+    so = tmp_path / "libmutant.so"
+    subprocess.check_call(["gcc", "-O1", "-fopenmp", "-fPIC", "-shared", "-w", "-o", str(so), str(src), "-lm"])
+    caught = []
+    with oracle.using_library(str(so)):
+        for pin in ALL_PINS:
+            try:
+                pin()
+            except (AssertionError, ValueError, ZeroDivisionError, FloatingPointError):
+                caught.append(pin.__name__)
+    assert caught, f"mutant {name} passed every pin"
