@@ -1,0 +1,25 @@
+"""OmniMem memory-retrieval attention (arXiv 2605.30519) on AMD MI355X.
+
+The compute path is libomnimem.so (hand-written HIP for gfx950, C ABI in
+include/omnimem.h); ``omnimem`` is its thin ctypes binding and ``synth`` the
+seeded synthetic-input generator.  Importing this package loads nothing: the
+library is opened on the first call.
+"""
+from .omnimem import (  # noqa: F401
+    EXPORTED,
+    OmniMemError,
+    PagedKVCache,
+    Selection,
+    lib,
+    library_path,
+    omnimem_awe_active,
+    omnimem_blocks_per_chunk,
+    omnimem_dense_attn,
+    omnimem_select,
+    omnimem_select_workspace_bytes,
+    omnimem_sparse_attn,
+    omnimem_status_string,
+    omnimem_union_gather_attn,
+    omnimem_union_workspace_bytes,
+    select_params,
+)

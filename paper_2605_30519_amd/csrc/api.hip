@@ -1,0 +1,224 @@
+// api.hip -- the extern "C" entry points of libomnimem.so: host-side validation,
+// workspace planning and kernel launch.  Nothing here allocates memory or
+// synchronises with the device.
+#include <math.h>
+#include <stdint.h>
+
+#include "../../include/omnimem.h"
+#include "launch.h"
+
+#define OMNIMEM_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+using omnimem::CacheGeom;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// Resolves and validates a cache descriptor.  Returns OMNIMEM_OK or an error.
+omnimem_status_t resolve_cache(const omnimem_kv_cache_t* kv, CacheGeom& g) {
+  if (kv == nullptr) return OMNIMEM_EINVAL;
+  if (kv->dtype != OMNIMEM_BF16 && kv->dtype != OMNIMEM_F32) return OMNIMEM_EUNSUPPORTED;
+  if (kv->num_heads < 1 || kv->chunk_tokens < 1 || kv->num_chunks < 0 || kv->num_pages < 0) return OMNIMEM_EINVAL;
+  if (kv->head_dim != 64 && kv->head_dim != 128) return OMNIMEM_EUNSUPPORTED;
+  if (kv->block_size != 64 && kv->block_size != 128) return OMNIMEM_EUNSUPPORTED;
+  g.dtype = kv->dtype == OMNIMEM_BF16 ? 0 : 1;
+  g.H = kv->num_heads;
+  g.D = kv->head_dim;
+  g.B = kv->block_size;
+  g.S = kv->chunk_tokens;
+  g.n = kv->num_chunks;
+  g.Bpc = (g.S + g.B - 1) / g.B;
+  const int64_t nb = static_cast<int64_t>(g.n) * g.Bpc;
+  if (nb > (int64_t{1} << 30)) return OMNIMEM_EINVAL;
+  g.nb = static_cast<int>(nb);
+  g.num_pages = kv->num_pages;
+  // page pool size in elements must fit comfortably in int64 addressing
+  if (g.num_pages > (int64_t{1} << 40) / (static_cast<int64_t>(g.H) * g.B * g.D)) return OMNIMEM_EINVAL;
+  g.k_pages = kv->k_pages;
+  g.v_pages = kv->v_pages;
+  g.page_table = kv->page_table;
+  if (g.nb > 0) {
+    if (g.page_table == nullptr) return OMNIMEM_EINVAL;
+    if (g.num_pages > 0 && (g.k_pages == nullptr || g.v_pages == nullptr)) return OMNIMEM_EINVAL;
+    if (!aligned16(g.k_pages) || !aligned16(g.v_pages) || (reinterpret_cast<uintptr_t>(g.page_table) & 3u))
+      return OMNIMEM_EINVAL;
+  }
+  return OMNIMEM_OK;
+}
+
+omnimem_status_t hip_status(hipError_t e) { return e == hipSuccess ? OMNIMEM_OK : OMNIMEM_EHIP; }
+
+bool good_scale(float s) { return isfinite(s) && s > 0.f; }
+
+omnimem_status_t check_attn_common(const CacheGeom& g, const void* q, int32_t lq, const void* out) {
+  (void)g;
+  if (lq < 0) return OMNIMEM_EINVAL;
+  if (lq == 0) return OMNIMEM_OK;
+  if (q == nullptr || out == nullptr || !aligned16(q) || !aligned16(out)) return OMNIMEM_EINVAL;
+  return OMNIMEM_OK;
+}
+
+}  // namespace
+
+OMNIMEM_API int32_t omnimem_blocks_per_chunk(int32_t chunk_tokens, int32_t block_size) {
+  if (chunk_tokens < 1 || block_size < 1) return -1;
+  return (chunk_tokens + block_size - 1) / block_size;
+}
+
+OMNIMEM_API int32_t omnimem_awe_active(int32_t n, int32_t E, int32_t T_out, int32_t K, int32_t Bpc) {
+  if (n < 0 || E < 0 || T_out < 0 || K < 1 || Bpc < 1) return -1;
+  const int64_t outside = n > E ? static_cast<int64_t>(n) - E : 0;
+  return (outside >= T_out && outside * Bpc >= K) ? 1 : 0;
+}
+
+namespace {
+
+omnimem_status_t resolve_select(const omnimem_kv_cache_t* kv, int32_t lq, const omnimem_select_params_t* p,
+                                CacheGeom& g, omnimem::SelectPlan& plan) {
+  omnimem_status_t st = resolve_cache(kv, g);
+  if (st != OMNIMEM_OK) return st;
+  if (p == nullptr || lq < 0) return OMNIMEM_EINVAL;
+  if (p->top_k < 1 || p->group_size < 1 || p->window_chunks < 0 || p->awe_min_outside_chunks < 0 ||
+      !good_scale(p->scale))
+    return OMNIMEM_EINVAL;
+  const int awe = omnimem_awe_active(g.n, p->window_chunks, p->awe_min_outside_chunks, p->top_k, g.Bpc);
+  if (lq == 0) {
+    plan = omnimem::SelectPlan{};
+    plan.awe = awe;
+    return OMNIMEM_OK;
+  }
+  plan = omnimem::plan_select(g, lq, p->top_k, p->group_size, p->window_chunks, p->awe_min_outside_chunks, p->scale,
+                              awe);
+  return OMNIMEM_OK;
+}
+
+}  // namespace
+
+OMNIMEM_API size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq,
+                                                  const omnimem_select_params_t* p) {
+  CacheGeom g;
+  omnimem::SelectPlan plan;
+  if (resolve_select(kv, lq, p, g, plan) != OMNIMEM_OK) return 0;
+  return lq == 0 ? 256 : plan.total;
+}
+
+OMNIMEM_API omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                            const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt,
+                                            float* score, int32_t* awe_active, void* workspace,
+                                            size_t workspace_bytes, void* stream) {
+  CacheGeom g;
+  omnimem::SelectPlan plan;
+  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
+  if (st != OMNIMEM_OK) return st;
+  if (awe_active) *awe_active = plan.awe;
+  if (lq == 0) return OMNIMEM_OK;
+  if (q == nullptr || idx == nullptr || cnt == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
+  if (!aligned16(q) || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
+  if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
+  return hip_status(
+      omnimem::launch_select(g, plan, q, idx, cnt, score, workspace, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API omnimem_status_t omnimem_sparse_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                                 const int32_t* idx, const int32_t* cnt, int32_t top_k,
+                                                 int32_t group_size, float scale, void* out, float* lse,
+                                                 void* stream) {
+  CacheGeom g;
+  omnimem_status_t st = resolve_cache(kv, g);
+  if (st != OMNIMEM_OK) return st;
+  if (top_k < 1 || group_size < 1 || !good_scale(scale)) return OMNIMEM_EINVAL;
+  st = check_attn_common(g, q, lq, out);
+  if (st != OMNIMEM_OK || lq == 0) return st;
+  if (idx == nullptr || cnt == nullptr) return OMNIMEM_EINVAL;
+  omnimem::AttnLaunch a{};
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.lq = lq;
+  a.group_size = group_size;
+  a.R = (lq + group_size - 1) / group_size;
+  a.idx = idx;
+  a.cnt = cnt;
+  a.top_k = top_k;
+  a.scale = scale;
+  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API omnimem_status_t omnimem_dense_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                                int32_t chunk_begin, int32_t chunk_end, float scale, void* out,
+                                                float* lse, void* stream) {
+  CacheGeom g;
+  omnimem_status_t st = resolve_cache(kv, g);
+  if (st != OMNIMEM_OK) return st;
+  if (chunk_begin < 0 || chunk_end < chunk_begin || chunk_end > g.n || !good_scale(scale)) return OMNIMEM_EINVAL;
+  st = check_attn_common(g, q, lq, out);
+  if (st != OMNIMEM_OK || lq == 0) return st;
+  omnimem::AttnLaunch a{};
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.lq = lq;
+  a.group_size = lq;
+  a.R = 1;
+  a.idx = nullptr;
+  a.cnt = nullptr;
+  a.top_k = 1;
+  a.dense_first_block = chunk_begin * g.Bpc;
+  a.dense_num_blocks = (chunk_end - chunk_begin) * g.Bpc;
+  a.scale = scale;
+  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API size_t omnimem_union_workspace_bytes(const omnimem_kv_cache_t* kv) {
+  CacheGeom g;
+  if (resolve_cache(kv, g) != OMNIMEM_OK) return 0;
+  return omnimem::plan_union(g).total;
+}
+
+OMNIMEM_API omnimem_status_t omnimem_union_gather_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                                       const int32_t* idx, const int32_t* cnt, int32_t top_k,
+                                                       int32_t group_size, float scale, void* out, float* lse,
+                                                       int32_t* union_blocks, void* workspace,
+                                                       size_t workspace_bytes, void* stream) {
+  CacheGeom g;
+  omnimem_status_t st = resolve_cache(kv, g);
+  if (st != OMNIMEM_OK) return st;
+  if (top_k < 1 || group_size < 1 || !good_scale(scale)) return OMNIMEM_EINVAL;
+  st = check_attn_common(g, q, lq, out);
+  if (st != OMNIMEM_OK || lq == 0) return st;
+  if (idx == nullptr || cnt == nullptr || union_blocks == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return OMNIMEM_EINVAL;
+  const omnimem::UnionPlan up = omnimem::plan_union(g);
+  if (workspace_bytes < up.total) return OMNIMEM_EWORKSPACE;
+  omnimem::AttnLaunch a{};
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.lq = lq;
+  a.group_size = group_size;
+  a.R = (lq + group_size - 1) / group_size;
+  a.idx = idx;
+  a.cnt = cnt;
+  a.top_k = top_k;
+  a.scale = scale;
+  return hip_status(
+      omnimem::launch_union_gather(g, up, a, union_blocks, workspace, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API const char* omnimem_status_string(int32_t status) {
+  switch (status) {
+    case OMNIMEM_OK:
+      return "ok";
+    case OMNIMEM_EINVAL:
+      return "invalid argument";
+    case OMNIMEM_EUNSUPPORTED:
+      return "unsupported shape or dtype";
+    case OMNIMEM_EWORKSPACE:
+      return "workspace too small";
+    case OMNIMEM_EHIP:
+      return "HIP launch error";
+    default:
+      return "unknown status";
+  }
+}

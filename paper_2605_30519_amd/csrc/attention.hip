@@ -1,0 +1,414 @@
+// attention.hip -- attention over per-(head, group) block lists read in place from
+// the paged KV cache (Sec. 3.3 Eq. 5, Per-Head Scattered KV Access; App. C Alg. 1
+// Step 2), and over contiguous chunk ranges (dense / sliding-window attention).
+//
+// bf16 kernel (k_attn_bf16): flash-style, one workgroup = 4 waves = a tile of
+// query rows of one (head, query group); the group's block list is walked 64 keys
+// at a time.  Each 64-key tile of K and V (one (page, head) slab, or half of one at
+// B = 128) is staged in LDS with 16-byte coalesced loads, prefetched into registers
+// one tile ahead.  Every wave keeps 32 query rows of Q in registers and computes
+//   S^T = K Q^T        on v_mfma_f32_32x32x16_bf16 (K rows as the A operand),
+//   O^T += V^T P^T     on the same instruction, V^T read with ds_read_b64_tr_b16,
+// so that each lane owns one query column of both S^T and O^T: the online softmax
+// (fp32, exp2 domain with the scale folded in) and the rescaling of O need one
+// cross-lane exchange (lane l <-> l^32) per tile and no transposes.  The A-operand
+// rows of K are fed in an order (bits 2 and 3 of the row swapped) that makes the
+// S^T accumulator registers line up with the B-operand layout of P^T, so P goes from
+// accumulator to MFMA operand with a bf16 pack and nothing else.
+//
+// f32 kernel (k_attn_f32): one lane per query row, fp32 dot products and exact
+// expf-based online softmax, for fp32 inputs.
+#include <math.h>
+
+#include "device_common.h"
+#include "launch.h"
+
+namespace omnimem {
+namespace {
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kLn2 = 0.6931471805599453f;
+
+struct AttnArgs {
+  const void* q;
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* page_table;
+  int64_t num_pages;
+  int H, S, B, Bpc, nb;
+  int lq, G, R;
+  const int32_t* idx;
+  const int32_t* cnt;
+  int top_k;
+  int dense_first, dense_count;
+  float scale;
+  void* out;
+  float* lse;
+  int tiles_per_group;
+};
+
+// Walks the (block, sub-tile) sequence of a block list, skipping padding,
+// out-of-range ids and non-resident pages.  Everything here is workgroup-uniform.
+template <int TK>
+struct TileWalk {
+  const AttnArgs& a;
+  const int32_t* list;
+  int count;
+  int t = 0, sub = 0;
+  int64_t page = 0;
+  int nvalid = 0;
+
+  __device__ TileWalk(const AttnArgs& args, const int32_t* l, int c) : a(args), list(l), count(c) {}
+
+  // position on the next non-empty tile at or after (t, sub); false at the end
+  __device__ bool seek() {
+    while (t < count) {
+      const int id = list ? list[t] : a.dense_first + t;
+      if (id >= 0 && id < a.nb) {
+        const int32_t p = a.page_table[id];
+        if (p >= 0 && p < a.num_pages) {
+          const int o = id % a.Bpc;
+          const int in_block = (o == a.Bpc - 1 ? a.S - o * a.B : a.B) - sub * TK;
+          if (in_block > 0) {
+            page = p;
+            nvalid = in_block < TK ? in_block : TK;
+            return true;
+          }
+        }
+      }
+      ++t;
+      sub = 0;
+    }
+    return false;
+  }
+  __device__ void advance() {
+    if (++sub * TK >= a.B) {
+      ++t;
+      sub = 0;
+    }
+  }
+  __device__ int64_t slab_offset(int h, int D) const {
+    return (page * a.H + h) * static_cast<int64_t>(a.B) * D + static_cast<int64_t>(sub) * TK * D;
+  }
+};
+
+__device__ __forceinline__ void resolve_tile(const AttnArgs& a, int rows_per_wg, int& h, int& hr, int& row0,
+                                             int& row_end) {
+  const int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
+  const int tile = id % a.tiles_per_group;
+  hr = id / a.tiles_per_group;
+  const int r = hr % a.R;
+  h = hr / a.R;
+  const int g_begin = r * a.G;
+  const int g_end = min(g_begin + a.G, a.lq);
+  row0 = g_begin + tile * rows_per_wg;
+  row_end = min(row0 + rows_per_wg, g_end);
+}
+
+__device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const int32_t*& list, int& count) {
+  if (a.idx) {
+    list = a.idx + static_cast<int64_t>(hr) * a.top_k;
+    const int c = a.cnt[hr];
+    count = c < 0 ? 0 : (c > a.top_k ? a.top_k : c);
+  } else {
+    list = nullptr;
+    count = a.dense_count;
+  }
+}
+
+// ------------------------------------------------------------------ bf16 / MFMA
+constexpr int kTileKeys = 64;
+constexpr int kWaves = 4;
+
+// A-operand row order for S^T = K Q^T: swapping bits 2 and 3 of the row makes the
+// accumulator element i of lane l hold key 8*(l/32)+i (i < 8) or 16+8*(l/32)+(i-8).
+__device__ __forceinline__ int s_row_perm(int x) { return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1); }
+
+template <int D>
+__global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
+  constexpr int ROWS = kWaves * 32;
+  constexpr int LDS_STRIDE = D + 8;                 // bf16 elements per LDS row (pad against bank conflicts)
+  constexpr int CHUNKS_PER_ROW = D / 8;             // 16-byte chunks per key row
+  constexpr int CPT = kTileKeys * CHUNKS_PER_ROW / (kWaves * kWave);  // chunks per thread per tile
+  constexpr int DT = D / 32;                        // 32-wide output tiles along d
+  constexpr int KK = D / 16;                        // k-steps of QK^T
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kTileKeys * LDS_STRIDE];
+  uint16_t* k_lds = lds;
+  uint16_t* v_lds = lds + kTileKeys * LDS_STRIDE;
+
+  int h, hr, row0, row_end;
+  resolve_tile(a, ROWS, h, hr, row0, row_end);
+  if (row0 >= row_end) return;  // workgroup-uniform: no barrier has been reached
+  const int32_t* list;
+  int count;
+  resolve_list(a, hr, list, count);
+
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int half = lane / 32;
+  const uint16_t* qp = static_cast<const uint16_t*>(a.q);
+  const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
+  const uint16_t* vp = static_cast<const uint16_t*>(a.v_pages);
+
+  // Q^T as the B operand: lane holds query (lane % 32), d = 16*kk + 8*half + 0..7
+  const int my_row = row0 + wave * 32 + lane % 32;
+  bf16x8 qreg[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    uint4 raw = make_uint4(0, 0, 0, 0);
+    if (my_row < row_end)
+      raw = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(my_row) * a.H + h) * D + 16 * kk + 8 * half);
+    qreg[kk] = __builtin_bit_cast(bf16x8, raw);
+  }
+
+  f32x16 o_acc[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) o_acc[dt][i] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = a.scale * kLog2e;
+
+  TileWalk<kTileKeys> walk(a, list, count);
+  uint4 kreg[CPT], vreg[CPT];
+  auto prefetch = [&]() {
+    const uint16_t* ks = kp + walk.slab_offset(h, D);
+    const uint16_t* vs = vp + walk.slab_offset(h, D);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int cid = tid + i * kWaves * kWave;
+      const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
+      if (row < walk.nvalid) {
+        kreg[i] = *reinterpret_cast<const uint4*>(ks + row * D + c8 * 8);
+        vreg[i] = *reinterpret_cast<const uint4*>(vs + row * D + c8 * 8);
+      } else {
+        kreg[i] = make_uint4(0, 0, 0, 0);
+        vreg[i] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+
+  bool have = walk.seek();
+  if (have) prefetch();
+  const int krow = s_row_perm(lane % 32);
+  while (have) {
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int cid = tid + i * kWaves * kWave;
+      const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
+      *reinterpret_cast<uint4*>(k_lds + row * LDS_STRIDE + c8 * 8) = kreg[i];
+      *reinterpret_cast<uint4*>(v_lds + row * LDS_STRIDE + c8 * 8) = vreg[i];
+    }
+    const int nvalid = walk.nvalid;
+    __syncthreads();
+    walk.advance();
+    have = walk.seek();
+    if (have) prefetch();
+
+    // ---- S^T = K Q^T for keys [0, 64): two 32-key accumulators
+    f32x16 s_acc[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s_acc[t2][i] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        const bf16x8 kf =
+            *reinterpret_cast<const bf16x8*>(k_lds + (32 * t2 + krow) * LDS_STRIDE + 16 * kk + 8 * half);
+        s_acc[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qreg[kk], s_acc[t2], 0, 0, 0);
+      }
+    }
+
+    // ---- online softmax for this lane's query (exp2 domain)
+    float x[2][16];
+    float mloc = -INFINITY;
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
+        const float v = key < nvalid ? s_acc[t2][i] * c : -INFINITY;
+        x[t2][i] = v;
+        mloc = fmaxf(mloc, v);
+      }
+    const float m_tile = fmaxf(mloc, __shfl_xor(mloc, 32));
+    const float m_new = fmaxf(m_run, m_tile);
+    const float m_use = m_new == -INFINITY ? 0.f : m_new;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
+    float psum = 0.f;
+    bf16x8 pb[4];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = __builtin_amdgcn_exp2f(x[t2][i] - m_use);
+        psum += p;
+        pb[2 * t2 + i / 8][i % 8] = static_cast<__bf16>(p);
+      }
+    l_run = l_run * alpha + psum;
+    m_run = m_new;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o_acc[dt][i] *= alpha;
+
+    // ---- O^T += V^T P^T: 4 key steps of 16
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * LDS_STRIDE + col));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * LDS_STRIDE + col));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
+      }
+    }
+    __syncthreads();
+  }
+
+  // ---- epilogue: normalise, stage O through LDS, store rows with 16-byte writes
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+  constexpr int SSTRIDE = D + 8;
+  uint16_t* stage = lds + wave * 32 * SSTRIDE;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) {
+      const int d0 = 32 * dt + 8 * i4 + 4 * half;
+      bf16x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(o_acc[dt][4 * i4 + e] * inv);
+      *reinterpret_cast<bf16x4*>(stage + (lane % 32) * SSTRIDE + d0) = w;
+    }
+  __syncthreads();
+  uint16_t* op = static_cast<uint16_t*>(a.out);
+  constexpr int OCHUNKS = 32 * CHUNKS_PER_ROW;
+#pragma unroll
+  for (int i = 0; i < OCHUNKS / kWave; ++i) {
+    const int cid = lane + i * kWave;
+    const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
+    const int qrow = row0 + wave * 32 + row;
+    if (qrow < row_end)
+      *reinterpret_cast<uint4*>(op + (static_cast<int64_t>(qrow) * a.H + h) * D + c8 * 8) =
+          *reinterpret_cast<const uint4*>(stage + row * SSTRIDE + c8 * 8);
+  }
+  if (a.lse && lane < 32 && my_row < row_end)
+    a.lse[static_cast<int64_t>(h) * a.lq + my_row] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+}
+
+// ------------------------------------------------------------------ fp32 / SIMT
+constexpr int kF32Keys = 32;
+
+template <int D>
+__global__ __launch_bounds__(kWave) void k_attn_f32(AttnArgs a) {
+  __shared__ float k_lds[kF32Keys][D];
+  __shared__ float v_lds[kF32Keys][D];
+  int h, hr, row0, row_end;
+  resolve_tile(a, kWave, h, hr, row0, row_end);
+  if (row0 >= row_end) return;
+  const int32_t* list;
+  int count;
+  resolve_list(a, hr, list, count);
+  const int lane = threadIdx.x;
+  const int my_row = row0 + lane;
+  const bool active = my_row < row_end;
+  const float* qp = static_cast<const float*>(a.q);
+  const float* kp = static_cast<const float*>(a.k_pages);
+  const float* vp = static_cast<const float*>(a.v_pages);
+
+  float qv[D], o[D];
+#pragma unroll
+  for (int j = 0; j < D; ++j) {
+    qv[j] = active ? qp[(static_cast<int64_t>(my_row) * a.H + h) * D + j] : 0.f;
+    o[j] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
+  TileWalk<kF32Keys> walk(a, list, count);
+  while (walk.seek()) {
+    const float* ks = kp + walk.slab_offset(h, D);
+    const float* vs = vp + walk.slab_offset(h, D);
+    const int nvalid = walk.nvalid;
+    for (int i = lane; i < kF32Keys * D / 4; i += kWave) {
+      const int row = i / (D / 4), c4 = i % (D / 4);
+      float4 kv = make_float4(0.f, 0.f, 0.f, 0.f), vv = kv;
+      if (row < nvalid) {
+        kv = *reinterpret_cast<const float4*>(ks + row * D + 4 * c4);
+        vv = *reinterpret_cast<const float4*>(vs + row * D + 4 * c4);
+      }
+      *reinterpret_cast<float4*>(&k_lds[row][4 * c4]) = kv;
+      *reinterpret_cast<float4*>(&v_lds[row][4 * c4]) = vv;
+    }
+    __syncthreads();
+    for (int key = 0; key < nvalid; ++key) {
+      float dot = 0.f;
+#pragma unroll
+      for (int j = 0; j < D; ++j) dot = fmaf(qv[j], k_lds[key][j], dot);
+      const float s = a.scale * dot;
+      const float m_new = fmaxf(m, s);
+      const float alpha = expf(m - m_new);
+      const float p = expf(s - m_new);
+      l = l * alpha + p;
+#pragma unroll
+      for (int j = 0; j < D; ++j) o[j] = fmaf(p, v_lds[key][j], o[j] * alpha);
+      m = m_new;
+    }
+    __syncthreads();
+    walk.advance();
+  }
+  if (!active) return;
+  float* op = static_cast<float*>(a.out) + (static_cast<int64_t>(my_row) * a.H + h) * D;
+  const float inv = l > 0.f ? 1.0f / l : 0.f;
+#pragma unroll
+  for (int j = 0; j < D; ++j) op[j] = o[j] * inv;
+  if (a.lse) a.lse[static_cast<int64_t>(h) * a.lq + my_row] = l > 0.f ? m + logf(l) : -INFINITY;
+}
+
+}  // namespace
+
+hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t stream) {
+  AttnArgs a;
+  a.q = L.q;
+  a.k_pages = g.k_pages;
+  a.v_pages = g.v_pages;
+  a.page_table = g.page_table;
+  a.num_pages = g.num_pages;
+  a.H = g.H;
+  a.S = g.S;
+  a.B = g.B;
+  a.Bpc = g.Bpc;
+  a.nb = g.nb;
+  a.lq = L.lq;
+  a.G = L.group_size;
+  a.R = L.R;
+  a.idx = L.idx;
+  a.cnt = L.cnt;
+  a.top_k = L.top_k;
+  a.dense_first = L.dense_first_block;
+  a.dense_count = L.dense_num_blocks;
+  a.scale = L.scale;
+  a.out = L.out;
+  a.lse = L.lse;
+  const int rows = L.group_size < L.lq ? L.group_size : L.lq;
+  const int rows_per_wg = g.dtype == 0 ? kWaves * 32 : kWave;
+  a.tiles_per_group = (rows + rows_per_wg - 1) / rows_per_wg;
+  const int64_t nwg = static_cast<int64_t>(g.H) * L.R * a.tiles_per_group;
+  if (nwg <= 0) return hipSuccess;
+  if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
+  if (g.dtype == 0) {
+    if (g.D == 128)
+      hipLaunchKernelGGL(k_attn_bf16<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWaves * kWave), 0, stream, a);
+    else
+      hipLaunchKernelGGL(k_attn_bf16<64>, dim3(static_cast<unsigned>(nwg)), dim3(kWaves * kWave), 0, stream, a);
+  } else {
+    if (g.D == 128)
+      hipLaunchKernelGGL(k_attn_f32<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWave), 0, stream, a);
+    else
+      hipLaunchKernelGGL(k_attn_f32<64>, dim3(static_cast<unsigned>(nwg)), dim3(kWave), 0, stream, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace omnimem

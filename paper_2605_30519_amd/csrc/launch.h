@@ -1,0 +1,71 @@
+// launch.h -- host-side launchers of the libomnimem kernels (internal to the library).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace omnimem {
+
+// Geometry of one paged layer cache, resolved and validated on the host.
+struct CacheGeom {
+  int dtype;          // 0 = bf16, 1 = f32
+  int H, D, B, S;     // heads, head dim, tokens per block, tokens per chunk
+  int n;              // cached history chunks
+  int Bpc;            // blocks per chunk = ceil(S/B)
+  int nb;             // history blocks = n * Bpc
+  int64_t num_pages;
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* page_table;
+};
+
+// ---------------------------------------------------------------- selection
+struct SelectPlan {
+  int lq, G, R, K;
+  int awe;              // exclusion active
+  int first_excluded;   // blocks >= this id are outside Omega (nb when exclusion is off)
+  float scale;
+  int qsplit;           // row splits per group in the proxy-query reduction
+  bool inline_scores;   // scores computed inside the pooling kernel (small R)
+  // workspace carve-up (byte offsets)
+  size_t off_qpart, off_qbar, off_kbar, off_scores, total;
+};
+
+constexpr int kQRowsPerSplit = 128;
+constexpr int kInlineGroups = 4;
+
+SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe);
+
+hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
+                         float* score, void* workspace, hipStream_t stream);
+
+// ---------------------------------------------------------------- attention
+struct AttnLaunch {
+  const void* q;
+  void* out;
+  float* lse;
+  int lq;
+  int group_size, R;
+  // sparse mode: per-(h, r) lists; dense mode: idx == nullptr, contiguous block range
+  const int32_t* idx;
+  const int32_t* cnt;
+  int top_k;
+  int dense_first_block, dense_num_blocks;
+  float scale;
+};
+
+hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& a, hipStream_t stream);
+
+// ---------------------------------------------------------------- union gather
+struct UnionPlan {
+  size_t off_flags, off_pos, off_table, off_kbuf, off_vbuf, total;
+  int64_t slab_bytes;  // one (page, head) slab
+};
+
+UnionPlan plan_union(const CacheGeom& g);
+
+hipError_t launch_union_gather(const CacheGeom& g, const UnionPlan& up, const AttnLaunch& a, int32_t* union_blocks,
+                               void* workspace, hipStream_t stream);
+
+}  // namespace omnimem

@@ -1,0 +1,311 @@
+"""Python binding of libomnimem.so (ctypes).  Argument marshalling only: every
+step of the computation runs in the HIP kernels behind the C ABI declared in
+include/omnimem.h.  PyTorch supplies device memory and the current stream.
+
+The functions carry the C names: omnimem_select, omnimem_sparse_attn,
+omnimem_dense_attn, omnimem_union_gather_attn, plus the host-side helpers.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+import threading
+from dataclasses import dataclass
+from typing import Optional
+
+import torch
+
+from . import _build
+
+BF16, F32 = 0, 1
+_DTYPES = {torch.bfloat16: BF16, torch.float32: F32}
+
+_lock = threading.Lock()
+_lib = None
+
+
+class OmniMemError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {omnimem_status_string(status)} (status {status})")
+        self.status = status
+
+
+class omnimem_kv_cache_t(ctypes.Structure):
+    _fields_ = [
+        ("dtype", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("chunk_tokens", ctypes.c_int32),
+        ("num_chunks", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64),
+        ("k_pages", ctypes.c_void_p),
+        ("v_pages", ctypes.c_void_p),
+        ("page_table", ctypes.c_void_p),
+    ]
+
+
+class omnimem_select_params_t(ctypes.Structure):
+    _fields_ = [
+        ("top_k", ctypes.c_int32),
+        ("group_size", ctypes.c_int32),
+        ("window_chunks", ctypes.c_int32),
+        ("awe_min_outside_chunks", ctypes.c_int32),
+        ("scale", ctypes.c_float),
+    ]
+
+
+EXPORTED = [
+    "omnimem_blocks_per_chunk",
+    "omnimem_awe_active",
+    "omnimem_select_workspace_bytes",
+    "omnimem_select",
+    "omnimem_sparse_attn",
+    "omnimem_dense_attn",
+    "omnimem_union_workspace_bytes",
+    "omnimem_union_gather_attn",
+    "omnimem_status_string",
+]
+
+
+def _configure(L):
+    i32, i64, vp, f32, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_size_t
+    kvp = ctypes.POINTER(omnimem_kv_cache_t)
+    pp = ctypes.POINTER(omnimem_select_params_t)
+    L.omnimem_blocks_per_chunk.argtypes = [i32, i32]
+    L.omnimem_blocks_per_chunk.restype = i32
+    L.omnimem_awe_active.argtypes = [i32] * 5
+    L.omnimem_awe_active.restype = i32
+    L.omnimem_select_workspace_bytes.argtypes = [kvp, i32, pp]
+    L.omnimem_select_workspace_bytes.restype = sz
+    L.omnimem_select.argtypes = [kvp, vp, i32, pp, vp, vp, vp, ctypes.POINTER(i32), vp, sz, vp]
+    L.omnimem_select.restype = i32
+    L.omnimem_sparse_attn.argtypes = [kvp, vp, i32, vp, vp, i32, i32, f32, vp, vp, vp]
+    L.omnimem_sparse_attn.restype = i32
+    L.omnimem_dense_attn.argtypes = [kvp, vp, i32, i32, i32, f32, vp, vp, vp]
+    L.omnimem_dense_attn.restype = i32
+    L.omnimem_union_workspace_bytes.argtypes = [kvp]
+    L.omnimem_union_workspace_bytes.restype = sz
+    L.omnimem_union_gather_attn.argtypes = [kvp, vp, i32, vp, vp, i32, i32, f32, vp, vp, vp, vp, sz, vp]
+    L.omnimem_union_gather_attn.restype = i32
+    L.omnimem_status_string.argtypes = [i32]
+    L.omnimem_status_string.restype = ctypes.c_char_p
+    return L
+
+
+def lib():
+    """The loaded libomnimem.so.  Builds it if it has never been built; there is no
+    fallback: without the HIP library nothing in this module runs."""
+    global _lib
+    with _lock:
+        if _lib is None:
+            if not _build.is_built():
+                _build.build()
+            _lib = _configure(ctypes.CDLL(_build.LIB))
+    return _lib
+
+
+def library_path() -> str:
+    return os.path.realpath(_build.LIB)
+
+
+# ----------------------------------------------------------------------- cache
+
+@dataclass
+class PagedKVCache:
+    """One layer's paged KV cache (device tensors owned by the caller).
+
+    k_pages, v_pages: [num_pages, H, B, d] (bf16 or fp32); page_table: [n, Bpc] int32,
+    negative = block not resident."""
+    k_pages: torch.Tensor
+    v_pages: torch.Tensor
+    page_table: torch.Tensor
+    chunk_tokens: int
+
+    @property
+    def num_heads(self) -> int:
+        return int(self.k_pages.shape[1])
+
+    @property
+    def block_size(self) -> int:
+        return int(self.k_pages.shape[2])
+
+    @property
+    def head_dim(self) -> int:
+        return int(self.k_pages.shape[3])
+
+    @property
+    def num_chunks(self) -> int:
+        return int(self.page_table.shape[0])
+
+    @property
+    def blocks_per_chunk(self) -> int:
+        return -(-self.chunk_tokens // self.block_size)
+
+    @property
+    def num_blocks(self) -> int:
+        return self.num_chunks * self.blocks_per_chunk
+
+    @property
+    def dtype(self) -> torch.dtype:
+        return self.k_pages.dtype
+
+    def descriptor(self, num_chunks: Optional[int] = None) -> omnimem_kv_cache_t:
+        """C descriptor; `num_chunks` < n exposes only the oldest chunks (a shorter history)."""
+        if self.k_pages.dtype not in _DTYPES or self.v_pages.dtype != self.k_pages.dtype:
+            raise TypeError(f"unsupported page dtype {self.k_pages.dtype}")
+        for t in (self.k_pages, self.v_pages, self.page_table):
+            if not t.is_contiguous():
+                raise ValueError("cache tensors must be contiguous")
+        if self.page_table.dtype != torch.int32:
+            raise TypeError("page_table must be int32")
+        n = self.num_chunks if num_chunks is None else int(num_chunks)
+        if n > self.num_chunks:
+            raise ValueError("num_chunks exceeds the page table")
+        return omnimem_kv_cache_t(
+            _DTYPES[self.k_pages.dtype], self.num_heads, self.head_dim, self.block_size, self.chunk_tokens, n,
+            int(self.k_pages.shape[0]), self.k_pages.data_ptr(), self.v_pages.data_ptr(),
+            self.page_table.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if isinstance(stream, torch.cuda.Stream):
+        return ctypes.c_void_p(stream.cuda_stream)
+    return ctypes.c_void_p(int(stream))
+
+
+def _ptr(t: Optional[torch.Tensor]):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(None)
+
+
+def _check(status: int, what: str):
+    if status != 0:
+        raise OmniMemError(status, what)
+
+
+def _default_scale(cache: PagedKVCache, scale):
+    return 1.0 / math.sqrt(cache.head_dim) if scale is None else float(scale)
+
+
+# --------------------------------------------------------------- host helpers
+
+def omnimem_blocks_per_chunk(chunk_tokens: int, block_size: int) -> int:
+    return int(lib().omnimem_blocks_per_chunk(chunk_tokens, block_size))
+
+
+def omnimem_awe_active(num_chunks: int, window_chunks: int, awe_min_outside_chunks: int, top_k: int,
+                       blocks_per_chunk: int) -> int:
+    return int(lib().omnimem_awe_active(num_chunks, window_chunks, awe_min_outside_chunks, top_k, blocks_per_chunk))
+
+
+def omnimem_status_string(status: int) -> str:
+    return lib().omnimem_status_string(status).decode()
+
+
+def select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, scale) -> omnimem_select_params_t:
+    return omnimem_select_params_t(top_k, group_size, window_chunks, awe_min_outside_chunks, scale)
+
+
+def omnimem_select_workspace_bytes(cache: PagedKVCache, lq: int, params: omnimem_select_params_t,
+                                   num_chunks: Optional[int] = None) -> int:
+    d = cache.descriptor(num_chunks)
+    return int(lib().omnimem_select_workspace_bytes(ctypes.byref(d), lq, ctypes.byref(params)))
+
+
+def omnimem_union_workspace_bytes(cache: PagedKVCache, num_chunks: Optional[int] = None) -> int:
+    d = cache.descriptor(num_chunks)
+    return int(lib().omnimem_union_workspace_bytes(ctypes.byref(d)))
+
+
+# ------------------------------------------------------------------ the calls
+
+@dataclass
+class Selection:
+    idx: torch.Tensor      # [H, R, K] int32, ascending, -1 padded
+    cnt: torch.Tensor      # [H, R] int32
+    score: Optional[torch.Tensor]  # [H, R, K] float32
+    awe_active: int
+
+
+def workspace_tensor(nbytes: int, device) -> torch.Tensor:
+    # torch's caching allocator returns 256-byte (or better) aligned blocks
+    return torch.empty(max(int(nbytes), 256), dtype=torch.uint8, device=device)
+
+
+def omnimem_select(cache: PagedKVCache, q: torch.Tensor, top_k: int, group_size: int, window_chunks: int,
+                   awe_min_outside_chunks: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
+                   want_score: bool = True, workspace: Optional[torch.Tensor] = None,
+                   out: Optional[Selection] = None, stream=None) -> Selection:
+    lq, H, d = (int(s) for s in q.shape)
+    params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
+    desc = cache.descriptor(num_chunks)
+    R = -(-lq // group_size)
+    dev = q.device
+    if out is None:
+        out = Selection(torch.empty((H, R, top_k), dtype=torch.int32, device=dev),
+                        torch.empty((H, R), dtype=torch.int32, device=dev),
+                        torch.empty((H, R, top_k), dtype=torch.float32, device=dev) if want_score else None, 0)
+    need = int(lib().omnimem_select_workspace_bytes(ctypes.byref(desc), lq, ctypes.byref(params)))
+    if workspace is None:
+        workspace = workspace_tensor(need, dev)
+    awe = ctypes.c_int32(0)
+    st = lib().omnimem_select(ctypes.byref(desc), _ptr(q), lq, ctypes.byref(params), _ptr(out.idx), _ptr(out.cnt),
+                              _ptr(out.score), ctypes.byref(awe), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "omnimem_select")
+    out.awe_active = int(awe.value)
+    return out
+
+
+def omnimem_sparse_attn(cache: PagedKVCache, q: torch.Tensor, idx: torch.Tensor, cnt: torch.Tensor,
+                        group_size: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
+                        out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                        stream=None):
+    lq, H, d = (int(s) for s in q.shape)
+    desc = cache.descriptor(num_chunks)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
+    st = lib().omnimem_sparse_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), int(idx.shape[-1]),
+                                   group_size, _default_scale(cache, scale), _ptr(out), _ptr(lse), _stream(stream))
+    _check(st, "omnimem_sparse_attn")
+    return out, lse
+
+
+def omnimem_dense_attn(cache: PagedKVCache, q: torch.Tensor, chunk_begin: int, chunk_end: int,
+                       scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
+                       out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                       stream=None):
+    lq, H, d = (int(s) for s in q.shape)
+    desc = cache.descriptor(num_chunks)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
+    st = lib().omnimem_dense_attn(ctypes.byref(desc), _ptr(q), lq, chunk_begin, chunk_end,
+                                  _default_scale(cache, scale), _ptr(out), _ptr(lse), _stream(stream))
+    _check(st, "omnimem_dense_attn")
+    return out, lse
+
+
+def omnimem_union_gather_attn(cache: PagedKVCache, q: torch.Tensor, idx: torch.Tensor, cnt: torch.Tensor,
+                              group_size: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
+                              workspace: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
+                              lse: Optional[torch.Tensor] = None, stream=None):
+    lq, H, d = (int(s) for s in q.shape)
+    desc = cache.descriptor(num_chunks)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None:
+        lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
+    union_blocks = torch.zeros(1, dtype=torch.int32, device=q.device)
+    if workspace is None:
+        workspace = workspace_tensor(int(lib().omnimem_union_workspace_bytes(ctypes.byref(desc))), q.device)
+    st = lib().omnimem_union_gather_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), int(idx.shape[-1]),
+                                         group_size, _default_scale(cache, scale), _ptr(out), _ptr(lse),
+                                         _ptr(union_blocks), _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "omnimem_union_gather_attn")
+    return out, lse, union_blocks

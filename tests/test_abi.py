@@ -1,0 +1,159 @@
+"""The C ABI without a GPU: the library loads, exports every symbol that
+include/omnimem.h declares, and rejects invalid arguments on the host before
+anything is launched (so none of these calls reaches the HIP runtime)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from conftest import ROOT
+from paper_2605_30519_amd import omnimem as om
+
+HEADER = os.path.join(ROOT, "include", "omnimem.h")
+FAKE = 0x10000  # aligned, never dereferenced: every call below fails validation first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(omnimem_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = om.lib()
+    names = declared_functions()
+    assert set(names) == set(om.EXPORTED), names
+    for name in names:
+        assert hasattr(L, name), name
+
+
+def test_only_the_abi_is_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", om.library_path()], capture_output=True, text=True).stdout
+    exported = sorted({line.split()[-1] for line in out.splitlines() if " T " in line})
+    assert [n for n in exported if n.startswith("omnimem_")] == declared_functions()
+    assert not [n for n in exported if "omnimem" in n and not n.startswith("omnimem_")]
+
+
+def test_host_helpers():
+    L = om.lib()
+    assert L.omnimem_blocks_per_chunk(4680, 64) == 74
+    assert L.omnimem_blocks_per_chunk(4680, 128) == 37
+    assert L.omnimem_blocks_per_chunk(0, 64) == -1
+    # tiny fp32 workload: exclusion from a 4-chunk history on
+    assert [L.omnimem_awe_active(n, 1, 3, 4, 4) for n in range(9)] == [0, 0, 0, 0, 1, 1, 1, 1, 1]
+    assert L.omnimem_awe_active(10, 1, 0, 36, 4) == 1 and L.omnimem_awe_active(10, 1, 0, 37, 4) == 0
+    assert L.omnimem_awe_active(-1, 1, 3, 4, 4) == -1
+    assert L.omnimem_status_string(0) == b"ok"
+    assert L.omnimem_status_string(-3) == b"workspace too small"
+    assert L.omnimem_status_string(7) == b"unknown status"
+
+
+def test_awe_matches_oracle_truth_table():
+    import oracle
+    L = om.lib()
+    for n in range(0, 9):
+        for E in range(0, 4):
+            for T in range(0, 5):
+                for K in (1, 4, 9, 40):
+                    for Bpc in (1, 4, 74):
+                        assert L.omnimem_awe_active(n, E, T, K, Bpc) == int(oracle.awe_active(n, E, T, K, Bpc))
+
+
+def cache(**kw):
+    d = dict(dtype=0, num_heads=2, head_dim=64, block_size=64, chunk_tokens=256, num_chunks=3, num_pages=12,
+             k_pages=FAKE, v_pages=FAKE, page_table=FAKE)
+    d.update(kw)
+    return om.omnimem_kv_cache_t(**d)
+
+
+def params(**kw):
+    d = dict(top_k=4, group_size=256, window_chunks=1, awe_min_outside_chunks=3, scale=0.125)
+    d.update(kw)
+    return om.omnimem_select_params_t(**d)
+
+
+EINVAL, EUNSUP, EWS = -1, -2, -3
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dtype=7), EUNSUP),
+    (dict(head_dim=96), EUNSUP),
+    (dict(block_size=32), EUNSUP),
+    (dict(num_heads=0), EINVAL),
+    (dict(chunk_tokens=0), EINVAL),
+    (dict(num_chunks=-1), EINVAL),
+    (dict(num_pages=-1), EINVAL),
+    (dict(page_table=0), EINVAL),
+    (dict(k_pages=0), EINVAL),
+    (dict(k_pages=FAKE + 8), EINVAL),
+])
+def test_cache_validation(kw, want):
+    L = om.lib()
+    c = cache(**kw)
+    st = L.omnimem_sparse_attn(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, None)
+    assert st == want
+    st = L.omnimem_dense_attn(ctypes.byref(c), FAKE, 256, 0, 1, 0.125, FAKE, None, None)
+    assert st == want
+
+
+def test_select_validation():
+    L = om.lib()
+    c = cache()
+    ws = L.omnimem_select_workspace_bytes(ctypes.byref(c), 256, ctypes.byref(params()))
+    assert ws > 0 and ws % 256 == 0
+    assert L.omnimem_select_workspace_bytes(None, 256, ctypes.byref(params())) == 0
+    assert L.omnimem_select_workspace_bytes(ctypes.byref(c), 256, ctypes.byref(params(top_k=0))) == 0
+
+    def call(p=params(), lq=256, q=FAKE, idx=FAKE, cnt=FAKE, work=FAKE, nbytes=ws):
+        return L.omnimem_select(ctypes.byref(c), q, lq, ctypes.byref(p), idx, cnt, None, None, work, nbytes, None)
+
+    assert call(p=params(top_k=0)) == EINVAL
+    assert call(p=params(group_size=0)) == EINVAL
+    assert call(p=params(window_chunks=-1)) == EINVAL
+    assert call(p=params(awe_min_outside_chunks=-2)) == EINVAL
+    assert call(p=params(scale=0.0)) == EINVAL
+    assert call(p=params(scale=float("nan"))) == EINVAL
+    assert call(lq=-1) == EINVAL
+    assert call(q=0) == EINVAL
+    assert call(q=FAKE + 2) == EINVAL
+    assert call(idx=0) == EINVAL
+    assert call(cnt=0) == EINVAL
+    assert call(work=0) == EINVAL
+    assert call(work=FAKE + 16) == EINVAL           # workspace must be 256-byte aligned
+    assert call(nbytes=ws - 1) == EWS
+    # lq = 0 is a no-op that still reports the exclusion state
+    awe = ctypes.c_int32(-5)
+    st = L.omnimem_select(ctypes.byref(c), None, 0, ctypes.byref(params()), None, None, None, ctypes.byref(awe), None,
+                          0, None)
+    assert st == 0 and awe.value == 0            # 3 chunks, 2 outside the window < 3
+    c4 = cache(num_chunks=5)
+    st = L.omnimem_select(ctypes.byref(c4), None, 0, ctypes.byref(params()), None, None, None, ctypes.byref(awe), None,
+                          0, None)
+    assert st == 0 and awe.value == 1
+
+
+def test_attention_validation():
+    L = om.lib()
+    c = cache()
+    sp = L.omnimem_sparse_attn
+    assert sp(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 0, 256, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 0, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, -1.0, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, 256, 0, FAKE, 4, 256, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, 256, FAKE, 0, 4, 256, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, 0, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE + 4, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), FAKE, -3, FAKE, FAKE, 4, 256, 0.125, FAKE, None, None) == EINVAL
+    assert sp(ctypes.byref(c), None, 0, None, None, 4, 256, 0.125, None, None, None) == 0   # empty: no-op
+    dn = L.omnimem_dense_attn
+    assert dn(ctypes.byref(c), FAKE, 256, 2, 1, 0.125, FAKE, None, None) == EINVAL
+    assert dn(ctypes.byref(c), FAKE, 256, 0, 4, 0.125, FAKE, None, None) == EINVAL
+    assert dn(ctypes.byref(c), FAKE, 256, -1, 1, 0.125, FAKE, None, None) == EINVAL
+    ug = L.omnimem_union_gather_attn
+    uws = L.omnimem_union_workspace_bytes(ctypes.byref(c))
+    # 12 blocks x 2 heads x (64 x 64 bf16) x (K + V) plus two int32 tables
+    assert uws >= 12 * 2 * 64 * 64 * 2 * 2
+    assert ug(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, FAKE, FAKE, uws - 1, None) == EWS
+    assert ug(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, 0, FAKE, uws, None) == EINVAL

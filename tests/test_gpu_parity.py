@@ -1,0 +1,314 @@
+"""Parity of the HIP path (through the C ABI) with the fp64 oracle.
+
+Small shapes are compared element by element on every output; the full-size
+workloads are compared on the complete selection (all heads, or a head subset
+for the largest) and on sampled attention rows the oracle computes one by one.
+Inputs are the seeded synthetic workloads; the oracle always receives host copies
+of exactly the values the GPU consumed (logical, unpaged layout), while the GPU
+reads a paged cache whose pages are shuffled, whose tail slots hold NaN and which
+may contain non-resident blocks.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_30519_amd import (omnimem_dense_attn, omnimem_select, omnimem_sparse_attn,
+                                  omnimem_union_gather_attn, synth)
+from parity import (check_bf16, check_f32, check_lse, check_selection, say)
+
+pytestmark = pytest.mark.gpu
+NAN = float("nan")
+
+
+@pytest.fixture(scope="module")
+def dev():
+    d = torch.device("cuda:0")
+    torch.cuda.set_device(d)
+    return d
+
+
+def host(x):
+    return x.detach().cpu()
+
+
+def sample_rows(H, Lq, m, seed):
+    rng = np.random.default_rng(seed)
+    return rng.integers(0, H, m).astype(np.int32), rng.integers(0, Lq, m).astype(np.int32)
+
+
+def run_select(cache, x, w, n=None):
+    sel = omnimem_select(cache, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                         num_chunks=n)
+    torch.cuda.synchronize()
+    return sel
+
+
+def oracle_select(x, w, n, resident=None, heads=None):
+    return oracle.select(host(x.q), host(x.k[:n]), w.block_size, w.top_k, w.group_size, w.window_chunks,
+                         w.awe_min_outside_chunks, w.scale, resident=resident, heads=heads, want_all_scores=True)
+
+
+def attn_check(got_out, got_lse, ref_out, ref_lse, hs, qs, dtype, what):
+    o = host(got_out).float().numpy()[qs, hs]
+    lse = host(got_lse).numpy()[hs, qs]
+    if dtype == torch.float32:
+        check_f32(o, ref_out, what)
+        check_lse(lse, ref_lse, what + " lse", 1e-5)
+    else:
+        check_bf16(o, ref_out, what)
+        check_lse(lse, ref_lse, what + " lse", 5e-3)
+
+
+# ----------------------------------------------------------------- tiny fp32
+
+def test_tiny_fp32_every_history_length(dev):
+    w = synth.WORKLOADS["tiny_fp32"]
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=11, pad_value=NAN)
+    for n in range(0, w.history_chunks + 1):
+        say(f"tiny_fp32 n={n}: select / sparse / dense")
+        sel = run_select(cache, x, w, n)
+        ref = oracle_select(x, w, n)
+        assert sel.awe_active == int(ref["awe"]) == int(n >= 4)
+        check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref)
+        if ref["awe"]:  # selected blocks avoid the window exactly when exclusion is on
+            assert (host(sel.idx).numpy() < (n - w.window_chunks) * w.blocks_per_chunk).all()
+        out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale, num_chunks=n)
+        o_ref, l_ref, hs, qs = oracle.sparse_attn(host(x.q), host(x.k[:n]), host(x.v[:n]), w.block_size, ref["idx"],
+                                                  ref["cnt"], w.group_size, w.scale)
+        attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, f"sparse n={n}")
+        for c0 in {0, max(n - w.window_chunks, 0)}:
+            dout, dlse = omnimem_dense_attn(cache, x.q, c0, n, w.scale, num_chunks=n)
+            d_ref, dl_ref, hs, qs = oracle.dense_attn(host(x.q), host(x.k[:n]), host(x.v[:n]), w.block_size, c0, n,
+                                                      w.scale)
+            attn_check(dout, dlse, d_ref, dl_ref, hs, qs, w.dtype, f"dense [{c0},{n})")
+
+
+# ------------------------------------------------- small shapes, every output
+
+SMALL = [
+    # H, d, S, Lq, B, n, K, G, E, T, dtype
+    (3, 128, 300, 300, 64, 6, 7, 130, 1, 2, torch.bfloat16),   # ragged tail block, 3 groups, ragged tiles
+    (2, 64, 200, 333, 64, 5, 5, 333, 1, 3, torch.bfloat16),    # d = 64, one group spanning 3 row tiles
+    (2, 128, 300, 257, 128, 4, 3, 100, 1, 2, torch.bfloat16),  # B = 128 (two 64-key halves, 44-token tail)
+    (2, 128, 130, 70, 64, 3, 2, 1, 1, 1, torch.bfloat16),      # per-query selection (G = 1, R = 70)
+    (2, 128, 300, 300, 64, 5, 4, 15, 1, 3, torch.bfloat16),    # the paper's G = 15 (R = 20)
+    (2, 128, 300, 100, 128, 4, 3, 40, 0, 0, torch.float32),    # fp32, d = 128, B = 128, no window
+    (1, 64, 64, 1, 64, 3, 2, 1, 2, 0, torch.float32),          # one query row, exact-block chunks
+]
+
+
+@pytest.mark.parametrize("H,d,S,Lq,B,n,K,G,E,T,dtype", SMALL)
+def test_small_shapes_every_output(dev, H, d, S, Lq, B, n, K, G, E, T, dtype):
+    say(f"small H={H} d={d} S={S} Lq={Lq} B={B} n={n} K={K} G={G} E={E} T={T} {dtype}")
+    w = synth.Workload("small", H, d, S, Lq, B, n, n, K, G, E, T, dtype, dtype == torch.bfloat16, 1, 7)
+    x = synth.make_layer(w, 0, device=dev)
+    Bpc = w.blocks_per_chunk
+    nonres = [1, n * Bpc - 2] if n * Bpc > 4 else []
+    cache = synth.page_layer(x.k, x.v, B, seed=3, pad_value=NAN, nonresident=nonres, extra_pages=5)
+    resident = synth.resident_mask(cache).numpy()
+    sel = run_select(cache, x, w)
+    ref = oracle_select(x, w, n, resident=resident)
+    assert sel.awe_active == int(ref["awe"])
+    check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref)
+    assert not np.isin(host(sel.idx).numpy(), nonres).any()
+    got_score = host(sel.score).numpy()
+    want = np.where(ref["idx"] >= 0, ref["score"], -np.inf)
+    fin = np.isfinite(want)
+    assert np.allclose(got_score[fin], want[fin], rtol=1e-4, atol=1e-5) and np.isneginf(got_score[~fin]).all()
+
+    out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, G, w.scale)
+    o_ref, l_ref, hs, qs = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), B, ref["idx"], ref["cnt"], G, w.scale,
+                                              resident=resident)
+    attn_check(out, lse, o_ref, l_ref, hs, qs, dtype, "sparse")
+    for c0, c1 in [(0, n), (n - 1, n), (1, n - 1)]:
+        dout, dlse = omnimem_dense_attn(cache, x.q, c0, c1, w.scale)
+        d_ref, dl_ref, hs, qs = oracle.dense_attn(host(x.q), host(x.k), host(x.v), B, c0, c1, w.scale,
+                                                  resident=resident)
+        attn_check(dout, dlse, d_ref, dl_ref, hs, qs, dtype, f"dense [{c0},{c1})")
+    # the union-gather comparator reproduces sparse attention bit for bit
+    uout, ulse, ub = omnimem_union_gather_attn(cache, x.q, sel.idx, sel.cnt, G, w.scale)
+    torch.cuda.synchronize()
+    per, tot = oracle.union(host(sel.idx).numpy(), host(sel.cnt).numpy(), n * Bpc)
+    assert int(ub.item()) == tot
+    assert torch.equal(uout.view(torch.int16) if dtype == torch.bfloat16 else uout.view(torch.int32),
+                       out.view(torch.int16) if dtype == torch.bfloat16 else out.view(torch.int32))
+    assert torch.equal(ulse, lse)
+
+
+# ------------------------------------------------------------- edge cases
+
+def test_edge_cases(dev):
+    w = synth.Workload("edge", 2, 128, 200, 150, 64, 4, 4, 5, 50, 1, 1, torch.bfloat16, False, 1, 8)
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, 64, seed=1, pad_value=NAN)
+    say("edge: empty history")
+    sel = run_select(cache, x, w, 0)
+    assert (host(sel.cnt) == 0).all() and (host(sel.idx) == -1).all() and sel.awe_active == 0
+    out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale, num_chunks=0)
+    dout, dlse = omnimem_dense_attn(cache, x.q, 0, 0, w.scale, num_chunks=0)
+    torch.cuda.synchronize()
+    for o, l in ((out, lse), (dout, dlse)):
+        assert (host(o).float() == 0).all() and torch.isneginf(host(l)).all()
+
+    say("edge: K larger than the history")
+    big = synth.Workload("edge", 2, 128, 200, 150, 64, 4, 4, 100, 50, 1, 1, torch.bfloat16, False, 1, 8)
+    sel = run_select(cache, x, big)
+    ref = oracle_select(x, big, 4)
+    assert not ref["awe"] and (host(sel.cnt) == 16).all()
+    check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref)
+    out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, big.group_size, big.scale)
+    dout, dlse = omnimem_dense_attn(cache, x.q, 0, 4, big.scale)
+    torch.cuda.synchronize()
+    # all blocks selected in ascending order: same tiles in the same order as dense
+    assert torch.equal(out.view(torch.int16), dout.view(torch.int16)) and torch.equal(lse, dlse)
+
+    say("edge: caller lists with duplicates, padding inside, out-of-range ids")
+    R = -(-150 // 50)
+    idx = torch.tensor([[[3, 3, -1, 9, 99, 2]] * R] * 2, dtype=torch.int32, device=dev)
+    cnt = torch.full((2, R), 6, dtype=torch.int32, device=dev)
+    out, lse = omnimem_sparse_attn(cache, x.q, idx, cnt, 50, w.scale)
+    ref_idx = np.array([[[3, 3, 9, 2]] * R] * 2, dtype=np.int32)
+    o_ref, l_ref, hs, qs = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), 64, ref_idx, np.full((2, R), 4),
+                                              50, w.scale)
+    attn_check(out, lse, o_ref, l_ref, hs, qs, torch.bfloat16, "caller list")
+
+    say("edge: every block non-resident")
+    cold = synth.page_layer(x.k, x.v, 64, seed=1, nonresident=range(16))
+    sel = run_select(cold, x, w)
+    assert (host(sel.cnt) == 0).all()
+    dout, dlse = omnimem_dense_attn(cold, x.q, 0, 4, w.scale)
+    torch.cuda.synchronize()
+    assert (host(dout).float() == 0).all() and torch.isneginf(host(dlse)).all()
+
+    say("edge: determinism")
+    a1 = run_select(cache, x, w)
+    a2 = run_select(cache, x, w)
+    assert torch.equal(a1.idx, a2.idx) and torch.equal(a1.score, a2.score)
+    o1, l1 = omnimem_sparse_attn(cache, x.q, a1.idx, a1.cnt, w.group_size, w.scale)
+    o2, l2 = omnimem_sparse_attn(cache, x.q, a1.idx, a1.cnt, w.group_size, w.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+
+
+# ------------------------------------------------------------ full-size workloads
+
+def planted_recall(sel, x, w, n):
+    """Planted relevance must be found: Rel[h,r] & Omega is selected whenever it fits in K."""
+    rel = x.rel.relevant[:, :, : n * w.blocks_per_chunk].cpu().numpy()
+    idx = host(sel.idx).numpy()
+    Bpc = w.blocks_per_chunk
+    missed = 0
+    for h in range(w.heads):
+        for r in range(w.groups):
+            want = set(np.nonzero(rel[h, r])[0].tolist())
+            if sel.awe_active:
+                want = {b for b in want if b < (n - w.window_chunks) * Bpc}
+            if len(want) <= w.top_k:
+                missed += len(want - set(idx[h, r].tolist()))
+    return missed
+
+
+def test_wan13b_n20(dev):
+    w = synth.WORKLOADS["wan1.3b_n20"]
+    say("wan1.3b_n20: generate")
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=21, pad_value=NAN)
+    sel = run_select(cache, x, w)
+    say("wan1.3b_n20: oracle select (all heads)")
+    ref = oracle_select(x, w, w.history_chunks)
+    assert sel.awe_active == 1
+    ties = check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref)
+    say(f"  selection matches ({ties} near-tie rows)")
+    assert planted_recall(sel, x, w, w.history_chunks) == 0
+    out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale)
+    hs, qs = sample_rows(w.heads, w.query_tokens, 384, 1)
+    o_ref, l_ref, _, _ = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), w.block_size, ref["idx"], ref["cnt"],
+                                            w.group_size, w.scale, hs=hs, qs=qs)
+    attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, "sparse (384 sampled rows)")
+    dout, dlse = omnimem_dense_attn(cache, x.q, 0, w.history_chunks, w.scale)
+    hs, qs = sample_rows(w.heads, w.query_tokens, 32, 2)
+    d_ref, dl_ref, _, _ = oracle.dense_attn(host(x.q), host(x.k), host(x.v), w.block_size, 0, w.history_chunks,
+                                            w.scale, hs=hs, qs=qs)
+    attn_check(dout, dlse, d_ref, dl_ref, hs, qs, w.dtype, "dense (32 sampled rows)")
+
+
+def test_wan13b_long_sweep(dev):
+    w = synth.WORKLOADS["wan1.3b_long"]
+    say("wan1.3b_long: generate 120 chunks")
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=31, pad_value=NAN)
+    heads = (0, 3)
+    for n in (10, 30, 60, 120):
+        say(f"wan1.3b_long n={n}")
+        xn = synth.LayerInputs(synth.queries(w, 0, n, x.rel, dev), x.k, x.v, x.rel)
+        sel = run_select(cache, xn, w, n)
+        ref = oracle_select(xn, w, n, heads=heads)
+        check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref, heads=range(*heads))
+        assert sel.awe_active == 1 and planted_recall(sel, xn, w, n) == 0
+        out, lse = omnimem_sparse_attn(cache, xn.q, sel.idx, sel.cnt, w.group_size, w.scale, num_chunks=n)
+        hs, qs = sample_rows(heads[1], w.query_tokens, 64, n)
+        o_ref, l_ref, _, _ = oracle.sparse_attn(host(xn.q), host(x.k[:n]), host(x.v[:n]), w.block_size, ref["idx"],
+                                                ref["cnt"], w.group_size, w.scale, hs=hs, qs=qs)
+        attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, f"sparse n={n}")
+        if n in (10, 120):
+            dout, dlse = omnimem_dense_attn(cache, xn.q, 0, n, w.scale, num_chunks=n)
+            hs, qs = sample_rows(w.heads, w.query_tokens, 8, n + 1)
+            d_ref, dl_ref, _, _ = oracle.dense_attn(host(xn.q), host(x.k[:n]), host(x.v[:n]), w.block_size, 0, n,
+                                                    w.scale, hs=hs, qs=qs)
+            attn_check(dout, dlse, d_ref, dl_ref, hs, qs, w.dtype, f"dense n={n}")
+
+
+def test_wan13b_30layer_ramp_sampled(dev):
+    w = synth.WORKLOADS["wan1.3b_30layer"]
+    for layer in (0, 29):
+        say(f"wan1.3b_30layer layer={layer}: generate 60 chunks")
+        x = synth.make_layer(w, layer, device=dev)
+        cache = synth.page_layer(x.k, x.v, w.block_size, seed=100 + layer, pad_value=NAN)
+        for n in (1, 2, 3, 4, 5, 30, 60):
+            say(f"  layer={layer} n={n}")
+            xn = synth.LayerInputs(synth.queries(w, layer, n, x.rel, dev), x.k, x.v, x.rel)
+            sel = run_select(cache, xn, w, n)
+            assert sel.awe_active == int(n >= 4)
+            ref = oracle_select(xn, w, n, heads=(0, 4))
+            check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref, heads=range(4))
+            idx = host(sel.idx).numpy()
+            win0 = (n - w.window_chunks) * w.blocks_per_chunk
+            if sel.awe_active:
+                assert (idx < win0).all()
+            if n in (4, 60):
+                out, lse = omnimem_sparse_attn(cache, xn.q, sel.idx, sel.cnt, w.group_size, w.scale, num_chunks=n)
+                hs, qs = sample_rows(4, w.query_tokens, 64, n)
+                o_ref, l_ref, _, _ = oracle.sparse_attn(host(xn.q), host(x.k[:n]), host(x.v[:n]), w.block_size,
+                                                        ref["idx"], ref["cnt"], w.group_size, w.scale, hs=hs, qs=qs)
+                attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, f"sparse layer={layer} n={n}")
+        del x, cache
+        torch.cuda.empty_cache()
+
+
+def test_wan14b_stress(dev):
+    w = synth.WORKLOADS["wan14b_stress"]
+    say("wan14b_stress: generate 60 chunks x 40 heads")
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=51, pad_value=NAN)
+    sel = run_select(cache, x, w)
+    heads = (0, 3)
+    say("wan14b_stress: oracle select on 3 heads")
+    ref = oracle_select(x, w, w.history_chunks, heads=heads)
+    check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref, heads=range(*heads))
+    assert planted_recall(sel, x, w, w.history_chunks) == 0
+    out, lse = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale)
+    hs, qs = sample_rows(3, w.query_tokens, 96, 5)
+    o_ref, l_ref, _, _ = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), w.block_size, ref["idx"], ref["cnt"],
+                                            w.group_size, w.scale, hs=hs, qs=qs)
+    attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, "sparse (96 sampled rows)")
+    say("wan14b_stress: union gather")
+    uout, ulse, ub = omnimem_union_gather_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale)
+    torch.cuda.synchronize()
+    nb = w.history_chunks * w.blocks_per_chunk
+    per, tot = oracle.union(host(sel.idx).numpy(), host(sel.cnt).numpy(), nb)
+    omega = nb - w.window_chunks * w.blocks_per_chunk
+    say(f"  union {tot} of {omega} candidate blocks ({100.0 * tot / omega:.1f}%), sum_h |U_h| = {int(per.sum())}")
+    assert int(ub.item()) == tot and tot > 0.8 * omega
+    assert torch.equal(uout.view(torch.int16), out.view(torch.int16)) and torch.equal(ulse, lse)
