@@ -1,0 +1,340 @@
+"""Benchmark of OmniMem's memory-retrieval attention step on one MI355X.
+
+A step = one chunk-layer: omnimem_select (query-shared top-K with Adaptive
+Window Exclusion over the whole history) followed by omnimem_sparse_attn (per-head
+scattered block-sparse attention), on the Wan2.1-1.3B-shaped layer: 12 heads x
+128, a 4680-token chunk, 20 chunks of history (93,600 cached keys), 64-token
+blocks, K = 64, one query group, 1-chunk window.  Four independent layer caches
+(2.3 GB of K+V) are used in rotation, so no step finds its cache in the 256 MB
+Infinity Cache.  Inputs are resident in HBM before the timed region.
+
+Prints ONE JSON line: value = effective TFLOP/s of select + sparse attention
+(attention flops over the valid selected keys + scoring flops, per step time),
+ms_per_step = ms per chunk-layer, a roofline object for the dominant kernel
+(measured with HIP events on the launch stream), the CPU oracle's throughput on
+a bounded sample of the same workload, per-stage times, and a sweep over history
+length (10/30/60/120 chunks) with the speedup over in-build dense attention.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ms per chunk-layer + effective TFLOP/s of select+sparse-attn vs history length"
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_HBM_GBS = 8000.0
+WORKLOAD = "wan1.3b_n20"
+ROTATE_LAYERS = 4
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=40)
+    p.add_argument("--warmup", type=int, default=8)
+    p.add_argument("--no-sweep", action="store_true", help="skip the history-length sweep")
+    p.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
+    p.add_argument("--stress", action="store_true", help="add the 14B-shaped union-gather comparison")
+    return p.parse_args()
+
+
+def attn_flops(idx, cnt, w, n_chunks):
+    """4 * d * sum over (head, query row) of the valid keys in its selected blocks."""
+    import torch
+    Bpc, B, S = w.blocks_per_chunk, w.block_size, w.chunk_tokens
+    o = torch.remainder(idx.long(), Bpc)
+    valid = torch.where(o == Bpc - 1, S - o * B, torch.full_like(o, B))
+    K = idx.shape[-1]
+    keep = (torch.arange(K, device=idx.device)[None, None, :] < cnt[..., None].long()) & (idx >= 0)
+    keys = (valid * keep).sum(-1)                                  # [H, R]
+    rows = torch.tensor([min(w.group_size, w.query_tokens - r * w.group_size) for r in range(idx.shape[1])],
+                        device=idx.device)
+    return float(4 * w.head_dim * (keys * rows[None, :]).sum().item())
+
+
+def select_bytes(w, n_chunks, awe):
+    """Algorithmic HBM bytes of select: every candidate K block once (valid tokens), plus Q."""
+    eb = 2
+    Bpc = w.blocks_per_chunk
+    cand_chunks = n_chunks - w.window_chunks if awe else n_chunks
+    return cand_chunks * w.chunk_tokens * w.heads * w.head_dim * eb + w.query_tokens * w.heads * w.head_dim * eb
+
+
+def score_flops(w, n_chunks):
+    return 2.0 * w.groups * n_chunks * w.blocks_per_chunk * w.heads * w.head_dim
+
+
+def source_digest(path):
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def load_traffic(kernel):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if the kernel
+    source has not changed since they were taken; else None."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        rec = json.load(f)
+    src = os.path.join(ROOT, "paper_2605_30519_amd", "csrc", rec.get("source", ""))
+    if not os.path.exists(src) or source_digest(src) != rec.get("source_sha256"):
+        return None
+    return rec.get("bytes_per_launch")
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import (lib, omnimem_dense_attn, omnimem_select, omnimem_select_workspace_bytes,
+                                      omnimem_sparse_attn, omnimem_union_gather_attn, select_params, synth)
+    from paper_2605_30519_amd.omnimem import Selection, workspace_tensor
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lib()
+    w = synth.WORKLOADS[WORKLOAD]
+    n = w.history_chunks
+    H, R, K = w.heads, w.groups, w.top_k
+
+    # ---------------------------------------------------------------- inputs
+    log(f"generating {ROTATE_LAYERS} layer caches of {n} chunks")
+    layers = []
+    for layer in range(ROTATE_LAYERS):
+        x = synth.make_layer(w, layer, device=dev)
+        cache = synth.page_layer(x.k, x.v, w.block_size, seed=1000 + layer)
+        layers.append((x.q, cache))
+        if layer == 0:
+            x0 = x
+        else:
+            del x
+    params = select_params(K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    ws = workspace_tensor(omnimem_select_workspace_bytes(layers[0][1], w.query_tokens, params), dev)
+    sels = [Selection(torch.empty((H, R, K), dtype=torch.int32, device=dev),
+                      torch.empty((H, R), dtype=torch.int32, device=dev), None, 0) for _ in layers]
+    outs = [torch.empty_like(q) for q, _ in layers]
+    lses = [torch.empty((H, w.query_tokens), dtype=torch.float32, device=dev) for _ in layers]
+    torch.cuda.synchronize()
+
+    def step(i, ev=None):
+        q, cache = layers[i % ROTATE_LAYERS]
+        s = sels[i % ROTATE_LAYERS]
+        if ev is not None:
+            ev[0].record()
+        omnimem_select(cache, q, K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                       workspace=ws, out=s, want_score=False)
+        if ev is not None:
+            ev[1].record()
+        omnimem_sparse_attn(cache, q, s.idx, s.cnt, w.group_size, w.scale, out=outs[i % ROTATE_LAYERS],
+                            lse=lses[i % ROTATE_LAYERS])
+        if ev is not None:
+            ev[2].record()
+
+    log(f"warmup {args.warmup} steps, then {args.steps} timed steps")
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    flops_per_layer = [attn_flops(s.idx, s.cnt, w, n) for s in sels]
+    awe = sels[0].awe_active
+
+    # ---------------------------------------------------------------- timed region
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(args.steps):
+        step(i, evs[i])
+    t_end.record()
+    torch.cuda.synchronize()
+    total_ms = t_start.elapsed_time(t_end)
+    ms_per_step = total_ms / args.steps
+    sel_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
+    att_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
+    flops_steps = np.array([flops_per_layer[i % ROTATE_LAYERS] for i in range(args.steps)])
+    sflops = score_flops(w, n)
+    eff_tflops = float((flops_steps.sum() + sflops * args.steps) / (total_ms * 1e-3) / 1e12)
+
+    attn_tflops = float(flops_steps.mean() / (att_ms.mean() * 1e-3) / 1e12)
+    sbytes = select_bytes(w, n, awe)
+    sel_gbs = float(sbytes / (sel_ms.mean() * 1e-3) / 1e9)
+    attn_roof = {"kernel": "k_attn_bf16", "bound": "mfma", "achieved": round(attn_tflops, 2),
+                 "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                 "traffic": load_traffic("k_attn_bf16"),
+                 "per_launch": {"flops": flops_steps.mean(), "avg_ms": round(float(att_ms.mean()), 4)}}
+    sel_roof = {"kernel": "select (k_qmean_partial+k_qmean_final+k_pool_score+k_topk)", "bound": "hbm",
+                "achieved": round(sel_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(sel_gbs / PEAK_HBM_GBS, 4), "traffic": load_traffic("k_pool_score"),
+                "per_launch": {"bytes": sbytes, "avg_ms": round(float(sel_ms.mean()), 4)}}
+    dominant = attn_roof if att_ms.mean() >= sel_ms.mean() else sel_roof
+
+    result = {
+        "metric": METRIC,
+        "value": round(eff_tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "Wan2.1-1.3B-shaped attention layer: 12 heads x 128, 4680-token chunk, "
+                               "20-chunk history (93,600 keys) in 64-token blocks, top-64 per head, one query "
+                               "group, 1-chunk excluded window",
+                   "history_chunks": n, "heads": H, "head_dim": w.head_dim, "query_tokens": w.query_tokens,
+                   "block_size": w.block_size, "top_k": K, "group_size": w.group_size,
+                   "rotated_layer_caches": ROTATE_LAYERS},
+        "roofline": dominant,
+        "stages": {"select_ms": round(float(np.median(sel_ms)), 4),
+                   "sparse_attn_ms": round(float(np.median(att_ms)), 4),
+                   "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe},
+    }
+
+    # ---------------------------------------------------------------- sweep
+    if not args.no_sweep:
+        wl = synth.WORKLOADS["wan1.3b_long"]
+        log("history sweep 10/30/60/120 chunks (generating 120 chunks)")
+        del layers, sels, outs, lses
+        torch.cuda.empty_cache()
+        xl = synth.make_layer(wl, 0, device=dev)
+        cl = synth.page_layer(xl.k, xl.v, wl.block_size, seed=77)
+        del xl.k, xl.v
+        wsl = workspace_tensor(omnimem_select_workspace_bytes(cl, wl.query_tokens, params), dev)
+        sweep = []
+        for hn in (10, 30, 60, 120):
+            q = synth.queries(wl, 0, hn, xl.rel, dev)
+            s = Selection(torch.empty((H, R, K), dtype=torch.int32, device=dev),
+                          torch.empty((H, R), dtype=torch.int32, device=dev), None, 0)
+            out = torch.empty_like(q)
+            ls = torch.empty((H, wl.query_tokens), dtype=torch.float32, device=dev)
+            reps = 5
+            e = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps + 1)]
+            for r in range(reps + 1):
+                e[r][0].record()
+                omnimem_select(cl, q, K, wl.group_size, wl.window_chunks, wl.awe_min_outside_chunks, wl.scale,
+                               num_chunks=hn, workspace=wsl, out=s, want_score=False)
+                e[r][1].record()
+                omnimem_sparse_attn(cl, q, s.idx, s.cnt, wl.group_size, wl.scale, num_chunks=hn, out=out, lse=ls)
+                e[r][2].record()
+                omnimem_dense_attn(cl, q, 0, hn, wl.scale, num_chunks=hn, out=out, lse=ls)
+                e[r][3].record()
+            torch.cuda.synchronize()
+            ts = np.median([e[r][0].elapsed_time(e[r][1]) for r in range(1, reps + 1)])
+            ta = np.median([e[r][1].elapsed_time(e[r][2]) for r in range(1, reps + 1)])
+            td = np.median([e[r][2].elapsed_time(e[r][3]) for r in range(1, reps + 1)])
+            fl = attn_flops(s.idx, s.cnt, wl, hn)
+            dense_fl = 4.0 * wl.head_dim * wl.heads * wl.query_tokens * hn * wl.chunk_tokens
+            sweep.append({"history_chunks": hn, "cached_keys": hn * wl.chunk_tokens,
+                          "select_ms": round(float(ts), 4), "sparse_attn_ms": round(float(ta), 4),
+                          "ms_per_chunk_layer": round(float(ts + ta), 4),
+                          "effective_tflops": round((fl + score_flops(wl, hn)) / ((ts + ta) * 1e-3) / 1e12, 2),
+                          "select_gbs": round(select_bytes(wl, hn, s.awe_active) / (ts * 1e-3) / 1e9, 1),
+                          "sparse_attn_tflops": round(fl / (ta * 1e-3) / 1e12, 2),
+                          "dense_ms": round(float(td), 4),
+                          "dense_tflops": round(dense_fl / (td * 1e-3) / 1e12, 2),
+                          "speedup_vs_dense": round(float(td / (ts + ta)), 2)})
+        result["sweep"] = sweep
+        del cl
+
+    # ---------------------------------------------------------------- 14B comparator
+    if args.stress:
+        log("14B-shaped union-gather comparison")
+        result["stress"] = stress_comparison(dev)
+
+    # ---------------------------------------------------------------- CPU oracle
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a bounded sample")
+        result["cpu_baseline"] = cpu_baseline(x0, w, flops_per_layer[0] + sflops)
+
+    print(json.dumps(result), flush=True)
+
+
+def stress_comparison(dev):
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select, omnimem_sparse_attn, omnimem_union_gather_attn, synth
+    from paper_2605_30519_amd.omnimem import omnimem_union_workspace_bytes, workspace_tensor
+    w = synth.WORKLOADS["wan14b_stress"]
+    x = synth.make_layer(w, 0, device=dev)
+    c = synth.page_layer(x.k, x.v, w.block_size, seed=55)
+    del x.k, x.v
+    uws = workspace_tensor(omnimem_union_workspace_bytes(c), dev)
+    reps = 5
+    e = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(reps + 1)]
+    for r in range(reps + 1):
+        e[r][0].record()
+        s = omnimem_select(c, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+        e[r][1].record()
+        out, lse = omnimem_sparse_attn(c, x.q, s.idx, s.cnt, w.group_size, w.scale)
+        e[r][2].record()
+        uo, ul, ub = omnimem_union_gather_attn(c, x.q, s.idx, s.cnt, w.group_size, w.scale, workspace=uws)
+        e[r][3].record()
+    torch.cuda.synchronize()
+    med = lambda a, b: float(np.median([e[r][a].elapsed_time(e[r][b]) for r in range(1, reps + 1)]))
+    nb = w.history_chunks * w.blocks_per_chunk
+    U = int(ub.item())
+    idx = s.idx.cpu().numpy()
+    per_head = [len(set(idx[h][idx[h] >= 0].tolist())) for h in range(w.heads)]
+    slab = w.block_size * w.head_dim * 2 * 2
+    return {"workload": "Wan2.1-14B-shaped layer: 40 heads x 128, B=128, K=32, 3 query groups, 60 chunks",
+            "select_ms": round(med(0, 1), 4), "scattered_attn_ms": round(med(1, 2), 4),
+            "union_gather_attn_ms": round(med(2, 3), 4),
+            "union_blocks": U, "candidate_blocks": nb - w.window_chunks * w.blocks_per_chunk,
+            "union_fraction": round(U / (nb - w.window_chunks * w.blocks_per_chunk), 4),
+            "scattered_kv_bytes": int(sum(per_head)) * slab, "merged_buffer_bytes": w.heads * U * slab,
+            "outputs_bit_equal": bool(torch.equal(uo.view(torch.int16), out.view(torch.int16)))}
+
+
+def cpu_baseline(x, w, step_flops, reps=3):
+    """The fp64 oracle on the host cores: one whole chunk-layer (selection over the
+    full history for every head, then selection attention for every query row of
+    every head), repeated `reps` times; the median time is reported."""
+    import numpy as np
+
+    import oracle
+
+    q, k, v = x.q.cpu(), x.k.cpu(), x.v.cpu()
+    oracle.lib()
+    hh, qq = np.meshgrid(np.arange(w.heads), np.arange(w.query_tokens), indexing="ij")
+    times, sel_t = [], []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        ref = oracle.select(q, k, w.block_size, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks,
+                            w.scale)
+        t1 = time.perf_counter()
+        oracle.sparse_attn(q, k, v, w.block_size, ref["idx"], ref["cnt"], w.group_size, w.scale, hs=hh.ravel(),
+                           qs=qq.ravel())
+        t2 = time.perf_counter()
+        times.append(t2 - t0)
+        sel_t.append(t1 - t0)
+    full_s = float(np.median(times))
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": round(step_flops / full_s / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": f"one whole chunk-layer of the same workload (selection for all {w.heads} heads over the "
+                      f"20-chunk history + selection attention for all {w.heads * w.query_tokens} (head, row) "
+                      f"pairs), fp64, median of {reps} runs, {sum(times):.1f} s in total",
+            "ms_per_chunk_layer": round(full_s * 1e3, 1), "select_s": round(float(np.median(sel_t)), 3)}
+
+
+if __name__ == "__main__":
+    main()
