@@ -118,23 +118,38 @@ __device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const in
 
 // ------------------------------------------------------------------ bf16 / MFMA
 constexpr int kTileKeys = 64;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;  // 256 query rows per workgroup, two waves per SIMD
 
 // A-operand row order for S^T = K Q^T: swapping bits 2 and 3 of the row makes the
 // accumulator element i of lane l hold key 8*(l/32)+i (i < 8) or 16+8*(l/32)+(i-8).
 __device__ __forceinline__ int s_row_perm(int x) { return (x & ~12) | ((x & 4) << 1) | ((x & 8) >> 1); }
 
+// LDS row strides (bf16 elements), chosen for gfx950's 64 four-byte banks:
+//  K rows are read 16 B per lane, 16 lanes (16 rows) per pass: a stride of 4 (mod 64)
+//    dwords puts the 16 rows on disjoint bank quads;
+//  V rows are read by ds_read_b64_tr_b16, 4 rows x 32 B per 16-lane group and two
+//    groups per pass: a stride of 16 or 48 (mod 64) dwords makes the 8 row segments of a
+//    pass disjoint.
+template <int D>
+struct AttnLds {
+  static constexpr int K_STRIDE = D == 128 ? 136 : 72;
+  static constexpr int V_STRIDE = D == 128 ? 160 : 96;
+  static constexpr int K_ELEMS = kTileKeys * K_STRIDE;
+  static constexpr int V_ELEMS = kTileKeys * V_STRIDE;
+  static constexpr int BUF_ELEMS = K_ELEMS + V_ELEMS;
+};
+
 template <int D>
 __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
+  using L = AttnLds<D>;
+  constexpr int NT = kWaves * kWave;
   constexpr int ROWS = kWaves * 32;
-  constexpr int LDS_STRIDE = D + 8;                 // bf16 elements per LDS row (pad against bank conflicts)
-  constexpr int CHUNKS_PER_ROW = D / 8;             // 16-byte chunks per key row
-  constexpr int CPT = kTileKeys * CHUNKS_PER_ROW / (kWaves * kWave);  // chunks per thread per tile
-  constexpr int DT = D / 32;                        // 32-wide output tiles along d
-  constexpr int KK = D / 16;                        // k-steps of QK^T
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kTileKeys * LDS_STRIDE];
-  uint16_t* k_lds = lds;
-  uint16_t* v_lds = lds + kTileKeys * LDS_STRIDE;
+  constexpr int CHUNKS_PER_ROW = D / 8;                        // 16-byte chunks per key row
+  constexpr int CPT = kTileKeys * CHUNKS_PER_ROW / NT;         // chunks per thread per tile (K and V each)
+  constexpr int DT = D / 32;                                   // 32-wide output tiles along d
+  constexpr int KK = D / 16;                                   // k-steps of QK^T
+  static_assert(CPT >= 1, "tile too small for the workgroup");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * L::BUF_ELEMS];
 
   int h, hr, row0, row_end;
   resolve_tile(a, ROWS, h, hr, row0, row_end);
@@ -151,6 +166,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
 
   // Q^T as the B operand: lane holds query (lane % 32), d = 16*kk + 8*half + 0..7
   const int my_row = row0 + wave * 32 + lane % 32;
+  const bool wave_live = row0 + wave * 32 < row_end;  // wave-uniform
   bf16x8 qreg[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
@@ -165,6 +181,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
     for (int i = 0; i < 16; ++i) o_acc[dt][i] = 0.f;
+  // running max (raw score units) and this lane's share of the denominator
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale * kLog2e;
 
@@ -175,7 +192,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
     const uint16_t* vs = vp + walk.slab_offset(h, D);
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int cid = tid + i * kWaves * kWave;
+      const int cid = tid + i * NT;
       const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
       if (row < walk.nvalid) {
         kreg[i] = *reinterpret_cast<const uint4*>(ks + row * D + c8 * 8);
@@ -186,93 +203,116 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       }
     }
   };
-
-  bool have = walk.seek();
-  if (have) prefetch();
-  const int krow = s_row_perm(lane % 32);
-  while (have) {
+  auto stage = [&](uint16_t* buf) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const int cid = tid + i * kWaves * kWave;
+      const int cid = tid + i * NT;
       const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
-      *reinterpret_cast<uint4*>(k_lds + row * LDS_STRIDE + c8 * 8) = kreg[i];
-      *reinterpret_cast<uint4*>(v_lds + row * LDS_STRIDE + c8 * 8) = vreg[i];
+      *reinterpret_cast<uint4*>(buf + row * L::K_STRIDE + c8 * 8) = kreg[i];
+      *reinterpret_cast<uint4*>(buf + L::K_ELEMS + row * L::V_STRIDE + c8 * 8) = vreg[i];
     }
-    const int nvalid = walk.nvalid;
-    __syncthreads();
+  };
+
+  bool have = walk.seek();
+  int nvalid = walk.nvalid;
+  if (have) {
+    prefetch();
+    stage(lds);
+  }
+  __syncthreads();
+  const int krow = s_row_perm(lane % 32);
+  int cur = 0;
+  while (have) {
+    const int cur_nvalid = nvalid;
     walk.advance();
     have = walk.seek();
-    if (have) prefetch();
+    nvalid = walk.nvalid;
+    if (have) prefetch();  // next tile: global loads in flight during this tile's math
+    const uint16_t* k_lds = lds + cur * L::BUF_ELEMS;
+    const uint16_t* v_lds = k_lds + L::K_ELEMS;
 
-    // ---- S^T = K Q^T for keys [0, 64): two 32-key accumulators
-    f32x16 s_acc[2];
+    if (wave_live) {
+      // ---- S^T = K Q^T for keys [0, 64): two 32-key accumulators
+      f32x16 s_acc[2];
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2) {
+      for (int t2 = 0; t2 < 2; ++t2) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s_acc[t2][i] = 0.f;
+        for (int i = 0; i < 16; ++i) s_acc[t2][i] = 0.f;
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) {
-        const bf16x8 kf =
-            *reinterpret_cast<const bf16x8*>(k_lds + (32 * t2 + krow) * LDS_STRIDE + 16 * kk + 8 * half);
-        s_acc[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qreg[kk], s_acc[t2], 0, 0, 0);
+        for (int kk = 0; kk < KK; ++kk) {
+          const bf16x8 kf =
+              *reinterpret_cast<const bf16x8*>(k_lds + (32 * t2 + krow) * L::K_STRIDE + 16 * kk + 8 * half);
+          s_acc[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qreg[kk], s_acc[t2], 0, 0, 0);
+        }
+      }
+      // ---- online softmax for this lane's query (exp2 domain, scale folded into one FMA)
+      if (cur_nvalid < kTileKeys) {  // partial tile: mask the keys past the block's end
+#pragma unroll
+        for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
+            if (key >= cur_nvalid) s_acc[t2][i] = -INFINITY;
+          }
+      }
+      float mloc = s_acc[0][0];
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s_acc[t2][i]);
+      const float m_tile = fmaxf(mloc, __shfl_xor(mloc, 32));
+      // rescale only when some lane's running max grows (exact: alpha == 1 otherwise)
+      if (__any(m_tile > m_run)) {
+        const float m_new = fmaxf(m_run, m_tile);
+        const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
+        l_run *= alpha;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) o_acc[dt][i] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = m_run == -INFINITY ? 0.f : m_run * c;
+      float psum = 0.f;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float p = __builtin_amdgcn_exp2f(fmaf(s_acc[t2][i], c, -mc));
+          psum += p;
+          pb[2 * t2 + i / 8][i % 8] = static_cast<__bf16>(p);
+        }
+      l_run += psum;
+
+      // ---- O^T += V^T P^T: 4 key steps of 16
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
+          typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+          const i16x4 lo =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * L::V_STRIDE + col));
+          const i16x4 hi =
+              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * L::V_STRIDE + col));
+          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+          o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
+        }
       }
     }
-
-    // ---- online softmax for this lane's query (exp2 domain)
-    float x[2][16];
-    float mloc = -INFINITY;
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
-        const float v = key < nvalid ? s_acc[t2][i] * c : -INFINITY;
-        x[t2][i] = v;
-        mloc = fmaxf(mloc, v);
-      }
-    const float m_tile = fmaxf(mloc, __shfl_xor(mloc, 32));
-    const float m_new = fmaxf(m_run, m_tile);
-    const float m_use = m_new == -INFINITY ? 0.f : m_new;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_use);
-    float psum = 0.f;
-    bf16x8 pb[4];
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(x[t2][i] - m_use);
-        psum += p;
-        pb[2 * t2 + i / 8][i % 8] = static_cast<__bf16>(p);
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o_acc[dt][i] *= alpha;
-
-    // ---- O^T += V^T P^T: 4 key steps of 16
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
-        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * LDS_STRIDE + col));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * LDS_STRIDE + col));
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-        o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
-      }
-    }
+    if (have) stage(lds + (cur ^ 1) * L::BUF_ELEMS);  // the other buffer: last read one tile ago
     __syncthreads();
+    cur ^= 1;
   }
 
   // ---- epilogue: normalise, stage O through LDS, store rows with 16-byte writes
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   constexpr int SSTRIDE = D + 8;
-  uint16_t* stage = lds + wave * 32 * SSTRIDE;
+  static_assert(kWaves * 32 * SSTRIDE <= 2 * L::BUF_ELEMS, "output staging does not fit");
+  uint16_t* stage_o = lds + wave * 32 * SSTRIDE;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
@@ -281,7 +321,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       bf16x4 w;
 #pragma unroll
       for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(o_acc[dt][4 * i4 + e] * inv);
-      *reinterpret_cast<bf16x4*>(stage + (lane % 32) * SSTRIDE + d0) = w;
+      *reinterpret_cast<bf16x4*>(stage_o + (lane % 32) * SSTRIDE + d0) = w;
     }
   __syncthreads();
   uint16_t* op = static_cast<uint16_t*>(a.out);
@@ -293,10 +333,11 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
     const int qrow = row0 + wave * 32 + row;
     if (qrow < row_end)
       *reinterpret_cast<uint4*>(op + (static_cast<int64_t>(qrow) * a.H + h) * D + c8 * 8) =
-          *reinterpret_cast<const uint4*>(stage + row * SSTRIDE + c8 * 8);
+          *reinterpret_cast<const uint4*>(stage_o + row * SSTRIDE + c8 * 8);
   }
   if (a.lse && lane < 32 && my_row < row_end)
-    a.lse[static_cast<int64_t>(h) * a.lq + my_row] = l_tot > 0.f ? (m_run + __log2f(l_tot)) * kLn2 : -INFINITY;
+    a.lse[static_cast<int64_t>(h) * a.lq + my_row] =
+        l_tot > 0.f ? (m_run * c + __log2f(l_tot)) * kLn2 : -INFINITY;
 }
 
 // ------------------------------------------------------------------ fp32 / SIMT
