@@ -136,7 +136,9 @@ struct AttnLds {
   static constexpr int V_STRIDE = D == 128 ? 160 : 96;
   static constexpr int K_ELEMS = kTileKeys * K_STRIDE;
   static constexpr int V_ELEMS = kTileKeys * V_STRIDE;
-  static constexpr int BUF_ELEMS = K_ELEMS + V_ELEMS;
+  static constexpr int K_STAGES = 2;
+  static constexpr int V_STAGES = 3;  // the phase-shifted waves still read the previous tile's V
+  static constexpr int TOTAL_ELEMS = K_STAGES * K_ELEMS + V_STAGES * V_ELEMS;
 };
 
 template <int D>
@@ -149,7 +151,9 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   constexpr int DT = D / 32;                                   // 32-wide output tiles along d
   constexpr int KK = D / 16;                                   // k-steps of QK^T
   static_assert(CPT >= 1, "tile too small for the workgroup");
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * L::BUF_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t lds[L::TOTAL_ELEMS];
+  uint16_t* const k_ring = lds;
+  uint16_t* const v_ring = lds + L::K_STAGES * L::K_ELEMS;
 
   int h, hr, row0, row_end;
   resolve_tile(a, ROWS, h, hr, row0, row_end);
@@ -203,13 +207,35 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       }
     }
   };
-  auto stage = [&](uint16_t* buf) {
+  auto stage = [&](int kst, int vst) {
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int cid = tid + i * NT;
       const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
-      *reinterpret_cast<uint4*>(buf + row * L::K_STRIDE + c8 * 8) = kreg[i];
-      *reinterpret_cast<uint4*>(buf + L::K_ELEMS + row * L::V_STRIDE + c8 * 8) = vreg[i];
+      *reinterpret_cast<uint4*>(k_ring + kst * L::K_ELEMS + row * L::K_STRIDE + c8 * 8) = kreg[i];
+      *reinterpret_cast<uint4*>(v_ring + vst * L::V_ELEMS + row * L::V_STRIDE + c8 * 8) = vreg[i];
+    }
+  };
+
+  // The two waves that share a SIMD (w and w + 4) run the same tile half a step
+  // apart: waves 0-3 do QK(t), softmax(t), PV(t); waves 4-7 do PV(t-1), QK(t),
+  // softmax(t).  While one of them is in its softmax (VALU) the other issues MFMAs.
+  const bool late = wave >= kWaves / 2;
+  bf16x8 pb[4];
+  auto pv = [&](const uint16_t* v_lds) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * L::V_STRIDE + col));
+        const i16x4 hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * L::V_STRIDE + col));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
+      }
     }
   };
 
@@ -217,21 +243,22 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   int nvalid = walk.nvalid;
   if (have) {
     prefetch();
-    stage(lds);
+    stage(0, 0);
   }
   __syncthreads();
   const int krow = s_row_perm(lane % 32);
-  int cur = 0;
+  int t = 0;
   while (have) {
     const int cur_nvalid = nvalid;
     walk.advance();
     have = walk.seek();
     nvalid = walk.nvalid;
     if (have) prefetch();  // next tile: global loads in flight during this tile's math
-    const uint16_t* k_lds = lds + cur * L::BUF_ELEMS;
-    const uint16_t* v_lds = k_lds + L::K_ELEMS;
+    const uint16_t* k_lds = k_ring + (t % 2) * L::K_ELEMS;
+    const uint16_t* v_lds = v_ring + (t % 3) * L::V_ELEMS;
 
     if (wave_live) {
+      if (late && t > 0) pv(v_ring + ((t + 2) % 3) * L::V_ELEMS);  // PV of the previous tile
       // ---- S^T = K Q^T for keys [0, 64): two 32-key accumulators
       f32x16 s_acc[2];
 #pragma unroll
@@ -274,7 +301,6 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       }
       const float mc = m_run == -INFINITY ? 0.f : m_run * c;
       float psum = 0.f;
-      bf16x8 pb[4];
 #pragma unroll
       for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
@@ -284,34 +310,20 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
           pb[2 * t2 + i / 8][i % 8] = static_cast<__bf16>(p);
         }
       l_run += psum;
-
-      // ---- O^T += V^T P^T: 4 key steps of 16
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
-#pragma unroll
-        for (int dt = 0; dt < DT; ++dt) {
-          const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
-          typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-          const i16x4 lo =
-              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * L::V_STRIDE + col));
-          const i16x4 hi =
-              __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * L::V_STRIDE + col));
-          const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-          o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
-        }
-      }
+      if (!late) pv(v_lds);
     }
-    if (have) stage(lds + (cur ^ 1) * L::BUF_ELEMS);  // the other buffer: last read one tile ago
+    if (have) stage((t + 1) % 2, (t + 1) % 3);  // stages not read in this step
     __syncthreads();
-    cur ^= 1;
+    ++t;
   }
+  if (late && wave_live && t > 0) pv(v_ring + ((t + 2) % 3) * L::V_ELEMS);  // the last tile's PV
+  __syncthreads();  // the rings are reused below for the output
 
   // ---- epilogue: normalise, stage O through LDS, store rows with 16-byte writes
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   constexpr int SSTRIDE = D + 8;
-  static_assert(kWaves * 32 * SSTRIDE <= 2 * L::BUF_ELEMS, "output staging does not fit");
+  static_assert(kWaves * 32 * SSTRIDE <= L::TOTAL_ELEMS, "output staging does not fit");
   uint16_t* stage_o = lds + wave * 32 * SSTRIDE;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
