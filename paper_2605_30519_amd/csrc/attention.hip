@@ -28,6 +28,7 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr int kTileKeys = 64;  // keys per attention tile (one B = 64 block, half of a B = 128 block)
 
 struct AttnArgs {
   const void* q;
@@ -116,8 +117,38 @@ __device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const in
   }
 }
 
+// Decodes list entries [first, first + NT) into a compact table of 64-key tiles in
+// LDS: entry i = (page, (sub-tile << 8) | valid keys).  Padding, out-of-range ids and
+// non-resident pages produce no tile; a B = 128 block produces up to two.  One list
+// entry per thread, compacted with a block-wide prefix sum; returns the tile count.
+// Contains barriers: every thread of the workgroup must call it.
+template <int NT>
+__device__ int decode_tiles(const AttnArgs& a, const int32_t* list, int count, int first, int2* table, int* scan_tmp) {
+  const int e = first + static_cast<int>(threadIdx.x);
+  int ntiles = 0, page = 0, nvb = 0;
+  if (e < count) {
+    const int id = list ? list[e] : a.dense_first + e;
+    if (id >= 0 && id < a.nb) {
+      const int32_t p = a.page_table[id];
+      if (p >= 0 && p < a.num_pages) {
+        const int o = id % a.Bpc;
+        nvb = o == a.Bpc - 1 ? a.S - o * a.B : a.B;
+        page = p;
+        ntiles = (nvb + kTileKeys - 1) / kTileKeys;
+      }
+    }
+  }
+  int total;
+  const int pos = block_exclusive_scan<NT>(ntiles, scan_tmp, total);
+  for (int s = 0; s < ntiles; ++s) {
+    const int nv = nvb - s * kTileKeys;
+    table[pos + s] = make_int2(page, (s << 8) | (nv < kTileKeys ? nv : kTileKeys));
+  }
+  __syncthreads();
+  return total;
+}
+
 // ------------------------------------------------------------------ bf16 / MFMA
-constexpr int kTileKeys = 64;
 constexpr int kWaves = 8;  // 256 query rows per workgroup, two waves per SIMD
 
 // A-operand row order for S^T = K Q^T: swapping bits 2 and 3 of the row makes the
@@ -152,6 +183,8 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   constexpr int KK = D / 16;                                   // k-steps of QK^T
   static_assert(CPT >= 1, "tile too small for the workgroup");
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::TOTAL_ELEMS];
+  __shared__ int2 table[2 * NT];  // decoded tiles of up to NT list entries
+  __shared__ int scan_tmp[kWaves];
   uint16_t* const k_ring = lds;
   uint16_t* const v_ring = lds + L::K_STAGES * L::K_ELEMS;
 
@@ -189,16 +222,18 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   float m_run = -INFINITY, l_run = 0.f;
   const float c = a.scale * kLog2e;
 
-  TileWalk<kTileKeys> walk(a, list, count);
   uint4 kreg[CPT], vreg[CPT];
-  auto prefetch = [&]() {
-    const uint16_t* ks = kp + walk.slab_offset(h, D);
-    const uint16_t* vs = vp + walk.slab_offset(h, D);
+  // loads one tile (page, sub-tile, valid keys) into the staging registers
+  auto prefetch = [&](int page, int meta) {
+    const int sub = meta >> 8, nv = meta & 255;
+    const int64_t slab = (static_cast<int64_t>(page) * a.H + h) * a.B * D + static_cast<int64_t>(sub) * kTileKeys * D;
+    const uint16_t* ks = kp + slab;
+    const uint16_t* vs = vp + slab;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int cid = tid + i * NT;
       const int row = cid / CHUNKS_PER_ROW, c8 = cid % CHUNKS_PER_ROW;
-      if (row < walk.nvalid) {
+      if (row < nv) {
         kreg[i] = *reinterpret_cast<const uint4*>(ks + row * D + c8 * 8);
         vreg[i] = *reinterpret_cast<const uint4*>(vs + row * D + c8 * 8);
       } else {
@@ -239,21 +274,40 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
     }
   };
 
-  bool have = walk.seek();
-  int nvalid = walk.nvalid;
+  // tile table: decode list entries NT at a time; `ti` indexes the current table
+  int next_entry = 0, ntab = 0, ti = 0;
+  while (ntab == 0 && next_entry < count) {
+    ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+    next_entry += NT;
+  }
+  bool have = ntab > 0;
+  int2 cur_tile = have ? table[0] : make_int2(0, 0);
+  cur_tile.x = __builtin_amdgcn_readfirstlane(cur_tile.x);
+  cur_tile.y = __builtin_amdgcn_readfirstlane(cur_tile.y);
   if (have) {
-    prefetch();
+    prefetch(cur_tile.x, cur_tile.y);
     stage(0, 0);
   }
   __syncthreads();
   const int krow = s_row_perm(lane % 32);
   int t = 0;
   while (have) {
-    const int cur_nvalid = nvalid;
-    walk.advance();
-    have = walk.seek();
-    nvalid = walk.nvalid;
-    if (have) prefetch();  // next tile: global loads in flight during this tile's math
+    const int cur_nvalid = cur_tile.y & 255;
+    if (++ti == ntab) {  // table exhausted: decode the next list entries (dense lists only)
+      ntab = 0;
+      ti = 0;
+      while (ntab == 0 && next_entry < count) {
+        ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+        next_entry += NT;
+      }
+    }
+    have = ti < ntab;
+    if (have) {
+      cur_tile = table[ti];
+      cur_tile.x = __builtin_amdgcn_readfirstlane(cur_tile.x);
+      cur_tile.y = __builtin_amdgcn_readfirstlane(cur_tile.y);
+      prefetch(cur_tile.x, cur_tile.y);  // next tile: global loads in flight during this tile's math
+    }
     const uint16_t* k_lds = k_ring + (t % 2) * L::K_ELEMS;
     const uint16_t* v_lds = v_ring + (t % 3) * L::V_ELEMS;
 
