@@ -29,10 +29,10 @@ struct SelectPlan {
   int qsplit;           // row splits per group in the proxy-query reduction
   bool inline_scores;   // scores computed inside the pooling kernel (small R)
   // workspace carve-up (byte offsets)
-  size_t off_qpart, off_qbar, off_kbar, off_scores, total;
+  size_t off_qpart, off_kbar, off_keys, total;
 };
 
-constexpr int kQRowsPerSplit = 128;
+constexpr int kQRowsPerSplit = 512;
 constexpr int kInlineGroups = 4;
 
 SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe);

@@ -2,14 +2,17 @@
 // (Sec. 3.2 Eq. 2, Sec. 3.3 Eq. 3) for gfx950.
 //
 // Pipeline (one stream, no host round trip):
-//   k_qmean_partial  Q rows -> fp32 partial column sums per (head, group, row split)
-//   k_qmean_final    partial sums -> proxy queries qbar[h][r][:] (group means)
+//   k_qmean_partial  Q rows -> fp32 partial column sums per (head, group, 512-row split)
 //   k_pool_score     streams every candidate K block once: block mean over its valid
-//                    tokens, then s[h][r][b] = scale * <qbar[h][r], kbar[h][b]>
-//                    (for many groups it writes kbar and k_score does the products)
-//   k_topk           per (head, group): exact top-K over Omega by an MSB-first
-//                    radix select on order-preserving 32-bit score keys in LDS,
-//                    ties to the lower block id, ids written in ascending order.
+//                    tokens, then s[h][r][b] = scale * <qbar[h][r], kbar[h][b]>, stored
+//                    as an order-preserving 32-bit key (0 outside Omega), the
+//                    proxy query qbar (group mean) being summed from the partials in
+//                    each wave's prologue (for many groups it writes kbar and k_score
+//                    does the products)
+//   k_topk           one workgroup per (head, group): exact top-K over Omega by
+//                    histogram refinement of the key interval holding the K-th key,
+//                    keys held in registers, ties to the lower block id, ids written
+//                    in ascending order.
 // The dominant cost is the K stream in k_pool_score, which is HBM-bound: each wave
 // owns whole (page, head) slabs (B*d contiguous elements) and reads them with
 // 16-byte loads, all lanes of a wave in flight on one slab at a time.
@@ -25,13 +28,16 @@ namespace {
 constexpr int kThreads = 256;
 
 // -------------------------------------------------------------- proxy queries
+constexpr int kQThreads = 1024;
+
 template <typename T, int D>
-__global__ __launch_bounds__(kThreads) void k_qmean_partial(const T* __restrict__ q, int lq, int H, int G, int R,
-                                                            int nsplit, float* __restrict__ partial) {
+__global__ __launch_bounds__(kQThreads) void k_qmean_partial(const T* __restrict__ q, int lq, int H, int G, int R,
+                                                             int nsplit, float* __restrict__ partial) {
   using V = Vec16<T>;
   constexpr int VEC = V::N;
-  constexpr int CPR = D / VEC;            // 16-byte chunks per row
-  constexpr int PHASES = kThreads / CPR;  // rows summed side by side
+  constexpr int CPR = D / VEC;             // 16-byte chunks per row
+  constexpr int PHASES = kQThreads / CPR;  // rows summed side by side
+  constexpr int UNROLL = 4;
   __shared__ float red[PHASES][D];
 
   const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z;
@@ -42,32 +48,65 @@ __global__ __launch_bounds__(kThreads) void k_qmean_partial(const T* __restrict_
   float acc[VEC];
 #pragma unroll
   for (int j = 0; j < VEC; ++j) acc[j] = 0.f;
-  for (int row = r0 + ph; row < r1; row += PHASES) {
-    float x[VEC];
-    V::load(q + (static_cast<int64_t>(row) * H + h) * D + c * VEC, x);
+  for (int row = r0 + ph; row < r1; row += UNROLL * PHASES) {
+    uint4 raw[UNROLL];  // UNROLL independent loads in flight before the adds
 #pragma unroll
-    for (int j = 0; j < VEC; ++j) acc[j] += x[j];
+    for (int u = 0; u < UNROLL; ++u) {
+      const int rr = row + u * PHASES;
+      raw[u] = rr < r1 ? *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(rr) * H + h) * D + c * VEC)
+                       : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int u = 0; u < UNROLL; ++u) {
+      float x[VEC];
+      V::widen(raw[u], x);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) acc[j] += x[j];
+    }
   }
 #pragma unroll
   for (int j = 0; j < VEC; ++j) red[ph][c * VEC + j] = acc[j];
   __syncthreads();
-  for (int col = threadIdx.x; col < D; col += kThreads) {
+  for (int col = threadIdx.x; col < D; col += kQThreads) {
     float sum = 0.f;
     for (int p = 0; p < PHASES; ++p) sum += red[p][col];
     partial[((static_cast<int64_t>(h) * R + r) * nsplit + s) * D + col] = sum;
   }
 }
 
-template <int D>
-__global__ __launch_bounds__(D) void k_qmean_final(const float* __restrict__ partial, int lq, int G, int R, int nsplit,
-                                                   float* __restrict__ qbar) {
-  const int r = blockIdx.x, h = blockIdx.y, col = threadIdx.x;
+// Proxy query columns [col, col + N) of group r: the partial sums added in split
+// order (the same order everywhere, so every reader gets identical values), divided
+// by the group's row count.
+template <int N>
+__device__ __forceinline__ void proxy_cols(const float* __restrict__ partial, int h, int r, int R, int nsplit, int D,
+                                           int col, int lq, int G, float (&out)[N]) {
   const int g0 = r * G, rows = min(g0 + G, lq) - g0;
   const int used = (rows + kQRowsPerSplit - 1) / kQRowsPerSplit;
   const float* p = partial + (static_cast<int64_t>(h) * R + r) * nsplit * D + col;
-  float sum = 0.f;
-  for (int s = 0; s < used; ++s) sum += p[static_cast<int64_t>(s) * D];
-  qbar[(static_cast<int64_t>(h) * R + r) * D + col] = sum / static_cast<float>(rows);
+#pragma unroll
+  for (int j = 0; j < N; ++j) out[j] = 0.f;
+  for (int s = 0; s < used; ++s)
+#pragma unroll
+    for (int j = 0; j < N; ++j) out[j] += p[static_cast<int64_t>(s) * D + j];
+  const float inv_rows = 1.0f / static_cast<float>(rows);
+#pragma unroll
+  for (int j = 0; j < N; ++j) out[j] = out[j] * inv_rows;
+}
+
+// -------------------------------------------------------------- score keys
+// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
+// -0 is folded onto +0 first so that equal scores compare equal.  Candidate keys
+// are forced >= 1 so that 0 can mark "not a candidate".
+__device__ __forceinline__ uint32_t score_key(float s) {
+  s = s + 0.0f;
+  const uint32_t u = __float_as_uint(s);
+  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return k == 0u ? 1u : k;
+}
+
+// Inverse of score_key on candidate keys (returns the score with -0 as +0).
+__device__ __forceinline__ float key_score(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
 }
 
 // -------------------------------------------------------------- pooling + scores
@@ -114,21 +153,15 @@ struct PoolArgs {
   const int32_t* page_table;
   int64_t num_pages;
   int H, S, Bpc, nb, first_excluded;
-  const float* qbar;  // [H][R][D]
+  const float* qpart;  // [H][R][nsplit][D] partial row sums of Q
+  int nsplit, lq, G;
   int R;
   float scale;
-  float* scores;  // [H][R][nb] (inline mode)
+  uint32_t* keys;  // [H][R][nbp] score keys, 0 outside Omega (inline mode)
+  int nbp;         // key row stride: nb rounded up to a multiple of 4
   float* kbar;    // [H][nb][D] (kbar mode)
   int blocks_per_wave;
 };
-
-__device__ __forceinline__ bool block_page(const PoolArgs& a, int b, int64_t& page) {
-  if (b >= a.first_excluded) return false;
-  const int32_t p = a.page_table[b];
-  if (p < 0 || p >= a.num_pages) return false;
-  page = p;
-  return true;
-}
 
 template <typename T, int D, int B, bool INLINE>
 __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
@@ -143,19 +176,33 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
 
   float q[INLINE ? kInlineGroups : 1][VEC];
   if (INLINE) {
+    // the workgroup's proxy queries, summed from the partials once and shared in LDS
+    __shared__ float qs[kInlineGroups][D];
+    for (int i = threadIdx.x; i < a.R * D; i += kThreads) {
+      float v[1];
+      proxy_cols<1>(a.qpart, h, i / D, a.R, a.nsplit, D, i % D, a.lq, a.G, v);
+      qs[i / D][i % D] = v[0];
+    }
+    __syncthreads();
 #pragma unroll
     for (int r = 0; r < kInlineGroups; ++r)
 #pragma unroll
-      for (int j = 0; j < VEC; ++j)
-        q[r][j] = r < a.R ? a.qbar[(static_cast<int64_t>(h) * a.R + r) * D + c * VEC + j] : 0.f;
+      for (int j = 0; j < VEC; ++j) q[r][j] = r < a.R ? qs[r][c * VEC + j] : 0.f;
   }
 
-  for (int b = first; b < last; ++b) {
-    int64_t page;
-    const bool live = block_page(a, b, page);
+  constexpr int kMaxBlocksPerWave = 8;
+  int32_t page_ids[kMaxBlocksPerWave];  // the wave's page ids, loaded together before any slab
+#pragma unroll
+  for (int i = 0; i < kMaxBlocksPerWave; ++i) page_ids[i] = first + i < last ? a.page_table[first + i] : -1;
+#pragma unroll
+  for (int i = 0; i < kMaxBlocksPerWave; ++i) {
+    const int b = first + i;
+    if (b >= last) break;
+    const int64_t page = page_ids[i];
+    const bool live = b < a.first_excluded && page >= 0 && page < a.num_pages;
     if (!live) {
       if (INLINE) {
-        if (lane < a.R) a.scores[(static_cast<int64_t>(h) * a.R + lane) * a.nb + b] = -INFINITY;
+        if (lane < a.R) a.keys[(static_cast<int64_t>(h) * a.R + lane) * a.nbp + b] = 0u;
       }
       continue;
     }
@@ -174,7 +221,7 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
         for (int j = 0; j < VEC; ++j) dot += q[r][j] * (colsum[j] * inv);
 #pragma unroll
         for (int m = 1; m < Sh::CPR; m <<= 1) dot += __shfl_xor(dot, m);
-        if (lane == 0) a.scores[(static_cast<int64_t>(h) * a.R + r) * a.nb + b] = a.scale * dot;
+        if (lane == 0) a.keys[(static_cast<int64_t>(h) * a.R + r) * a.nbp + b] = score_key(a.scale * dot);
       }
     } else {
       if (lane < Sh::CPR) {
@@ -186,12 +233,12 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
   }
 }
 
-// scores for many groups: tile of 64 blocks x 16 groups per workgroup
+// score keys for many groups: tile of 64 blocks x 16 groups per workgroup
 template <int D>
-__global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kbar, const float* __restrict__ qbar,
-                                                    const int32_t* __restrict__ page_table, int64_t num_pages,
-                                                    int nb, int first_excluded, int R, float scale,
-                                                    float* __restrict__ scores) {
+__global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kbar, const float* __restrict__ qpart,
+                                                    int nsplit, int lq, int G, const int32_t* __restrict__ page_table,
+                                                    int64_t num_pages, int nb, int nbp, int first_excluded, int R,
+                                                    float scale, uint32_t* __restrict__ keys) {
   constexpr int TB = 64, TR = 16;
   __shared__ float ks[TB][D + 1];
   __shared__ float qs[TR][D + 1];
@@ -202,7 +249,9 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
   }
   for (int i = threadIdx.x; i < TR * D; i += kThreads) {
     const int rr = i / D, j = i % D;
-    qs[rr][j] = r0 + rr < R ? qbar[(static_cast<int64_t>(h) * R + r0 + rr) * D + j] : 0.f;
+    float v[1] = {0.f};
+    if (r0 + rr < R) proxy_cols<1>(qpart, h, r0 + rr, R, nsplit, D, j, lq, G, v);
+    qs[rr][j] = v[0];
   }
   __syncthreads();
   for (int t = threadIdx.x; t < TB * TR; t += kThreads) {
@@ -213,155 +262,338 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
     for (int j = 0; j < D; ++j) dot += qs[rr][j] * ks[bb][j];
     const int32_t p = page_table[b];
     const bool live = b < first_excluded && p >= 0 && p < num_pages;
-    scores[(static_cast<int64_t>(h) * R + r) * nb + b] = live ? scale * dot : -INFINITY;
+    keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * dot) : 0u;
   }
 }
 
 // -------------------------------------------------------------- top-K
-// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
-// -0 is folded onto +0 first so that equal scores compare equal.  Candidate keys
-// are forced >= 1 so that 0 can mark "not a candidate".
-__device__ __forceinline__ uint32_t score_key(float s) {
-  s = s + 0.0f;
-  const uint32_t u = __float_as_uint(s);
-  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return k == 0u ? 1u : k;
+__device__ __forceinline__ int lane_rank(uint64_t mask) {
+  return __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                   __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0));
 }
 
-constexpr int kTopkLdsMax = 12288;  // candidates staged in LDS (48 KB) up to this many blocks
+// Exact top-K of one (head, group) key row, one workgroup of NT threads.
+//
+// Every key stays in a register: wave w holds the contiguous ids
+// [w C, (w + 1) C), C = 256 J, lane l the four ids w C + 256 j + 4 l + e (j < J, e < 4).
+// The K-th largest key is found by refinement over key intervals [lo, hi] for which
+// #{key >= lo} >= K and #{key > hi} < K: the interval is cut into 2048 equal bins
+// (a shift of key - lo), an LDS histogram and a suffix scan name the bin holding
+// the K-th key, and that bin's keys become the next interval.  Once a bin holds at
+// most kTopkList keys, their exact ranks (pairwise comparison in LDS) give the key;
+// a bin spans at most 2^-10 of its interval, so a few levels suffice for any input.
+// Emission walks the waves' ranges in id order: keys above the K-th are taken, ties
+// at it go to the lowest ids, positions come from ballot ranks.
+constexpr int kTopkMaxThreads = 1024;
+constexpr int kTopkVecPerLane = 8;                                        // J <= 8: 32 keys per lane
+constexpr int kTopkRegMax = kTopkMaxThreads * 4 * kTopkVecPerLane;        // larger rows take k_topk_wide
+constexpr int kTopkBinBits = 11;
+constexpr int kTopkBins = 1 << kTopkBinBits;
+constexpr int kTopkList = 256;
 
-template <bool IN_LDS>
-__global__ __launch_bounds__(kThreads) void k_topk(const float* __restrict__ scores,
-                                                   const int32_t* __restrict__ page_table, int64_t num_pages, int nb,
-                                                   int first_excluded, int R, int K, int32_t* __restrict__ idx,
-                                                   int32_t* __restrict__ cnt, float* __restrict__ score_out) {
-  extern __shared__ uint32_t keys[];  // [nb] when IN_LDS
-  __shared__ int hist[256];
-  __shared__ int scan_tmp[kThreads / kWave];
-  __shared__ int pick[2];
+template <int NT>
+__global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
+                                                       int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
+                                                       float* __restrict__ score_out) {
+  constexpr int kWaves = NT / kWave, kBinsPerThread = kTopkBins / NT;
+  __shared__ int hist[kTopkBins];
+  __shared__ __align__(16) uint32_t list[kTopkList];
+  __shared__ int wave_a[kWaves], wave_b[kWaves];
+  __shared__ uint32_t wave_lo[kWaves], wave_hi[kWaves];
+  __shared__ int s_bin, s_above, s_m;
+  __shared__ uint32_t s_kth;
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  const uint32_t* kp = keys + row * nbp;
+  const int J = min(kTopkVecPerLane, (nb + 4 * NT - 1) / (4 * NT));
+  const int base = wave * J * 4 * kWave;
 
-  const int r = blockIdx.x, h = blockIdx.y;
-  const int64_t row = static_cast<int64_t>(h) * R + r;
-  const float* s = scores + row * nb;
-
-  auto key_of = [&](int b) -> uint32_t {
-    const int32_t p = page_table[b];
-    const bool cand = b < first_excluded && p >= 0 && p < num_pages;
-    return cand ? score_key(s[b]) : 0u;
-  };
-  auto key_at = [&](int b) -> uint32_t { return IN_LDS ? keys[b] : key_of(b); };
-
-  int mine = 0;
-  for (int b = threadIdx.x; b < nb; b += kThreads) {
-    const uint32_t k = key_of(b);
-    if (IN_LDS) keys[b] = k;
-    mine += k != 0u;
-  }
-  int ncand;
-  block_exclusive_scan<kThreads>(mine, scan_tmp, ncand);  // also a barrier for `keys`
-
-  // Radix select of the K-th largest key: after the four 8-bit passes `prefix`
-  // is that key and `need` the number of keys equal to it that are taken.
-  uint32_t prefix = 0u, mask = 0u;
-  int need = K;
-  const bool all = ncand <= K;
-  if (!all) {
-    for (int shift = 24; shift >= 0; shift -= 8) {
-      hist[threadIdx.x] = 0;
-      __syncthreads();
-      for (int b = threadIdx.x; b < nb; b += kThreads) {
-        const uint32_t k = key_at(b);
-        if (k != 0u && (k & mask) == prefix) atomicAdd(&hist[(k >> shift) & 255u], 1);
-      }
-      __syncthreads();
-      if (threadIdx.x < kWave) {
-        // lane l owns digits 255-4l .. 252-4l (descending)
-        const int lane = threadIdx.x;
-        int hcount[4], lane_sum = 0;
+  uint32_t kr[4 * kTopkVecPerLane];
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          hcount[j] = hist[255 - 4 * lane - j];
-          lane_sum += hcount[j];
-        }
-        const int incl = wave_inclusive_scan(lane_sum);
-        const int excl = incl - lane_sum;
-        if (excl < need && need <= incl) {
-          int run = excl;
-#pragma unroll
-          for (int j = 0; j < 4; ++j) {
-            if (run + hcount[j] >= need) {
-              pick[0] = 255 - 4 * lane - j;
-              pick[1] = run;
-              break;
-            }
-            run += hcount[j];
-          }
-        }
-      }
-      __syncthreads();
-      need -= pick[1];
-      prefix |= static_cast<uint32_t>(pick[0]) << shift;
-      mask |= 255u << shift;
-      __syncthreads();
-    }
+  for (int j = 0; j < kTopkVecPerLane; ++j) {
+    const int i = base + (j * kWave + lane) * 4;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (j < J && i < nb) v = *reinterpret_cast<const uint4*>(kp + i);  // i + 3 < nbp
+    kr[4 * j + 0] = v.x;
+    kr[4 * j + 1] = i + 1 < nb ? v.y : 0u;
+    kr[4 * j + 2] = i + 2 < nb ? v.z : 0u;
+    kr[4 * j + 3] = i + 3 < nb ? v.w : 0u;
   }
-
-  // Emit in ascending id order: thread t owns ids [t*per, (t+1)*per).
-  const int per = (nb + kThreads - 1) / kThreads;
-  const int lo = min(threadIdx.x * per, nb), hi = min(lo + per, nb);
-  int n_eq = 0;
-  if (!all)
-    for (int b = lo; b < hi; ++b) n_eq += key_at(b) == prefix;
-  int tot_eq;
-  int eq_rank = block_exclusive_scan<kThreads>(n_eq, scan_tmp, tot_eq);
-  int n_sel = 0;
+#pragma unroll
+  for (int u = 0; u < kBinsPerThread; ++u) hist[tid * kBinsPerThread + u] = 0;
   {
-    int er = eq_rank;
-    for (int b = lo; b < hi; ++b) {
-      const uint32_t k = key_at(b);
-      bool take;
-      if (all) {
-        take = k != 0u;
-      } else if (k == prefix) {
-        take = er < need;
-        ++er;
-      } else {
-        take = k > prefix;
-      }
-      n_sel += take;
+    int n = 0;
+    uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+    for (int j = 0; j < 4 * kTopkVecPerLane; ++j) {
+      if (j >= 4 * J) break;
+      n += kr[j] != 0u;
+      kmin = min(kmin, kr[j] != 0u ? kr[j] : 0xffffffffu);
+      kmax = max(kmax, kr[j]);
+    }
+    n = __reduce_add_sync(~0ull, n);
+    kmin = __reduce_min_sync(~0ull, kmin);
+    kmax = __reduce_max_sync(~0ull, kmax);
+    if (lane == 0) {
+      wave_a[wave] = n;
+      wave_lo[wave] = kmin;
+      wave_hi[wave] = kmax;
     }
   }
-  int total;
-  int pos = block_exclusive_scan<kThreads>(n_sel, scan_tmp, total);
+  __syncthreads();
+  int ncand = 0;
+  uint32_t lo = 0xffffffffu, hi = 0u;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    ncand += wave_a[w];
+    lo = min(lo, wave_lo[w]);
+    hi = max(hi, wave_hi[w]);
+  }
+  const bool all = ncand <= K;
+  uint32_t kth = 0u;  // with `all`, every key > 0 is taken
+  if (!all) {
+    int above = 0;  // #{key > hi}
+    while (true) {
+      if (lo == hi) {
+        kth = lo;
+        break;
+      }
+      const int width = 32 - __clz(hi - lo);
+      const int shift = width > kTopkBinBits ? width - kTopkBinBits : 0;
+#pragma unroll
+      for (int j = 0; j < 4 * kTopkVecPerLane; ++j) {
+        if (j >= 4 * J) break;
+        if (kr[j] - lo <= hi - lo) atomicAdd(&hist[(kr[j] - lo) >> shift], 1);
+      }
+      __syncthreads();
+      // suffix scan from the top bin: thread t owns the kBinsPerThread bins that
+      // start kBinsPerThread * t bins below the top, in descending order
+      int c[kBinsPerThread], csum = 0;
+#pragma unroll
+      for (int u = 0; u < kBinsPerThread; ++u) {
+        c[u] = hist[kTopkBins - 1 - (tid * kBinsPerThread + u)];
+        csum += c[u];
+      }
+      const int incl = wave_inclusive_scan(csum);
+      if (lane == kWave - 1) wave_b[wave] = incl;
+      if (tid == 0) s_m = 0;
+      for (int i = tid; i < kTopkList; i += NT) list[i] = 0u;  // zero padding for the rank step
+      __syncthreads();
+      int before = above + incl - csum;
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) before += w < wave ? wave_b[w] : 0;
+#pragma unroll
+      for (int u = 0; u < kBinsPerThread; ++u) {
+        if (before < K && before + c[u] >= K) {
+          s_bin = kTopkBins - 1 - (tid * kBinsPerThread + u);
+          s_above = before;
+        }
+        before += c[u];
+      }
+      __syncthreads();
+      const int bstar = s_bin;
+      above = s_above;
+#pragma unroll
+      for (int u = 0; u < kBinsPerThread; ++u) hist[tid * kBinsPerThread + u] = 0;  // ready for a further level
+      // gather the keys of bin b* into the list: one LDS atomic per wave reserves
+      // the wave's slots, ballot ranks place the keys
+      const uint32_t bin_lo = lo + (static_cast<uint32_t>(bstar) << shift);
+      const uint32_t bin_span = static_cast<uint32_t>(
+          min(static_cast<uint64_t>(hi - bin_lo), (1ull << shift) - 1u));  // bin = [bin_lo, bin_lo + bin_span]
+      auto member = [&](uint32_t k) { return k - bin_lo <= bin_span; };
+      int wave_members = 0;
+#pragma unroll
+      for (int j = 0; j < 4 * kTopkVecPerLane; ++j) {
+        if (j >= 4 * J) break;
+        wave_members += __popcll(__ballot(member(kr[j])));
+      }
+      if (wave_members > 0) {
+        int at = 0;
+        if (lane == 0) at = atomicAdd(&s_m, wave_members);
+        at = __shfl(at, 0);
+#pragma unroll
+        for (int j = 0; j < 4 * kTopkVecPerLane; ++j) {
+          if (j >= 4 * J) break;
+          const bool mem = member(kr[j]);
+          const uint64_t mask = __ballot(mem);
+          const int pos = at + lane_rank(mask);
+          if (mem && pos < kTopkList) list[pos] = kr[j];
+          at += __popcll(mask);
+        }
+      }
+      __syncthreads();
+      const int m = s_m;
+      if (m <= kTopkList) {
+        // exact ranks inside the bin: the K-th key x has g(x) < need <= g(x) + e(x)
+        const int need = K - above;
+        if (tid < m) {
+          // entries past m are 0, below every candidate key
+          const uint32_t x = list[tid];
+          const uint4* l4 = reinterpret_cast<const uint4*>(list);
+          int g = 0, e = 0;
+          for (int i = 0; i < m; i += 16) {
+            uint4 y[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) y[u] = l4[i / 4 + u];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) {
+              g += (y[u].x > x) + (y[u].y > x) + (y[u].z > x) + (y[u].w > x);
+              e += (y[u].x == x) + (y[u].y == x) + (y[u].z == x) + (y[u].w == x);
+            }
+          }
+          if (g < need && need <= g + e) s_kth = x;
+        }
+        __syncthreads();
+        kth = s_kth;
+        break;
+      }
+      // more than kTopkList keys in b*: refine inside the bin's key range, which
+      // keeps #{key >= lo} >= K and #{key > hi} < K
+      lo = bin_lo;
+      hi = bin_lo + bin_span;
+    }
+  }
+
+  // per-wave counts above and at the K-th key, then emission in id order
+  {
+    int gt = 0, eq = 0;
+#pragma unroll
+    for (int j = 0; j < 4 * kTopkVecPerLane; ++j) {
+      if (j >= 4 * J) break;
+      gt += kr[j] > kth;
+      eq += kr[j] == kth;
+    }
+    gt = __reduce_add_sync(~0ull, gt);
+    eq = __reduce_add_sync(~0ull, eq);
+    __syncthreads();  // wave_a / wave_b are reused
+    if (lane == 0) {
+      wave_a[wave] = gt;
+      wave_b[wave] = eq;
+    }
+  }
+  __syncthreads();
+  int gt_all = 0, gt_before = 0, eq_before = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) {
+    gt_all += wave_a[w];
+    if (w < wave) {
+      gt_before += wave_a[w];
+      eq_before += wave_b[w];
+    }
+  }
+  const int total = all ? ncand : K;
+  const int need = all ? 0 : K - gt_all;  // ties at the K-th key still to take
   int32_t* out_idx = idx + row * K;
   float* out_score = score_out ? score_out + row * K : nullptr;
-  {
-    int er = eq_rank;
-    for (int b = lo; b < hi; ++b) {
-      const uint32_t k = key_at(b);
-      bool take;
-      if (all) {
-        take = k != 0u;
-      } else if (k == prefix) {
-        take = er < need;
-        ++er;
-      } else {
-        take = k > prefix;
-      }
-      if (take) {
-        if (pos < K) {  // holds by construction; the guard keeps a bad input from writing past the row
-          out_idx[pos] = b;
-          if (out_score) out_score[pos] = s[b];
+  int pos = gt_before + min(eq_before, need);
+  int eq_run = eq_before;
+#pragma unroll
+  for (int j = 0; j < kTopkVecPerLane; ++j) {
+    if (j >= J) break;
+    bool tie[4], take[4];
+    uint64_t tie_mask[4], take_mask[4];
+    int tie_below = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      tie[e] = !all && kr[4 * j + e] == kth;
+      tie_mask[e] = __ballot(tie[e]);
+      tie_below += lane_rank(tie_mask[e]);
+    }
+    int mine = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      take[e] = kr[4 * j + e] > kth || (tie[e] && eq_run + tie_below + mine < need);
+      mine += tie[e];
+    }
+    int take_below = 0;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      take_mask[e] = __ballot(take[e]);
+      take_below += lane_rank(take_mask[e]);
+    }
+    int at = pos + take_below;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (take[e]) {
+        if (at < K) {  // holds by construction; keeps a bad input inside the row
+          out_idx[at] = base + (j * kWave + lane) * 4 + e;
+          if (out_score) out_score[at] = key_score(kr[4 * j + e]);
         }
-        ++pos;
+        ++at;
       }
+      pos += __popcll(take_mask[e]);
+      eq_run += __popcll(tie_mask[e]);
     }
   }
-  for (int t = total + threadIdx.x; t < K; t += kThreads) {
-    out_idx[t] = -1;
-    if (out_score) out_score[t] = -INFINITY;
+  for (int i = total + tid; i < K; i += NT) {
+    out_idx[i] = -1;
+    if (out_score) out_score[i] = -INFINITY;
   }
-  if (threadIdx.x == 0) cnt[row] = total < K ? total : K;
+  if (tid == 0) cnt[row] = total < K ? total : K;
+}
+
+// Top-K for rows longer than the register-resident kernel holds: one wavefront,
+// keys re-read at every step of a plain bisection.
+__global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
+                                                     int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
+                                                     float* __restrict__ score_out) {
+  const int lane = threadIdx.x;
+  const int64_t row = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  const uint32_t* kp = keys + row * nbp;
+  int ncand = 0;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  for (int b = lane; b < nb; b += kWave) {
+    const uint32_t k = kp[b];
+    if (k != 0u) {
+      ++ncand;
+      kmin = min(kmin, k);
+      kmax = max(kmax, k);
+    }
+  }
+  ncand = __reduce_add_sync(~0ull, ncand);
+  kmin = __reduce_min_sync(~0ull, kmin);
+  kmax = __reduce_max_sync(~0ull, kmax);
+  auto count_ge = [&](uint32_t th, bool strict) -> int {
+    int c = 0;
+    for (int b = lane; b < nb; b += kWave) c += strict ? kp[b] > th : kp[b] >= th;
+    return __reduce_add_sync(~0ull, c);
+  };
+  const bool all = ncand <= K;
+  uint32_t kth = 0u;
+  int need = 0;
+  if (!all) {
+    uint32_t lo = kmin, hi = kmax;
+    while (lo < hi) {
+      const uint32_t mid = lo + (hi - lo) / 2 + 1;
+      if (count_ge(mid, false) >= K) lo = mid; else hi = mid - 1;
+    }
+    kth = lo;
+    need = K - count_ge(kth, true);
+  }
+  int32_t* out_idx = idx + row * K;
+  float* out_score = score_out ? score_out + row * K : nullptr;
+  int pos = 0, eq_run = 0;
+  for (int b0 = 0; b0 < nb; b0 += kWave) {
+    const int b = b0 + lane;
+    const uint32_t k = b < nb ? kp[b] : 0u;
+    const bool tie = !all && k == kth;
+    const uint64_t tie_mask = __ballot(tie);
+    const bool take = k > kth || (tie && eq_run + lane_rank(tie_mask) < need);
+    const uint64_t take_mask = __ballot(take);
+    const int at = pos + lane_rank(take_mask);
+    if (take && at < K) {
+      out_idx[at] = b;
+      if (out_score) out_score[at] = key_score(k);
+    }
+    pos += __popcll(take_mask);
+    eq_run += __popcll(tie_mask);
+  }
+  const int total = all ? ncand : K;
+  for (int i = total + lane; i < K; i += kWave) {
+    out_idx[i] = -1;
+    if (out_score) out_score[i] = -INFINITY;
+  }
+  if (lane == 0) cnt[row] = total < K ? total : K;
 }
 
 inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -371,14 +603,12 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
                                float* score, void* workspace, hipStream_t stream) {
   char* ws = static_cast<char*>(workspace);
   float* qpart = reinterpret_cast<float*>(ws + p.off_qpart);
-  float* qbar = reinterpret_cast<float*>(ws + p.off_qbar);
   float* kbar = reinterpret_cast<float*>(ws + p.off_kbar);
-  float* scores = reinterpret_cast<float*>(ws + p.off_scores);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
+  const int nbp = (g.nb + 3) / 4 * 4;
 
-  hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kThreads), 0, stream,
+  hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kQThreads), 0, stream,
                      static_cast<const T*>(q), p.lq, g.H, p.G, p.R, p.qsplit, qpart);
-  hipLaunchKernelGGL((k_qmean_final<D>), dim3(p.R, g.H), dim3(D), 0, stream, qpart, p.lq, p.G, p.R, p.qsplit, qbar);
-
   if (g.nb > 0) {
     PoolArgs a;
     a.k_pages = g.k_pages;
@@ -389,12 +619,16 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     a.Bpc = g.Bpc;
     a.nb = g.nb;
     a.first_excluded = p.first_excluded;
-    a.qbar = qbar;
+    a.qpart = qpart;
+    a.nsplit = p.qsplit;
+    a.lq = p.lq;
+    a.G = p.G;
     a.R = p.R;
     a.scale = p.scale;
-    a.scores = scores;
+    a.keys = keys;
+    a.nbp = nbp;
     a.kbar = kbar;
-    a.blocks_per_wave = 2;
+    a.blocks_per_wave = 2;  // at most the pooling kernel's page-id batch (kMaxBlocksPerWave)
     const int waves = (g.nb + a.blocks_per_wave - 1) / a.blocks_per_wave;
     const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
     if (g.B == 64) {
@@ -410,18 +644,18 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     }
     if (!p.inline_scores) {
       const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
-      hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, kbar, qbar, g.page_table, g.num_pages, g.nb,
-                         p.first_excluded, p.R, p.scale, scores);
+      hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, kbar, qpart, p.qsplit, p.lq, p.G,
+                         g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
     }
   }
   const dim3 tgrid(p.R, g.H);
-  if (g.nb <= kTopkLdsMax) {
-    hipLaunchKernelGGL((k_topk<true>), tgrid, dim3(kThreads), static_cast<size_t>(g.nb) * 4 + 16, stream, scores,
-                       g.page_table, g.num_pages, g.nb, p.first_excluded, p.R, p.K, idx, cnt, score);
-  } else {
-    hipLaunchKernelGGL((k_topk<false>), tgrid, dim3(kThreads), 0, stream, scores, g.page_table, g.num_pages, g.nb,
-                       p.first_excluded, p.R, p.K, idx, cnt, score);
-  }
+  // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice that
+  if (g.nb <= 512 * 4 * kTopkVecPerLane)
+    hipLaunchKernelGGL(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  else if (g.nb <= kTopkRegMax)
+    hipLaunchKernelGGL(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  else
+    hipLaunchKernelGGL(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
   return hipGetLastError();
 }
 
@@ -443,12 +677,10 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
   size_t off = 0;
   p.off_qpart = off;
   off = align256(off + static_cast<size_t>(g.H) * p.R * p.qsplit * g.D * sizeof(float));
-  p.off_qbar = off;
-  off = align256(off + static_cast<size_t>(g.H) * p.R * g.D * sizeof(float));
   p.off_kbar = off;
   if (!p.inline_scores) off = align256(off + static_cast<size_t>(g.H) * g.nb * g.D * sizeof(float));
-  p.off_scores = off;
-  off = align256(off + static_cast<size_t>(g.H) * p.R * (g.nb > 0 ? g.nb : 1) * sizeof(float));
+  p.off_keys = off;
+  off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
   p.total = off;
   return p;
 }

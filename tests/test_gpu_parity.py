@@ -192,6 +192,34 @@ def test_edge_cases(dev):
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
 
 
+# ------------------------------------------------------------- long block lists
+
+@pytest.mark.parametrize("n,zero_q", [(5000, True), (5000, False), (33000, False), (33000, True)])
+def test_long_lists_and_ties(dev, n, zero_q):
+    """Top-K over long block lists: 5000 blocks spread over several key partitions of
+    the register-resident search, 33000 blocks take the streaming search.  Zero
+    queries make every score exactly 0, so the lowest candidate ids must be chosen."""
+    say(f"long list n={n} zero_q={zero_q}")
+    w = synth.Workload("long", 1, 64, 64, 8, 64, n, n, 64, 8, 1, 1, torch.bfloat16, False, 1, 9)
+    g = torch.Generator(device=dev).manual_seed(17 + n)
+    k = torch.randn((n, 64, 1, 64), generator=g, device=dev).to(torch.bfloat16)
+    q = torch.randn((8, 1, 64), generator=g, device=dev).to(torch.bfloat16)
+    if zero_q:
+        q.zero_()
+    nonres = [0, 5, 2047, 2048, n - 3]
+    cache = synth.page_layer(k, k, 64, seed=2, nonresident=nonres)
+    resident = synth.resident_mask(cache).numpy()
+    x = synth.LayerInputs(q=q, k=k, v=k, rel=None)
+    sel = run_select(cache, x, w)
+    ref = oracle_select(x, w, n, resident=resident)
+    got = host(sel.idx).numpy()
+    check_selection(got, host(sel.cnt).numpy(), ref)
+    if zero_q:
+        assert (got == ref["idx"]).all()
+        omega = [b for b in range(n - 1) if resident[b]]  # the last chunk is the excluded window
+        assert got[0, 0].tolist() == omega[:64]
+
+
 # ------------------------------------------------------------ full-size workloads
 
 def planted_recall(sel, x, w, n):
