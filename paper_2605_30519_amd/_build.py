@@ -24,13 +24,19 @@ FLAGS = [
 ]
 
 
+# Per-source extra flags.  The 64-row attention kernel needs more than 256 registers
+# per lane; MFMA results in arch VGPRs (not accumulation registers) keep its softmax
+# VALU work free of register-file copies.
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+
+
 def build(verbose: bool = False) -> str:
     """Compile every source (in parallel) and link libomnimem.so.  Always rebuilds."""
     os.makedirs(OBJ_DIR, exist_ok=True)
     procs = []
     for src in SOURCES:
         obj = os.path.join(OBJ_DIR, src.replace(".hip", ".o"))
-        cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
         procs.append((src, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
     objs = []
     errors = []

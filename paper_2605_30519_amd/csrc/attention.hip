@@ -406,6 +406,333 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
         l_tot > 0.f ? (m_run * c + __log2f(l_tot)) * kLn2 : -INFINITY;
 }
 
+// ------------------------------------------------------------------ bf16 / MFMA, 64 rows per wave
+// Four waves (one per SIMD) x 64 query rows, as two 32-row halves that share every
+// K and V operand read from LDS: each 1 KB operand fragment feeds two MFMAs, half the
+// LDS bytes per flop of the 32-row kernel, whose operand traffic equals the LDS
+// bandwidth at the MFMA peak.  With one wave per SIMD the matrix core is kept busy
+// from inside the wave: the instruction stream alternates MFMAs of one half with
+// the softmax VALU work of the other (QK of half 1 with the exponentials of half
+// 0, PV of half 0 with the exponentials of half 1), and MFMAs run asynchronously.
+// The running max may lag the true one by up to kRescaleSlack (log2 units), so O
+// and l are rescaled only when a row's max grows by more than that; exponentials
+// are then at most 2^kRescaleSlack, well inside fp32 and bf16 range, and the final
+// normalisation cancels the stale max exactly.
+constexpr int kR64Waves = 4;
+constexpr float kRescaleSlack = 8.0f;
+
+// max / sum of a value over the lane pair (l, l ^ 32)
+__device__ __forceinline__ float pair_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Pins values at this point of the instruction stream: the exponentials of one half
+// are computed between the other half's MFMAs, not moved down to their first use.
+__device__ __forceinline__ void keep_here(const bf16x8 (&pb)[4], float l) {
+  asm volatile("" ::"v"(pb[0]), "v"(pb[1]), "v"(pb[2]), "v"(pb[3]), "v"(l));
+}
+
+// Workgroup barrier for LDS traffic only.  __syncthreads() also orders global memory,
+// which makes every wave drain its outstanding loads, including the DMA of tiles
+// meant to stay in flight across the barrier; LDS written by DMA is covered by the
+// explicit vmcnt wait before it, and the asm statements keep the compiler from
+// moving LDS accesses across it.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+// Buffer resource over `bytes` bytes at p (raw, unswizzled; offsets at or past the
+// end read as zero).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, 0x00020000);
+}
+
+// LDS tiles of the 64-row kernel: 64 rows of 256 bytes (d = 128 bf16), unpadded, with
+// the 16-byte chunks of each row permuted so that both the K fragment reads and the
+// transposing V reads touch every bank once per pass:
+//   K: chunk c of row r sits at chunk position c ^ (r mod 16)
+//   V: chunk c of row r sits at chunk position c ^ 4 (r mod 4)
+// Tiles arrive by buffer-to-LDS DMA: one instruction moves 64 lanes x 16 bytes into a
+// contiguous 1 KB (rows 4m .. 4m + 3), lane l filling chunk position l mod 16 of row
+// 4m + l / 16, so each lane fetches the global chunk that belongs at its position.
+constexpr int kR64TileBytes = kTileKeys * 128 * 2;
+__device__ __forceinline__ int k_pos(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
+__device__ __forceinline__ int v_pos(int r, int c) { return r * 256 + ((c ^ (4 * (r & 3))) << 4); }
+
+template <int D>
+__global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs a) {
+  static_assert(D == 128, "the 64-row kernel is laid out for d = 128");
+  constexpr int NT = kR64Waves * kWave;
+  constexpr int ROWS = kR64Waves * 64;
+  constexpr int DT = D / 32;
+  constexpr int KK = D / 16;
+  constexpr int DMA_PER_WAVE = kR64TileBytes / 1024 / kR64Waves;  // 1 KB DMA instructions per wave, K and V each
+  // three stages (K and V each), separate objects so that the compiler can tell a
+  // stage being read from the stages still being filled
+  __shared__ __attribute__((aligned(1024))) uint8_t k_st0[kR64TileBytes], k_st1[kR64TileBytes], k_st2[kR64TileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_st0[kR64TileBytes], v_st1[kR64TileBytes], v_st2[kR64TileBytes];
+  __shared__ int2 table[2 * NT];
+  __shared__ int scan_tmp[kR64Waves];
+
+  int h, hr, row0, row_end;
+  resolve_tile(a, ROWS, h, hr, row0, row_end);
+  if (row0 >= row_end) return;  // workgroup-uniform: no barrier has been reached
+  const int32_t* list;
+  int count;
+  resolve_list(a, hr, list, count);
+
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  const int half = lane / 32;
+  const uint16_t* qp = static_cast<const uint16_t*>(a.q);
+  const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
+  const uint16_t* vp = static_cast<const uint16_t*>(a.v_pages);
+
+  // Q^T B operands of the two halves: lane holds query wrow + 32 g + lane % 32
+  const int wrow = row0 + wave * 64;
+  const bool wave_live = wrow < row_end;  // wave-uniform
+  bf16x8 q0[KK], q1[KK];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    const int r0 = wrow + lane % 32, r1 = r0 + 32;
+    uint4 x0 = make_uint4(0, 0, 0, 0), x1 = x0;
+    if (r0 < row_end)
+      x0 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r0) * a.H + h) * D + 16 * kk + 8 * half);
+    if (r1 < row_end)
+      x1 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r1) * a.H + h) * D + 16 * kk + 8 * half);
+    q0[kk] = __builtin_bit_cast(bf16x8, x0);
+    q1[kk] = __builtin_bit_cast(bf16x8, x1);
+  }
+
+  f32x16 o0[DT], o1[DT];
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      o0[dt][i] = 0.f;
+      o1[dt][i] = 0.f;
+    }
+  // running max in scaled log2 units (max * scale * log2 e) and this lane's share of l
+  float ms0 = -INFINITY, ms1 = -INFINITY, l0 = 0.f, l1 = 0.f;
+  const float c = a.scale * kLog2e;
+
+  // ---- tile sequence: (page, sub-tile << 8 | valid keys), from the decoded table
+  int next_entry = 0, ntab = 0, ti = 0;
+  auto next_tile = [&]() -> int2 {  // workgroup-uniform; refills the table (barriers) when it runs out
+    if (ti == ntab) {
+      ntab = 0;
+      ti = 0;
+      while (ntab == 0 && next_entry < count) {
+        ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+        next_entry += NT;
+      }
+      if (ntab == 0) return make_int2(0, 0);  // past the end: an empty tile
+    }
+    int2 m = table[ti++];
+    m.x = __builtin_amdgcn_readfirstlane(m.x);
+    m.y = __builtin_amdgcn_readfirstlane(m.y);
+    return m;
+  };
+  // this lane's source offsets for its DMA instructions (row 4 m + lane / 16, m = wave + 4 i)
+  int k_src[DMA_PER_WAVE], v_src[DMA_PER_WAVE];
+#pragma unroll
+  for (int i = 0; i < DMA_PER_WAVE; ++i) {
+    const int r = 4 * (wave + kR64Waves * i) + lane / 16, p = lane % 16;
+    k_src[i] = r * 256 + ((p ^ (r & 15)) << 4);
+    v_src[i] = r * 256 + ((p ^ (4 * (r & 3))) << 4);
+  }
+  typedef __attribute__((address_space(3))) void lds_void;
+  auto issue = [&](int2 m, uint8_t* kst, uint8_t* vst) {  // empty tiles load nothing and write zeros
+    const int sub = m.y >> 8, nv = m.y & 255;
+    const int64_t slab = (static_cast<int64_t>(m.x) * a.H + h) * a.B * D + static_cast<int64_t>(sub) * kTileKeys * D;
+    const __amdgpu_buffer_rsrc_t kr = make_rsrc(kp + slab, nv * D * 2);
+    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vp + slab, nv * D * 2);
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) {
+      const int mi = wave + kR64Waves * i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(kst + mi * 1024), 16, k_src[i], 0, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(vst + mi * 1024), 16, v_src[i], 0, 0, 0);
+    }
+  };
+
+  // row max of a half over the tile, scaled; keys past the block's end are masked
+  auto tile_max = [&](f32x16 (&s)[2], int nvalid) -> float {
+    if (nvalid < kTileKeys) {
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
+          if (key >= nvalid) s[t2][i] = -INFINITY;
+        }
+    }
+    float m = s[0][0];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) m = fmaxf(m, s[t2][i]);
+    return pair_max(m) * c;
+  };
+  auto rescale = [&](float mt, float& ms, float& l, f32x16 (&o)[DT]) {
+    if (__any(mt > ms + kRescaleSlack)) {
+      const float m_new = fmaxf(ms, mt);
+      const float alpha = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - m_new);
+      l *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
+      ms = m_new;
+    }
+  };
+  // exponentials of elements 2i and 2i + 1 of a half's S tile (i < 16): p = 2^(s c - ms),
+  // packed into the bf16 P^T operand and summed into two partial row sums
+  auto exp_pair = [&](const f32x16 (&s)[2], float ms, float (&acc)[2], bf16x8 (&pb)[4], int i) {
+    const int t2 = i / 8, e = (2 * i) % 16;
+    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[t2][e], c, -ms));
+    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[t2][e + 1], c, -ms));
+    acc[0] += p0;
+    acc[1] += p1;
+    pb[2 * t2 + e / 8][e % 8] = static_cast<__bf16>(p0);
+    pb[2 * t2 + e / 8][e % 8 + 1] = static_cast<__bf16>(p1);
+  };
+
+  const int krow = s_row_perm(lane % 32);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  // one tile from stage (kst, vst); the tile after next goes into (kst2, vst2)
+  auto step = [&](int2 cur, int2 after_next, const uint8_t* kst, const uint8_t* vst, uint8_t* kst2, uint8_t* vst2) {
+    // this wave's DMA of the current tile is done (the next tile's DMA_PER_WAVE x 2
+    // instructions may still be in flight); the barrier then makes every wave's
+    // copies visible and frees the stage read one tile ago
+    __builtin_amdgcn_s_waitcnt(0xF70 | (2 * DMA_PER_WAVE));  // vmcnt(2 * DMA_PER_WAVE), expcnt and lgkmcnt not waited
+    lds_barrier();
+    issue(after_next, kst2, vst2);
+    if (!wave_live) return;
+    const int cur_nvalid = cur.y & 255;
+    // ---- S^T = K Q^T for both halves; each K fragment feeds two MFMAs
+    bf16x8 kf[2][KK];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk)
+        kf[t2][kk] = *reinterpret_cast<const bf16x8*>(kst + k_pos(32 * t2 + krow, 2 * kk + half));
+    f32x16 s0[2], s1[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        s0[t2][i] = 0.f;
+        s1[t2][i] = 0.f;
+      }
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s0[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t2][kk], q0[kk], s0[t2], 0, 0, 0);
+    rescale(tile_max(s0, cur_nvalid), ms0, l0, o0);
+    // ---- QK of half 1, one MFMA per pair of half-0 exponentials (the fences keep
+    // the interleaving: the wave issues in order and MFMAs run asynchronously)
+    bf16x8 pb0[4], pb1[4];
+    float acc0[2] = {0.f, 0.f}, acc1[2] = {0.f, 0.f};
+#pragma unroll
+    for (int i = 0; i < 2 * KK; ++i) {
+      s1[i / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / KK][i % KK], q1[i % KK], s1[i / KK], 0, 0, 0);
+      exp_pair(s0, ms0, acc0, pb0, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l0 += acc0[0] + acc0[1];
+    keep_here(pb0, l0);
+    rescale(tile_max(s1, cur_nvalid), ms1, l1, o1);
+    // ---- O^T += V^T P^T: PV of half 0 between pairs of half-1 exponentials, then PV of half 1
+    bf16x8 vf[4][DT];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int ch = 4 * dt + 2 * ((lane / 16) % 2) + (lane % 4) / 2, b8 = 8 * (lane % 2);
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0, ch) + b8));
+        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0 + 4, ch) + b8));
+        vf[j][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int i = 0; i < 4 * DT; ++i) {
+      o0[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb0[i / DT], o0[i % DT], 0, 0, 0);
+      exp_pair(s1, ms1, acc1, pb1, i);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    l1 += acc1[0] + acc1[1];
+#pragma unroll
+    for (int i = 0; i < 4 * DT; ++i)
+      o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
+  };
+
+  // ---- prologue: the first two tiles in flight; then three tiles per round, one per stage
+  int2 t0 = next_tile(), t1 = next_tile();
+  issue(t0, k_st0, v_st0);
+  issue(t1, k_st1, v_st1);
+  while ((t0.y & 255) != 0) {
+    int2 t2 = next_tile();
+    step(t0, t2, k_st0, v_st0, k_st2, v_st2);
+    if ((t1.y & 255) == 0) break;
+    int2 t3 = next_tile();
+    step(t1, t3, k_st1, v_st1, k_st0, v_st0);
+    if ((t2.y & 255) == 0) break;
+    int2 t4 = next_tile();
+    step(t2, t4, k_st2, v_st2, k_st1, v_st1);
+    t0 = t3;
+    t1 = t4;
+  }
+  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): no DMA may land in the stages reused below
+  __syncthreads();
+
+  // ---- epilogue: normalise, stage O through LDS (one 16 KB stage per wave, chunks
+  // permuted like K), store rows with 16-byte writes
+  uint8_t* const stage_o = wave == 0 ? k_st0 : wave == 1 ? k_st1 : wave == 2 ? k_st2 : v_st0;
+  auto finish = [&](f32x16 (&o)[DT], float ms, float l, int g) {
+    const float l_tot = pair_sum(l);
+    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+    const int r = 32 * g + lane % 32;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) {
+        bf16x4 w;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(o[dt][4 * i4 + e] * inv);
+        // d = 32 dt + 8 i4 + 4 half: chunk 4 dt + i4, byte 8 half within it
+        *reinterpret_cast<bf16x4*>(stage_o + k_pos(r, 4 * dt + i4) + 8 * half) = w;
+      }
+    const int qr = wrow + r;
+    if (a.lse && lane < 32 && qr < row_end)
+      a.lse[static_cast<int64_t>(h) * a.lq + qr] = l_tot > 0.f ? (ms + __log2f(l_tot)) * kLn2 : -INFINITY;
+  };
+  if (wave_live) {
+    finish(o0, ms0, l0, 0);
+    finish(o1, ms1, l1, 1);
+  }
+  __syncthreads();
+  uint16_t* op = static_cast<uint16_t*>(a.out);
+  if (wave_live) {
+#pragma unroll
+    for (int i = 0; i < 64 * 16 / kWave; ++i) {
+      const int cid = lane + i * kWave;
+      const int r = cid / 16, ch = cid % 16;
+      const int qrow = wrow + r;
+      if (qrow < row_end)
+        *reinterpret_cast<uint4*>(op + (static_cast<int64_t>(qrow) * a.H + h) * D + ch * 8) =
+            *reinterpret_cast<const uint4*>(stage_o + k_pos(r, ch));
+    }
+  }
+}
+
 // ------------------------------------------------------------------ fp32 / SIMT
 constexpr int kF32Keys = 32;
 
@@ -499,12 +826,16 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   a.out = L.out;
   a.lse = L.lse;
   const int rows = L.group_size < L.lq ? L.group_size : L.lq;
-  const int rows_per_wg = g.dtype == 0 ? kWaves * 32 : kWave;
+  // bf16, d = 128 and groups of more than 32 rows: 64 rows per wave; else 32
+  const bool r64 = g.dtype == 0 && g.D == 128 && rows > 32;
+  const int rows_per_wg = g.dtype != 0 ? kWave : r64 ? kR64Waves * 64 : kWaves * 32;
   a.tiles_per_group = (rows + rows_per_wg - 1) / rows_per_wg;
   const int64_t nwg = static_cast<int64_t>(g.H) * L.R * a.tiles_per_group;
   if (nwg <= 0) return hipSuccess;
   if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-  if (g.dtype == 0) {
+  if (r64) {
+    hipLaunchKernelGGL(k_attn_bf16_r64<128>, dim3(static_cast<unsigned>(nwg)), dim3(kR64Waves * kWave), 0, stream, a);
+  } else if (g.dtype == 0) {
     if (g.D == 128)
       hipLaunchKernelGGL(k_attn_bf16<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWaves * kWave), 0, stream, a);
     else
