@@ -24,10 +24,12 @@ FLAGS = [
 ]
 
 
-# Per-source extra flags.  The 64-row attention kernel needs more than 256 registers
-# per lane; MFMA results in arch VGPRs (not accumulation registers) keep its softmax
-# VALU work free of register-file copies.
-EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+# Per-source extra flags for attention.hip.  The 64-row attention kernel needs more
+# than 256 registers per lane; MFMA results in arch VGPRs (not accumulation
+# registers) keep its softmax VALU work free of register-file copies.  Without
+# IEEE-mode NaN quieting, fmaxf over MFMA results maps to plain v_max3 (no NaN is
+# ever produced or consumed on purpose there).
+EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans", "-mno-amdgpu-ieee"]}
 
 
 def build(verbose: bool = False) -> str:

@@ -414,12 +414,12 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
 // from inside the wave: the instruction stream alternates MFMAs of one half with
 // the softmax VALU work of the other (QK of half 1 with the exponentials of half
 // 0, PV of half 0 with the exponentials of half 1), and MFMAs run asynchronously.
-// The running max may lag the true one by up to kRescaleSlack (log2 units), so O
-// and l are rescaled only when a row's max grows by more than that; exponentials
-// are then at most 2^kRescaleSlack, well inside fp32 and bf16 range, and the final
-// normalisation cancels the stale max exactly.
+// The running max may lag the true one: O and l are rescaled only when exponentials
+// against the stale max could exceed 2^8, well inside fp32 and bf16 range, and the
+// final normalisation cancels the stale max exactly.
 constexpr int kR64Waves = 4;
-constexpr float kRescaleSlack = 8.0f;
+constexpr float kSlackSum = 256.0f;  // 2^8: how far exponentials may exceed 1 before O is rescaled
+constexpr float kNoMax = -1.0e30f;   // initial running max: finite, below any score (first tile rescales)
 
 // max / sum of a value over the lane pair (l, l ^ 32)
 __device__ __forceinline__ float pair_max(float v) {
@@ -432,7 +432,8 @@ __device__ __forceinline__ float pair_sum(float v) {
 }
 
 // Pins values at this point of the instruction stream: the exponentials of one half
-// are computed between the other half's MFMAs, not moved down to their first use.
+// are computed between the other half's MFMAs, not moved down past the check that
+// follows them to their first use.
 __device__ __forceinline__ void keep_here(const bf16x8 (&pb)[4], float l) {
   asm volatile("" ::"v"(pb[0]), "v"(pb[1]), "v"(pb[2]), "v"(pb[3]), "v"(l));
 }
@@ -448,12 +449,6 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("" ::: "memory");
 }
 
-// Buffer resource over `bytes` bytes at p (raw, unswizzled; offsets at or past the
-// end read as zero).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), 0, bytes, 0x00020000);
-}
-
 // LDS tiles of the 64-row kernel: 64 rows of 256 bytes (d = 128 bf16), unpadded, with
 // the 16-byte chunks of each row permuted so that both the K fragment reads and the
 // transposing V reads touch every bank once per pass:
@@ -466,6 +461,38 @@ constexpr int kR64TileBytes = kTileKeys * 128 * 2;
 __device__ __forceinline__ int k_pos(int r, int c) { return r * 256 + ((c ^ (r & 15)) << 4); }
 __device__ __forceinline__ int v_pos(int r, int c) { return r * 256 + ((c ^ (4 * (r & 3))) << 4); }
 
+// s_waitcnt operand that waits for at most n outstanding vector-memory operations
+// and for nothing else (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
+constexpr int vmcnt_only(int n) { return (n & 0xF) | ((n >> 4) << 14) | (0x7 << 4) | (0xF << 8); }
+
+// Buffer resource (raw, stride 0) over `bytes` bytes at p, in scalar registers; the
+// caller guarantees p and bytes are the same in every lane.  Offsets at or past the
+// end read as zero.
+__device__ __forceinline__ u32x4 buffer_rsrc(const void* p, int bytes) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  u32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u));
+  r[1] = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(u >> 32) & 0xffffu);
+  r[2] = __builtin_amdgcn_readfirstlane(static_cast<uint32_t>(bytes));
+  r[3] = 0x00020000u;
+  return r;
+}
+
+__device__ __forceinline__ uint32_t lds_offset(const void* p) {
+  return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+// One buffer-to-LDS DMA instruction: lane l's 16 bytes at rsrc + voffset land at LDS
+// byte lds + 16 l.  It is written as inline asm so that the compiler does not track
+// it as an LDS store (it would make every later LDS read wait for all DMA in flight);
+// the kernel orders it itself, with explicit vmcnt waits before the barriers that
+// publish a stage.
+__device__ __forceinline__ void dma_16x64(u32x4 rsrc, int voffset, uint32_t lds) {
+  // M0 (the LDS destination) is set by the compiler; the s_nop is the wait state an
+  // LDS DMA needs after an M0 write
+  asm volatile("s_nop 0\n\tbuffer_load_dwordx4 %0, %1, 0 offen lds" ::"v"(voffset), "s"(rsrc), "{m0}"(lds) : "memory");
+}
+
 template <int D>
 __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs a) {
   static_assert(D == 128, "the 64-row kernel is laid out for d = 128");
@@ -474,10 +501,10 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   constexpr int DT = D / 32;
   constexpr int KK = D / 16;
   constexpr int DMA_PER_WAVE = kR64TileBytes / 1024 / kR64Waves;  // 1 KB DMA instructions per wave, K and V each
-  // three stages (K and V each), separate objects so that the compiler can tell a
-  // stage being read from the stages still being filled
-  __shared__ __attribute__((aligned(1024))) uint8_t k_st0[kR64TileBytes], k_st1[kR64TileBytes], k_st2[kR64TileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v_st0[kR64TileBytes], v_st1[kR64TileBytes], v_st2[kR64TileBytes];
+  // three stages of K and V: one tile's V being read, the next tile's K being read,
+  // the tile after it arriving
+  __shared__ __attribute__((aligned(1024))) uint8_t k_ring[3 * kR64TileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_ring[3 * kR64TileBytes];
   __shared__ int2 table[2 * NT];
   __shared__ int scan_tmp[kR64Waves];
 
@@ -519,12 +546,15 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       o1[dt][i] = 0.f;
     }
   // running max in scaled log2 units (max * scale * log2 e) and this lane's share of l
-  float ms0 = -INFINITY, ms1 = -INFINITY, l0 = 0.f, l1 = 0.f;
+  float ms0 = kNoMax, ms1 = kNoMax, l0 = 0.f, l1 = 0.f;
   const float c = a.scale * kLog2e;
 
   // ---- tile sequence: (page, sub-tile << 8 | valid keys), from the decoded table
   int next_entry = 0, ntab = 0, ti = 0;
-  auto next_tile = [&]() -> int2 {  // workgroup-uniform; refills the table (barriers) when it runs out
+  // The next table entry as read from LDS (the same in every lane; made scalar where
+  // used, so that the read's latency is not waited for here).  Called by every thread
+  // together: it refills the table (with barriers) when it runs out.
+  auto next_tile_raw = [&]() -> int2 {
     if (ti == ntab) {
       ntab = 0;
       ti = 0;
@@ -534,10 +564,10 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       }
       if (ntab == 0) return make_int2(0, 0);  // past the end: an empty tile
     }
-    int2 m = table[ti++];
-    m.x = __builtin_amdgcn_readfirstlane(m.x);
-    m.y = __builtin_amdgcn_readfirstlane(m.y);
-    return m;
+    return table[ti++];
+  };
+  auto scalar_tile = [](int2 m) {
+    return make_int2(__builtin_amdgcn_readfirstlane(m.x), __builtin_amdgcn_readfirstlane(m.y));
   };
   // this lane's source offsets for its DMA instructions (row 4 m + lane / 16, m = wave + 4 i)
   int k_src[DMA_PER_WAVE], v_src[DMA_PER_WAVE];
@@ -547,155 +577,208 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     k_src[i] = r * 256 + ((p ^ (r & 15)) << 4);
     v_src[i] = r * 256 + ((p ^ (4 * (r & 3))) << 4);
   }
-  typedef __attribute__((address_space(3))) void lds_void;
-  auto issue = [&](int2 m, uint8_t* kst, uint8_t* vst) {  // empty tiles load nothing and write zeros
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);  // scalar copy: LDS destinations go to M0
+  // the DMA of tile m into stage st, instruction i of K and of V (empty tiles load
+  // nothing and write zeros); m is workgroup-uniform
+  auto issue_part = [&](int2 m, int st, int i) {
     const int sub = m.y >> 8, nv = m.y & 255;
     const int64_t slab = (static_cast<int64_t>(m.x) * a.H + h) * a.B * D + static_cast<int64_t>(sub) * kTileKeys * D;
-    const __amdgpu_buffer_rsrc_t kr = make_rsrc(kp + slab, nv * D * 2);
-    const __amdgpu_buffer_rsrc_t vr = make_rsrc(vp + slab, nv * D * 2);
-#pragma unroll
-    for (int i = 0; i < DMA_PER_WAVE; ++i) {
-      const int mi = wave + kR64Waves * i;
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void*)(kst + mi * 1024), 16, k_src[i], 0, 0, 0);
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void*)(vst + mi * 1024), 16, v_src[i], 0, 0, 0);
-    }
+    const u32x4 kr = buffer_rsrc(kp + slab, nv * D * 2), vr = buffer_rsrc(vp + slab, nv * D * 2);
+    const uint32_t off = st * kR64TileBytes + (wave_s + kR64Waves * i) * 1024;
+    dma_16x64(kr, k_src[i], lds_offset(k_ring) + off);
+    dma_16x64(vr, v_src[i], lds_offset(v_ring) + off);
   };
+  auto issue = [&](int2 m, int st) {
+#pragma unroll
+    for (int i = 0; i < DMA_PER_WAVE; ++i) issue_part(m, st, i);
+  };
+;
 
-  // row max of a half over the tile, scaled; keys past the block's end are masked
-  auto tile_max = [&](f32x16 (&s)[2], int nvalid) -> float {
-    if (nvalid < kTileKeys) {
-#pragma unroll
-      for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
-          if (key >= nvalid) s[t2][i] = -INFINITY;
-        }
-    }
-    float m = s[0][0];
+  // keys past the block's end of a partial tile get -inf scores (the key base goes
+  // through an empty asm so that none of this is computed ahead of the rare branch)
+  auto mask_tail = [&](f32x16 (&s)[2], int nvalid) {
+    int kb = 8 * half;
+    asm volatile("" : "+v"(kb));
 #pragma unroll
     for (int t2 = 0; t2 < 2; ++t2)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) m = fmaxf(m, s[t2][i]);
-    return pair_max(m) * c;
+      for (int i = 0; i < 16; ++i) {
+        const int key = 32 * t2 + (i < 8 ? kb + i : 16 + kb + (i - 8));
+        if (key >= nvalid) s[t2][i] = -INFINITY;
+      }
   };
-  auto rescale = [&](float mt, float& ms, float& l, f32x16 (&o)[DT]) {
-    if (__any(mt > ms + kRescaleSlack)) {
-      const float m_new = fmaxf(ms, mt);
-      const float alpha = ms == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(ms - m_new);
+  // Exponentials of elements 2i and 2i + 1 of a half's S tile against the running max
+  // ms, packed into the bf16 P^T operand; acc sums the packed bf16 values (the P that
+  // multiplies V).
+  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
+  auto exp_pair = [&](const f32x16 (&s)[2], float ms, float& acc, bf16x8 (&pb)[4], int i) {
+    const int t2 = i / 8, e = (2 * i) % 16;
+    const float x0 = s[t2][e], x1 = s[t2][e + 1];
+    const __bf16 b0 = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(x0, c, -ms)));
+    const __bf16 b1 = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(x1, c, -ms)));
+    const bf16x2 pk = {b0, b1};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc, false);
+    pb[2 * t2 + e / 8][e % 8] = b0;
+    pb[2 * t2 + e / 8][e % 8 + 1] = b1;
+  };
+  // The exponentials of a half are computed against its running max before the
+  // tile's own max is known.  They stand (every p <= 2^8) unless some lane's sum of
+  // them exceeds 2^8 or overflowed; only then is the tile max taken, O and l moved to
+  // it and the exponentials redone.
+  auto settle = [&](const f32x16 (&s)[2], float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4]) {
+    if (__any(acc > kSlackSum)) {
+      float m0 = fmaxf(s[0][0], s[1][0]), m1 = fmaxf(s[0][1], s[1][1]);
+#pragma unroll
+      for (int i = 2; i < 16; i += 2) {
+        m0 = fmaxf(m0, fmaxf(s[0][i], s[1][i]));
+        m1 = fmaxf(m1, fmaxf(s[0][i + 1], s[1][i + 1]));
+      }
+      const float m_new = fmaxf(ms, pair_max(fmaxf(m0, m1)) * c);
+      const float alpha = __builtin_amdgcn_exp2f(ms - m_new);
       l *= alpha;
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
         for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
       ms = m_new;
+      acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) exp_pair(s, ms, acc, pb, i);
     }
-  };
-  // exponentials of elements 2i and 2i + 1 of a half's S tile (i < 16): p = 2^(s c - ms),
-  // packed into the bf16 P^T operand and summed into two partial row sums
-  auto exp_pair = [&](const f32x16 (&s)[2], float ms, float (&acc)[2], bf16x8 (&pb)[4], int i) {
-    const int t2 = i / 8, e = (2 * i) % 16;
-    const float p0 = __builtin_amdgcn_exp2f(fmaf(s[t2][e], c, -ms));
-    const float p1 = __builtin_amdgcn_exp2f(fmaf(s[t2][e + 1], c, -ms));
-    acc[0] += p0;
-    acc[1] += p1;
-    pb[2 * t2 + e / 8][e % 8] = static_cast<__bf16>(p0);
-    pb[2 * t2 + e / 8][e % 8 + 1] = static_cast<__bf16>(p1);
+    l += acc;
   };
 
   const int krow = s_row_perm(lane % 32);
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  // one tile from stage (kst, vst); the tile after next goes into (kst2, vst2)
-  auto step = [&](int2 cur, int2 after_next, const uint8_t* kst, const uint8_t* vst, uint8_t* kst2, uint8_t* vst2) {
-    // this wave's DMA of the current tile is done (the next tile's DMA_PER_WAVE x 2
-    // instructions may still be in flight); the barrier then makes every wave's
-    // copies visible and frees the stage read one tile ago
-    __builtin_amdgcn_s_waitcnt(0xF70 | (2 * DMA_PER_WAVE));  // vmcnt(2 * DMA_PER_WAVE), expcnt and lgkmcnt not waited
-    lds_barrier();
-    issue(after_next, kst2, vst2);
-    if (!wave_live) return;
+  // ---- Software pipeline over tiles, three LDS stages (tile t in stage t mod 3).
+  // Iteration t runs four runs of 16 MFMAs, each carrying one exponential pair per
+  // two MFMA slots (the exponentials, a half-rate VALU op, fill the MFMA shadow only
+  // when spread this thin) plus LDS reads and DMA issues:
+  //   R1  QK of half 0 (tile t)     pairs 8-15 of half 1 (tile t-1), DMA of tile t+2
+  //   R2  PV of half 1 (tile t-1)   pairs 0-7 of half 0 (t), V^T fragments 0-7 of t
+  //   R3  QK of half 1 (t)          pairs 8-15 of half 0 (t), V^T fragments 8-15 of t
+  //   R4  PV of half 0 (t)          pairs 0-7 of half 1 (t), K fragments of tile t+1
+  // with half 1's softmax check after R1 and half 0's after R3, each ahead of the PV
+  // run that consumes its P.  One barrier per iteration, before R4: tile t+1 has
+  // landed (for its K fragments) and every wave is past the reads of tile t (its
+  // stage takes the DMA of tile t+3 in the next iteration's R1).  Before the first
+  // iteration, "tile -1" is an all-masked dummy (P = 0, V^T = 0).
+  bf16x8 kf[2][KK], vf[4][DT];
+  auto read_kf = [&](const uint8_t* kst, int i) {  // fragment i = (t2, kk)
+    kf[i / KK][i % KK] = *reinterpret_cast<const bf16x8*>(kst + k_pos(32 * (i / KK) + krow, 2 * (i % KK) + half));
+  };
+  auto read_vf = [&](const uint8_t* vst, int i) {  // fragment i = (j, dt): two transposing reads
+    const int j = i / DT, dt = i % DT;
+    const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+    const int ch = 4 * dt + 2 * ((lane / 16) % 2) + (lane % 4) / 2, b8 = 8 * (lane % 2);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0, ch) + b8));
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0 + 4, ch) + b8));
+    vf[j][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  f32x16 s0[2], s1[2];
+  bf16x8 pb0[4], pb1[4];
+  float acc1 = 0.f;
+#pragma unroll
+  for (int t2i = 0; t2i < 2; ++t2i)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s1[t2i][i] = -INFINITY;  // the dummy tile -1
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    pb1[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) vf[j][dt] = pb1[j];
+  }
+  int2 cur = scalar_tile(next_tile_raw());
+  int2 t1 = scalar_tile(next_tile_raw());
+  issue(cur, 0);
+  issue(t1, 1);
+  // Everything issued so far lands (the Q loads included): the compiler then knows
+  // no vector-memory load of its own is pending in the loop, where any wait it
+  // inserted would also drain the DMA in flight, which it does not see.
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+  lds_barrier();
+  if (wave_live) {
+#pragma unroll
+    for (int i = 0; i < 2 * KK; ++i) read_kf(k_ring, i);
+  }
+  static_assert(2 * KK == 16 && 4 * DT == 16 && DMA_PER_WAVE == 4, "the MFMA runs are laid out for d = 128");
+  for (int t = 0; (cur.y & 255) != 0; ++t) {
+    const int2 t2 = scalar_tile(next_tile_raw());  // every thread; refills the table at its end
+    const int st = t % 3, st1 = (t + 1) % 3, st2 = (t + 2) % 3;
+    const uint8_t* kst1 = k_ring + st1 * kR64TileBytes;
+    const uint8_t* vst = v_ring + st * kR64TileBytes;
     const int cur_nvalid = cur.y & 255;
-    // ---- S^T = K Q^T for both halves; each K fragment feeds two MFMAs
-    bf16x8 kf[2][KK];
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
-#pragma unroll
-      for (int kk = 0; kk < KK; ++kk)
-        kf[t2][kk] = *reinterpret_cast<const bf16x8*>(kst + k_pos(32 * t2 + krow, 2 * kk + half));
-    f32x16 s0[2], s1[2];
-#pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
+    if (wave_live) {
+      float acc0 = 0.f;
+      // ---- R1: QK of half 0, pairs 8-15 of half 1 of the previous tile, DMA of tile t+2
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        s0[t2][i] = 0.f;
-        s1[t2][i] = 0.f;
+        s0[i / 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / 8][i % 8], q0[i % 8], i % 8 ? s0[i / 8] : f32x16{},
+                                                            0, 0, 0);
+        if (i % 2 == 0) exp_pair(s1, ms1, acc1, pb1, 8 + i / 2);
+        else if (i / 2 < DMA_PER_WAVE) issue_part(t2, st2, i / 2);
+        __builtin_amdgcn_sched_barrier(0);
       }
+      keep_here(pb1, acc1);
+      settle(s1, ms1, l1, acc1, o1, pb1);
+      if (cur_nvalid < kTileKeys) mask_tail(s0, cur_nvalid);
+      // ---- R2: PV of half 1 of the previous tile, pairs 0-7 of half 0, V^T fragments
+      // 0-7 of this tile (each read into the registers its PV MFMA has just used)
 #pragma unroll
-    for (int t2 = 0; t2 < 2; ++t2)
+      for (int i = 0; i < 16; ++i) {
+        o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
+        if (i % 2 == 0) exp_pair(s0, ms0, acc0, pb0, i / 2);
+        if (i < 8) read_vf(vst, i);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      // ---- R3: QK of half 1, pairs 8-15 of half 0, V^T fragments 8-15
 #pragma unroll
-      for (int kk = 0; kk < KK; ++kk) s0[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t2][kk], q0[kk], s0[t2], 0, 0, 0);
-    rescale(tile_max(s0, cur_nvalid), ms0, l0, o0);
-    // ---- QK of half 1, one MFMA per pair of half-0 exponentials (the fences keep
-    // the interleaving: the wave issues in order and MFMAs run asynchronously)
-    bf16x8 pb0[4], pb1[4];
-    float acc0[2] = {0.f, 0.f}, acc1[2] = {0.f, 0.f};
-#pragma unroll
-    for (int i = 0; i < 2 * KK; ++i) {
-      s1[i / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / KK][i % KK], q1[i % KK], s1[i / KK], 0, 0, 0);
-      exp_pair(s0, ms0, acc0, pb0, i);
-      __builtin_amdgcn_sched_barrier(0);
+      for (int i = 0; i < 16; ++i) {
+        s1[i / 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / 8][i % 8], q1[i % 8], i % 8 ? s1[i / 8] : f32x16{},
+                                                            0, 0, 0);
+        if (i % 2 == 0) exp_pair(s0, ms0, acc0, pb0, 8 + i / 2);
+        if (i % 2 == 1) read_vf(vst, 8 + i / 2);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      keep_here(pb0, acc0);
+      settle(s0, ms0, l0, acc0, o0, pb0);
+      if (cur_nvalid < kTileKeys) mask_tail(s1, cur_nvalid);
+    } else {
+      issue(t2, st2);
     }
-    l0 += acc0[0] + acc0[1];
-    keep_here(pb0, l0);
-    rescale(tile_max(s1, cur_nvalid), ms1, l1, o1);
-    // ---- O^T += V^T P^T: PV of half 0 between pairs of half-1 exponentials, then PV of half 1
-    bf16x8 vf[4][DT];
+    // ---- tile t+1 has landed (the DMA of tile t+2 may still be in flight) and every
+    // wave is past its reads of tile t
+    __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * DMA_PER_WAVE));
+    lds_barrier();
+    if (wave_live) {
+      // ---- R4: PV of half 0, pairs 0-7 of half 1, K fragments of the next tile
+      acc1 = 0.f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int ch = 4 * dt + 2 * ((lane / 16) % 2) + (lane % 4) / 2, b8 = 8 * (lane % 2);
-        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0, ch) + b8));
-        const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0 + 4, ch) + b8));
-        vf[j][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      for (int i = 0; i < 16; ++i) {
+        o0[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb0[i / DT], o0[i % DT], 0, 0, 0);
+        if (i % 2 == 0) exp_pair(s1, ms1, acc1, pb1, i / 2);
+        read_kf(kst1, i);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int i = 0; i < 4 * DT; ++i) {
-      o0[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb0[i / DT], o0[i % DT], 0, 0, 0);
-      exp_pair(s1, ms1, acc1, pb1, i);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    l1 += acc1[0] + acc1[1];
-#pragma unroll
-    for (int i = 0; i < 4 * DT; ++i)
-      o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
-  };
-
-  // ---- prologue: the first two tiles in flight; then three tiles per round, one per stage
-  int2 t0 = next_tile(), t1 = next_tile();
-  issue(t0, k_st0, v_st0);
-  issue(t1, k_st1, v_st1);
-  while ((t0.y & 255) != 0) {
-    int2 t2 = next_tile();
-    step(t0, t2, k_st0, v_st0, k_st2, v_st2);
-    if ((t1.y & 255) == 0) break;
-    int2 t3 = next_tile();
-    step(t1, t3, k_st1, v_st1, k_st0, v_st0);
-    if ((t2.y & 255) == 0) break;
-    int2 t4 = next_tile();
-    step(t2, t4, k_st2, v_st2, k_st1, v_st1);
-    t0 = t3;
-    t1 = t4;
+    cur = t1;
+    t1 = t2;
   }
-  __builtin_amdgcn_s_waitcnt(0xF70);  // vmcnt(0): no DMA may land in the stages reused below
+  // ---- drain: the last tile's half 1 (or the dummy when there was no tile)
+  if (wave_live) {
+#pragma unroll
+    for (int i = 8; i < 16; ++i) exp_pair(s1, ms1, acc1, pb1, i);
+    settle(s1, ms1, l1, acc1, o1, pb1);
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
+  }
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));  // no DMA may land in the stages reused below
   __syncthreads();
 
   // ---- epilogue: normalise, stage O through LDS (one 16 KB stage per wave, chunks
   // permuted like K), store rows with 16-byte writes
-  uint8_t* const stage_o = wave == 0 ? k_st0 : wave == 1 ? k_st1 : wave == 2 ? k_st2 : v_st0;
+  uint8_t* const stage_o = wave < 3 ? k_ring + wave * kR64TileBytes : v_ring;  // 64 rows x 256 B per wave
   auto finish = [&](f32x16 (&o)[DT], float ms, float l, int g) {
     const float l_tot = pair_sum(l);
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
