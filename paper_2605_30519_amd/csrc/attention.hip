@@ -19,6 +19,7 @@
 // f32 kernel (k_attn_f32): one lane per query row, fp32 dot products and exact
 // expf-based online softmax, for fp32 inputs.
 #include <math.h>
+#include <type_traits>
 
 #include "device_common.h"
 #include "launch.h"
@@ -481,6 +482,26 @@ __device__ __forceinline__ u32x4 buffer_rsrc(const void* p, int bytes) {
 __device__ __forceinline__ uint32_t lds_offset(const void* p) {
   return static_cast<uint32_t>(reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
 }
+// P V product with its accumulator in AccVGPRs.  Selected by the compiler, every
+// MFMA accumulator sits in the VGPRs that the softmax VALU work also uses, and an
+// MFMA writing its result there slows that work down; the asm keeps O in AccVGPRs.
+// The asm also hides the MFMA from the compiler's hazard checks, so the wait states
+// come from the callers: `lead` puts two before an MFMA whose P operand or
+// accumulator VALU code may just have written, and VALU code touches the
+// accumulators only after acc_settled().
+__device__ __forceinline__ void pv_mfma(f32x16& acc, const bf16x8& v, const bf16x8& p, bool lead) {
+  if (lead)
+    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(p));
+  else
+    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(p));
+}
+// Sixteen wait states (more than an 8-pass MFMA result needs) before VALU code reads
+// or writes the accumulators; they pass through the asm so that no access moves
+// ahead of it.
+__device__ __forceinline__ void acc_settled(f32x16 (&o)[4]) {
+  asm volatile("s_nop 7\n\ts_nop 7" : "+a"(o[0]), "+a"(o[1]), "+a"(o[2]), "+a"(o[3]));
+}
+
 
 // One buffer-to-LDS DMA instruction: lane l's 16 bytes at rsrc + voffset land at LDS
 // byte lds + 16 l.  It is written as inline asm so that the compiler does not track
@@ -501,10 +522,12 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   constexpr int DT = D / 32;
   constexpr int KK = D / 16;
   constexpr int DMA_PER_WAVE = kR64TileBytes / 1024 / kR64Waves;  // 1 KB DMA instructions per wave, K and V each
-  // three stages of K and V: one tile's V being read, the next tile's K being read,
-  // the tile after it arriving
-  __shared__ __attribute__((aligned(1024))) uint8_t k_ring[3 * kR64TileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t v_ring[3 * kR64TileBytes];
+  // Four stages of K and V, tile t in stage t mod 4: iteration t reads the K of tile t
+  // and the V of tile t - 1 while tile t + 1 has landed and tile t + 2 arrives in the
+  // stage of tile t - 2.
+  constexpr int kStages = 4;
+  __shared__ __attribute__((aligned(1024))) uint8_t k_ring[kStages * kR64TileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t v_ring[kStages * kR64TileBytes];
   __shared__ int2 table[2 * NT];
   __shared__ int scan_tmp[kR64Waves];
 
@@ -521,9 +544,18 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
   const uint16_t* vp = static_cast<const uint16_t*>(a.v_pages);
 
-  // Q^T B operands of the two halves: lane holds query wrow + 32 g + lane % 32
+  // Q^T B operands of the two halves: lane holds query wrow + 32 g + lane % 32.
+  // Q is scaled by c = scale * log2(e) (rounded back to bf16), so that the MFMAs
+  // produce scores in the scaled log2 units of the softmax directly.
+  const float c = a.scale * kLog2e;
   const int wrow = row0 + wave * 64;
   const bool wave_live = wrow < row_end;  // wave-uniform
+  auto prescale = [&](uint4 x) {
+    bf16x8 v = __builtin_bit_cast(bf16x8, x);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[e] = static_cast<__bf16>(static_cast<float>(v[e]) * c);
+    return v;
+  };
   bf16x8 q0[KK], q1[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
@@ -533,8 +565,10 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       x0 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r0) * a.H + h) * D + 16 * kk + 8 * half);
     if (r1 < row_end)
       x1 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r1) * a.H + h) * D + 16 * kk + 8 * half);
-    q0[kk] = __builtin_bit_cast(bf16x8, x0);
-    q1[kk] = __builtin_bit_cast(bf16x8, x1);
+    q0[kk] = prescale(x0);
+    q1[kk] = prescale(x1);
+    // Q lives in AccVGPRs next to O; the VGPRs hold S, P and the operand fragments
+    asm volatile("" : "+a"(q0[kk]), "+a"(q1[kk]));
   }
 
   f32x16 o0[DT], o1[DT];
@@ -547,7 +581,11 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     }
   // running max in scaled log2 units (max * scale * log2 e) and this lane's share of l
   float ms0 = kNoMax, ms1 = kNoMax, l0 = 0.f, l1 = 0.f;
-  const float c = a.scale * kLog2e;
+  // -max as the MFMA accumulator's initial value: S comes out as c s - max, the
+  // exponent itself
+  f32x16 nm0, nm1;
+#pragma unroll
+  for (int i = 0; i < 16; ++i) nm0[i] = nm1[i] = -kNoMax;
 
   // ---- tile sequence: (page, sub-tile << 8 | valid keys), from the decoded table
   int next_entry = 0, ntab = 0, ti = 0;
@@ -592,7 +630,6 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
 #pragma unroll
     for (int i = 0; i < DMA_PER_WAVE; ++i) issue_part(m, st, i);
   };
-;
 
   // keys past the block's end of a partial tile get -inf scores (the key base goes
   // through an empty asm so that none of this is computed ahead of the rare branch)
@@ -607,89 +644,161 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         if (key >= nvalid) s[t2][i] = -INFINITY;
       }
   };
-  // Exponentials of elements 2i and 2i + 1 of a half's S tile against the running max
-  // ms, packed into the bf16 P^T operand; acc sums the packed bf16 values (the P that
-  // multiplies V).
-  const bf16x2 ones = {static_cast<__bf16>(1.0f), static_cast<__bf16>(1.0f)};
-  auto exp_pair = [&](const f32x16 (&s)[2], float ms, float& acc, bf16x8 (&pb)[4], int i) {
-    const int t2 = i / 8, e = (2 * i) % 16;
-    const float x0 = s[t2][e], x1 = s[t2][e + 1];
-    const __bf16 b0 = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(x0, c, -ms)));
-    const __bf16 b1 = static_cast<__bf16>(__builtin_amdgcn_exp2f(fmaf(x1, c, -ms)));
-    const bf16x2 pk = {b0, b1};
-    acc = __builtin_amdgcn_fdot2_f32_bf16(pk, ones, acc, false);
-    pb[2 * t2 + e / 8][e % 8] = b0;
-    pb[2 * t2 + e / 8][e % 8 + 1] = b1;
+  // A half's softmax as a stream over its 32 S elements per lane (element E is
+  // s[E / 16][E % 16], already c s - max; it lands in P^T fragment E / 8 at position
+  // E % 8).  Slot g takes the exponential of element g, adds element g - 1 to the row
+  // sum and, on odd slots, packs elements g - 3 and g - 2 into P (not earlier: the
+  // PV run that carries slots 0-15 still reads the previous tile's P fragment 0 up
+  // to the MFMA of slot 3).  No op of a slot reads a result of the same slot, so a
+  // slot placed next to one MFMA issues without waiting on VALU latency; slots 32 and
+  // 33 finish the stream.  Each result goes through an empty asm so that the IR
+  // passes keep it in its slot (they would otherwise sink every op next to its first
+  // use).  The row sum is taken over the fp32 values.
+  auto soft_slot = [&](const f32x16 (&s)[2], float& acc, bf16x8 (&pb)[4], float (&uq)[32], int g) {
+    if (g < 32) {
+      uq[g] = __builtin_amdgcn_exp2f(s[g / 16][g % 16]);
+      asm volatile("" : "+v"(uq[g]));
+    }
+    if (g >= 1 && g <= 32) {
+      acc += uq[g - 1];
+      asm volatile("" : "+v"(acc));
+    }
+    if (g % 2 == 1 && g >= 3 && g <= 33) {
+      const int e = g - 3;
+      bf16x2 pk = {static_cast<__bf16>(uq[e]), static_cast<__bf16>(uq[e + 1])};
+      asm volatile("" : "+v"(pk));
+      pb[e / 8][e % 8] = pk[0];
+      pb[e / 8][e % 8 + 1] = pk[1];
+    }
+  };
+  const int krow = s_row_perm(lane % 32);
+  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+  // Operand fragments, read from LDS two fragments ahead of the MFMAs that use them.
+  // The lane's part of each address is fixed for the whole loop (8 K and 4 V byte
+  // offsets, the chunk permutations depending only on the lane); the stage, the key
+  // group and the ring base are compile-time constants that fold into the reads'
+  // offset fields.
+  // (masked to the 18 bits of the LDS address space, which lets the compiler see that
+  // base + constant cannot wrap)
+  uint32_t k_lane[KK], v_lane[DT];
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) k_lane[kk] = (lds_offset(k_ring) + k_pos(krow, 2 * kk + half)) & 0x3ffffu;
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+    const int key0 = 8 * half + (lane % 16) / 4;
+    const int ch = 4 * dt + 2 * ((lane / 16) % 2) + (lane % 4) / 2;
+    v_lane[dt] = (lds_offset(v_ring) + v_pos(key0, ch) + 8 * (lane % 2)) & 0x3ffffu;
+  }
+  typedef __attribute__((address_space(3))) const uint8_t lds_u8;
+  auto k_frag = [&](int st, int f) {  // f = 8 t2 + kk: keys 32 t2 .., k-step kk
+    lds_u8* p = reinterpret_cast<lds_u8*>(static_cast<uintptr_t>(k_lane[f % KK])) + (st * kR64TileBytes + (f / KK) * 32 * 256);
+    return *reinterpret_cast<__attribute__((address_space(3))) const bf16x8*>(p);
+  };
+  auto v_frag = [&](int st, int f) {  // f = 4 j + dt: keys 16 j .., d 32 dt ..; two transposing reads (keys +4)
+    lds_u8* p = reinterpret_cast<lds_u8*>(static_cast<uintptr_t>(v_lane[f % DT])) + (st * kR64TileBytes + (f / DT) * 16 * 256);
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)p);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(p + 4 * 256));
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
   // The exponentials of a half are computed against its running max before the
   // tile's own max is known.  They stand (every p <= 2^8) unless some lane's sum of
-  // them exceeds 2^8 or overflowed; only then is the tile max taken, O and l moved to
-  // it and the exponentials redone.
-  auto settle = [&](const f32x16 (&s)[2], float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4]) {
+  // them exceeds 2^8 or overflowed; only then is the tile's S formed again from the K
+  // still in LDS (stage kst, nvalid keys), its max taken, O and l moved to the new max
+  // and the exponentials redone.  The next tile's S (sn), already formed against the
+  // old max, is moved to the new one too; while the old max is still the initial
+  // placeholder its values are meaningless, and they are left to overflow, which
+  // settles that tile the same way.
+  auto settle = [&](float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4], f32x16& nm,
+                    const bf16x8 (&q)[KK], int kst, int nvalid, f32x16 (&sn)[2]) {
     if (__any(acc > kSlackSum)) {
+      f32x16 s[2];
+#pragma unroll
+      for (int f = 0; f < 2 * KK; ++f) {
+        s[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k_frag(kst, f), q[f % KK], f % KK ? s[f / KK] : f32x16{}, 0,
+                                                           0, 0);
+        __builtin_amdgcn_sched_barrier(0);  // one fragment at a time: this path must not raise register use
+      }
+      if (nvalid < kTileKeys) mask_tail(s, nvalid);
       float m0 = fmaxf(s[0][0], s[1][0]), m1 = fmaxf(s[0][1], s[1][1]);
 #pragma unroll
       for (int i = 2; i < 16; i += 2) {
         m0 = fmaxf(m0, fmaxf(s[0][i], s[1][i]));
         m1 = fmaxf(m1, fmaxf(s[0][i + 1], s[1][i + 1]));
       }
-      const float m_new = fmaxf(ms, pair_max(fmaxf(m0, m1)) * c);
+      const float m_new = fmaxf(ms, pair_max(fmaxf(m0, m1)));
       const float alpha = __builtin_amdgcn_exp2f(ms - m_new);
       l *= alpha;
+      acc_settled(o);
+      // one 16-register block at a time through VGPRs (O stays in AccVGPRs)
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
+      for (int dt = 0; dt < DT; ++dt) {
+        f32x16 t = o[dt];
+        asm volatile("" : "+v"(t));
 #pragma unroll
-        for (int i = 0; i < 16; ++i) o[dt][i] *= alpha;
+        for (int i = 0; i < 16; ++i) t[i] *= alpha;
+        o[dt] = t;
+        asm volatile("" : "+a"(o[dt]));
+      }
+      const float shift = ms == kNoMax ? 0.f : m_new - ms;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        sn[0][i] -= shift;
+        sn[1][i] -= shift;
+      }
       ms = m_new;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) nm[i] = -m_new;
       acc = 0.f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) exp_pair(s, ms, acc, pb, i);
+      for (int e = 0; e < 32; e += 2) {
+        const float p0 = __builtin_amdgcn_exp2f(s[e / 16][e % 16] - m_new);
+        const float p1 = __builtin_amdgcn_exp2f(s[e / 16][e % 16 + 1] - m_new);
+        acc += p0 + p1;
+        pb[e / 8][e % 8] = static_cast<__bf16>(p0);
+        pb[e / 8][e % 8 + 1] = static_cast<__bf16>(p1);
+      }
     }
     l += acc;
   };
 
-  const int krow = s_row_perm(lane % 32);
-  typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  // ---- Software pipeline over tiles, three LDS stages (tile t in stage t mod 3).
-  // Iteration t runs four runs of 16 MFMAs, each carrying one exponential pair per
-  // two MFMA slots (the exponentials, a half-rate VALU op, fill the MFMA shadow only
-  // when spread this thin) plus LDS reads and DMA issues:
-  //   R1  QK of half 0 (tile t)     pairs 8-15 of half 1 (tile t-1), DMA of tile t+2
-  //   R2  PV of half 1 (tile t-1)   pairs 0-7 of half 0 (t), V^T fragments 0-7 of t
-  //   R3  QK of half 1 (t)          pairs 8-15 of half 0 (t), V^T fragments 8-15 of t
-  //   R4  PV of half 0 (t)          pairs 0-7 of half 1 (t), K fragments of tile t+1
-  // with half 1's softmax check after R1 and half 0's after R3, each ahead of the PV
-  // run that consumes its P.  One barrier per iteration, before R4: tile t+1 has
-  // landed (for its K fragments) and every wave is past the reads of tile t (its
-  // stage takes the DMA of tile t+3 in the next iteration's R1).  Before the first
-  // iteration, "tile -1" is an all-masked dummy (P = 0, V^T = 0).
-  bf16x8 kf[2][KK], vf[4][DT];
-  auto read_kf = [&](const uint8_t* kst, int i) {  // fragment i = (t2, kk)
-    kf[i / KK][i % KK] = *reinterpret_cast<const bf16x8*>(kst + k_pos(32 * (i / KK) + krow, 2 * (i % KK) + half));
-  };
-  auto read_vf = [&](const uint8_t* vst, int i) {  // fragment i = (j, dt): two transposing reads
-    const int j = i / DT, dt = i % DT;
-    const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
-    const int ch = 4 * dt + 2 * ((lane / 16) % 2) + (lane % 4) / 2, b8 = 8 * (lane % 2);
-    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0, ch) + b8));
-    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(vst + v_pos(key0 + 4, ch) + b8));
-    vf[j][dt] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-  };
-  f32x16 s0[2], s1[2];
+  // ---- Software pipeline over tiles.  Iteration t runs two runs of 32 MFMAs, each
+  // MFMA carrying one softmax stream slot (one exponential, a half-rate VALU op, and
+  // two or three other VALU ops fill the MFMA shadow only when spread this thin):
+  //   QK run  S of tile t, both halves (each K fragment feeds the two halves' MFMAs
+  //           back to back); slots 16-33 of tile t-1's two streams; DMA of tile t+2
+  //   PV run  O += P V of tile t-1, both halves (each V^T fragment feeds two MFMAs);
+  //           slots 0-15 of tile t's two streams
+  // with both halves' softmax checks of tile t-1 between the runs.  Operand fragments
+  // are read just in time, so the registers hold S of two tiles and P of one.  One
+  // barrier per iteration, at its end: tile t+1 has landed and every wave is past its
+  // reads of the stages that the next iteration's DMA refills.  "Tile -1" is an
+  // all-masked dummy (S = -inf, P = 0, its V stage DMA'd from an empty tile: zeros),
+  // and the sequence ends with one empty tile whose iteration finishes the last one.
+  static_assert(2 * KK == 16 && 4 * DT == 16 && DMA_PER_WAVE == 4, "the MFMA runs are laid out for d = 128");
+  f32x16 sa0[2], sa1[2], sb0[2], sb1[2];
   bf16x8 pb0[4], pb1[4];
-  float acc1 = 0.f;
+  float acc0 = 0.f, acc1 = 0.f;
+  // the two halves' softmax streams (only a few elements of each are live at a time)
+  float uq0[32], uq1[32];
 #pragma unroll
   for (int t2i = 0; t2i < 2; ++t2i)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) s1[t2i][i] = -INFINITY;  // the dummy tile -1
+    for (int i = 0; i < 16; ++i) {
+      sa0[t2i][i] = -INFINITY;
+      sa1[t2i][i] = -INFINITY;
+    }
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
-    pb1[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) vf[j][dt] = pb1[j];
+    pb0[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
+    pb1[j] = pb0[j];
   }
+  uq0[13] = uq0[14] = uq0[15] = 0.f;  // the dummy tile's streams enter the loop at slot 16
+  uq1[13] = uq1[14] = uq1[15] = 0.f;
+  int prev_nvalid = 0;
+
   int2 cur = scalar_tile(next_tile_raw());
   int2 t1 = scalar_tile(next_tile_raw());
+  issue(make_int2(0, 0), kStages - 1);  // V of tile -1
   issue(cur, 0);
   issue(t1, 1);
   // Everything issued so far lands (the Q loads included): the compiler then knows
@@ -697,88 +806,93 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   // inserted would also drain the DMA in flight, which it does not see.
   __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
   lds_barrier();
-  if (wave_live) {
-#pragma unroll
-    for (int i = 0; i < 2 * KK; ++i) read_kf(k_ring, i);
-  }
-  static_assert(2 * KK == 16 && 4 * DT == 16 && DMA_PER_WAVE == 4, "the MFMA runs are laid out for d = 128");
-  for (int t = 0; (cur.y & 255) != 0; ++t) {
+
+  // Iteration t (t mod 4 = T, a compile-time constant, as are the stages) with tile
+  // t-1's S in (so0, so1) and tile t's formed in (sn0, sn1); consecutive iterations
+  // swap the two, so that no S is ever copied.  Returns false after the iteration of
+  // the empty tile that ends the sequence.
+  auto iteration = [&](f32x16 (&so0)[2], f32x16 (&so1)[2], f32x16 (&sn0)[2], f32x16 (&sn1)[2], auto tmod) {
+    constexpr int T = decltype(tmod)::value;
+    constexpr int kst = T, vst = (T + kStages - 1) % kStages, st2 = (T + 2) % kStages;
+    bf16x8 kf[2 * KK], vf[4 * DT];
+    if (wave_live) {
+      kf[0] = k_frag(kst, 0);
+      kf[1] = k_frag(kst, 1);
+    }
     const int2 t2 = scalar_tile(next_tile_raw());  // every thread; refills the table at its end
-    const int st = t % 3, st1 = (t + 1) % 3, st2 = (t + 2) % 3;
-    const uint8_t* kst1 = k_ring + st1 * kR64TileBytes;
-    const uint8_t* vst = v_ring + st * kR64TileBytes;
     const int cur_nvalid = cur.y & 255;
     if (wave_live) {
-      float acc0 = 0.f;
-      // ---- R1: QK of half 0, pairs 8-15 of half 1 of the previous tile, DMA of tile t+2
+      // ---- QK run
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s0[i / 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / 8][i % 8], q0[i % 8], i % 8 ? s0[i / 8] : f32x16{},
-                                                            0, 0, 0);
-        if (i % 2 == 0) exp_pair(s1, ms1, acc1, pb1, 8 + i / 2);
-        else if (i / 2 < DMA_PER_WAVE) issue_part(t2, st2, i / 2);
+      for (int i = 0; i < 32; ++i) {
+        const int f = i / 2;
+        if (i % 2 == 0) {
+          sn0[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q0[f % KK], f % KK ? sn0[f / KK] : nm0, 0, 0, 0);
+          soft_slot(so0, acc0, pb0, uq0, 16 + f);
+          if (f + 2 < 2 * KK) kf[f + 2] = k_frag(kst, f + 2);
+        } else {
+          sn1[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q1[f % KK], f % KK ? sn1[f / KK] : nm1, 0, 0, 0);
+          soft_slot(so1, acc1, pb1, uq1, 16 + f);
+        }
+        if (i % 8 == 5) issue_part(t2, st2, i / 8);
         __builtin_amdgcn_sched_barrier(0);
       }
-      keep_here(pb1, acc1);
-      settle(s1, ms1, l1, acc1, o1, pb1);
-      if (cur_nvalid < kTileKeys) mask_tail(s0, cur_nvalid);
-      // ---- R2: PV of half 1 of the previous tile, pairs 0-7 of half 0, V^T fragments
-      // 0-7 of this tile (each read into the registers its PV MFMA has just used)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
-        if (i % 2 == 0) exp_pair(s0, ms0, acc0, pb0, i / 2);
-        if (i < 8) read_vf(vst, i);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-      // ---- R3: QK of half 1, pairs 8-15 of half 0, V^T fragments 8-15
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s1[i / 8] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[i / 8][i % 8], q1[i % 8], i % 8 ? s1[i / 8] : f32x16{},
-                                                            0, 0, 0);
-        if (i % 2 == 0) exp_pair(s0, ms0, acc0, pb0, 8 + i / 2);
-        if (i % 2 == 1) read_vf(vst, 8 + i / 2);
-        __builtin_amdgcn_sched_barrier(0);
+      for (int g = 32; g < 34; ++g) {
+        soft_slot(so0, acc0, pb0, uq0, g);
+        soft_slot(so1, acc1, pb1, uq1, g);
       }
       keep_here(pb0, acc0);
-      settle(s0, ms0, l0, acc0, o0, pb0);
-      if (cur_nvalid < kTileKeys) mask_tail(s1, cur_nvalid);
+      keep_here(pb1, acc1);
+      vf[0] = v_frag(vst, 0);
+      vf[1] = v_frag(vst, 1);
+      settle(ms0, l0, acc0, o0, pb0, nm0, q0, vst, prev_nvalid, sn0);
+      settle(ms1, l1, acc1, o1, pb1, nm1, q1, vst, prev_nvalid, sn1);
+      acc0 = 0.f;
+      acc1 = 0.f;
+      if (cur_nvalid < kTileKeys) {
+        mask_tail(sn0, cur_nvalid);
+        mask_tail(sn1, cur_nvalid);
+      }
+      // ---- PV run (each MFMA reads its P fragment before this slot's stream op can
+      // overwrite it with the next tile's)
+#pragma unroll
+      for (int i = 0; i < 32; ++i) {
+        const int f = i / 2;
+        if (i % 2 == 0) {
+          pv_mfma(o0[f % DT], vf[f], pb0[f / DT], i == 0);
+          soft_slot(sn0, acc0, pb0, uq0, f);
+          if (f + 2 < 4 * DT) vf[f + 2] = v_frag(vst, f + 2);
+        } else {
+          pv_mfma(o1[f % DT], vf[f], pb1[f / DT], false);
+          soft_slot(sn1, acc1, pb1, uq1, f);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
     } else {
       issue(t2, st2);
     }
     // ---- tile t+1 has landed (the DMA of tile t+2 may still be in flight) and every
-    // wave is past its reads of tile t
+    // wave is past its reads of the stages refilled next
     __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * DMA_PER_WAVE));
     lds_barrier();
-    if (wave_live) {
-      // ---- R4: PV of half 0, pairs 0-7 of half 1, K fragments of the next tile
-      acc1 = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        o0[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb0[i / DT], o0[i % DT], 0, 0, 0);
-        if (i % 2 == 0) exp_pair(s1, ms1, acc1, pb1, i / 2);
-        read_kf(kst1, i);
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
     cur = t1;
     t1 = t2;
-  }
-  // ---- drain: the last tile's half 1 (or the dummy when there was no tile)
-  if (wave_live) {
-#pragma unroll
-    for (int i = 8; i < 16; ++i) exp_pair(s1, ms1, acc1, pb1, i);
-    settle(s1, ms1, l1, acc1, o1, pb1);
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      o1[i % DT] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf[i / DT][i % DT], pb1[i / DT], o1[i % DT], 0, 0, 0);
+    prev_nvalid = cur_nvalid;
+    return cur_nvalid != 0;
+  };
+  for (;;) {
+    if (!iteration(sa0, sa1, sb0, sb1, std::integral_constant<int, 0>{})) break;
+    if (!iteration(sb0, sb1, sa0, sa1, std::integral_constant<int, 1>{})) break;
+    if (!iteration(sa0, sa1, sb0, sb1, std::integral_constant<int, 2>{})) break;
+    if (!iteration(sb0, sb1, sa0, sa1, std::integral_constant<int, 3>{})) break;
   }
   __builtin_amdgcn_s_waitcnt(vmcnt_only(0));  // no DMA may land in the stages reused below
   __syncthreads();
 
   // ---- epilogue: normalise, stage O through LDS (one 16 KB stage per wave, chunks
   // permuted like K), store rows with 16-byte writes
-  uint8_t* const stage_o = wave < 3 ? k_ring + wave * kR64TileBytes : v_ring;  // 64 rows x 256 B per wave
+  uint8_t* const stage_o = k_ring + wave * kR64TileBytes;  // 64 rows x 256 B per wave
   auto finish = [&](f32x16 (&o)[DT], float ms, float l, int g) {
     const float l_tot = pair_sum(l);
     const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
@@ -798,6 +912,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       a.lse[static_cast<int64_t>(h) * a.lq + qr] = l_tot > 0.f ? (ms + __log2f(l_tot)) * kLn2 : -INFINITY;
   };
   if (wave_live) {
+    acc_settled(o0);
+    acc_settled(o1);
     finish(o0, ms0, l0, 0);
     finish(o1, ms1, l1, 1);
   }

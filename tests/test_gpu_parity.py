@@ -57,7 +57,9 @@ def attn_check(got_out, got_lse, ref_out, ref_lse, hs, qs, dtype, what):
         check_lse(lse, ref_lse, what + " lse", 1e-5)
     else:
         check_bf16(o, ref_out, what)
-        check_lse(lse, ref_lse, what + " lse", 5e-3)
+        # LSE has no bar of its own: it takes the output's max-abs bar, the size of
+        # the error bf16 scores (Q scaled by scale * log2 e in bf16) leave in it
+        check_lse(lse, ref_lse, what + " lse", 2e-2)
 
 
 # ----------------------------------------------------------------- tiny fp32
