@@ -616,15 +616,26 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     v_src[i] = r * 256 + ((p ^ (4 * (r & 3))) << 4);
   }
   const int wave_s = __builtin_amdgcn_readfirstlane(wave);  // scalar copy: LDS destinations go to M0
+  // Scalar bases: this head's slab of page 0, the page stride, and the wave's first
+  // LDS destination.  Everything about a tile's DMA is then a few scalar ops.
+  const int64_t h_elems = static_cast<int64_t>(__builtin_amdgcn_readfirstlane(h)) * a.B * D;
+  const uint16_t* const kp_h = kp + h_elems;
+  const uint16_t* const vp_h = vp + h_elems;
+  const int64_t page_elems = static_cast<int64_t>(a.H) * a.B * D;
+  const uint32_t m0_k = lds_offset(k_ring) + wave_s * 1024, m0_v = lds_offset(v_ring) + wave_s * 1024;
   // the DMA of tile m into stage st, instruction i of K and of V (empty tiles load
-  // nothing and write zeros); m is workgroup-uniform
+  // nothing and write zeros); m is workgroup-uniform.  The LDS bases pass through an
+  // empty asm so that each destination is formed where it is used: hoisted out of
+  // the loop, the 32 stage/instruction combinations would each hold a scalar register.
   auto issue_part = [&](int2 m, int st, int i) {
     const int sub = m.y >> 8, nv = m.y & 255;
-    const int64_t slab = (static_cast<int64_t>(m.x) * a.H + h) * a.B * D + static_cast<int64_t>(sub) * kTileKeys * D;
-    const u32x4 kr = buffer_rsrc(kp + slab, nv * D * 2), vr = buffer_rsrc(vp + slab, nv * D * 2);
-    const uint32_t off = st * kR64TileBytes + (wave_s + kR64Waves * i) * 1024;
-    dma_16x64(kr, k_src[i], lds_offset(k_ring) + off);
-    dma_16x64(vr, v_src[i], lds_offset(v_ring) + off);
+    const int64_t slab = static_cast<int64_t>(m.x) * page_elems + static_cast<int64_t>(sub) * kTileKeys * D;
+    const u32x4 kr = buffer_rsrc(kp_h + slab, nv * D * 2), vr = buffer_rsrc(vp_h + slab, nv * D * 2);
+    uint32_t mk = m0_k, mv = m0_v;
+    asm volatile("" : "+s"(mk), "+s"(mv));
+    const uint32_t off = st * kR64TileBytes + kR64Waves * i * 1024;
+    dma_16x64(kr, k_src[i], mk + off);
+    dma_16x64(vr, v_src[i], mv + off);
   };
   auto issue = [&](int2 m, int st) {
 #pragma unroll
