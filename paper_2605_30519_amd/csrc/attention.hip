@@ -486,14 +486,13 @@ __device__ __forceinline__ uint32_t lds_offset(const void* p) {
 // MFMA accumulator sits in the VGPRs that the softmax VALU work also uses, and an
 // MFMA writing its result there slows that work down; the asm keeps O in AccVGPRs.
 // The asm also hides the MFMA from the compiler's hazard checks, so the wait states
-// come from the callers: `lead` puts two before an MFMA whose P operand or
-// accumulator VALU code may just have written, and VALU code touches the
-// accumulators only after acc_settled().
-__device__ __forceinline__ void pv_mfma(f32x16& acc, const bf16x8& v, const bf16x8& p, bool lead) {
-  if (lead)
-    asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(p));
-  else
-    asm volatile("v_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(p));
+// are explicit: two before the MFMA (any operand may have been written by VALU code
+// just before it: a rematerialised constant, a copy out of a spill), the callers
+// keep the A and B operands unchanged until the MFMA has read them (it reads them
+// over its passes), and VALU code touches the accumulators only after
+// acc_settled().
+__device__ __forceinline__ void pv_mfma(f32x16& acc, const bf16x8& v, const bf16x8& p) {
+  asm volatile("s_nop 1\n\tv_mfma_f32_32x32x16_bf16 %0, %1, %2, %0" : "+a"(acc) : "v"(v), "v"(p));
 }
 // Sixteen wait states (more than an 8-pass MFMA result needs) before VALU code reads
 // or writes the accumulators; they pass through the asm so that no access moves
@@ -556,20 +555,19 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     for (int e = 0; e < 8; ++e) v[e] = static_cast<__bf16>(static_cast<float>(v[e]) * c);
     return v;
   };
-  bf16x8 q0[KK], q1[KK];
+  // the raw Q rows are loaded here and scaled once the first tiles' DMA is issued,
+  // so that their latency overlaps the block-list decode
+  uint4 qx0[KK], qx1[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
     const int r0 = wrow + lane % 32, r1 = r0 + 32;
-    uint4 x0 = make_uint4(0, 0, 0, 0), x1 = x0;
+    qx0[kk] = qx1[kk] = make_uint4(0, 0, 0, 0);
     if (r0 < row_end)
-      x0 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r0) * a.H + h) * D + 16 * kk + 8 * half);
+      qx0[kk] = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r0) * a.H + h) * D + 16 * kk + 8 * half);
     if (r1 < row_end)
-      x1 = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r1) * a.H + h) * D + 16 * kk + 8 * half);
-    q0[kk] = prescale(x0);
-    q1[kk] = prescale(x1);
-    // Q lives in AccVGPRs next to O; the VGPRs hold S, P and the operand fragments
-    asm volatile("" : "+a"(q0[kk]), "+a"(q1[kk]));
+      qx1[kk] = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(r1) * a.H + h) * D + 16 * kk + 8 * half);
   }
+  bf16x8 q0[KK], q1[KK];
 
   f32x16 o0[DT], o1[DT];
 #pragma unroll
@@ -658,13 +656,13 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   // A half's softmax as a stream over its 32 S elements per lane (element E is
   // s[E / 16][E % 16], already c s - max; it lands in P^T fragment E / 8 at position
   // E % 8).  Slot g takes the exponential of element g, adds element g - 1 to the row
-  // sum and, on odd slots, packs elements g - 3 and g - 2 into P (not earlier: the
-  // PV run that carries slots 0-15 still reads the previous tile's P fragment 0 up
-  // to the MFMA of slot 3).  No op of a slot reads a result of the same slot, so a
-  // slot placed next to one MFMA issues without waiting on VALU latency; slots 32 and
-  // 33 finish the stream.  Each result goes through an empty asm so that the IR
-  // passes keep it in its slot (they would otherwise sink every op next to its first
-  // use).  The row sum is taken over the fp32 values.
+  // sum and, on odd slots, packs elements g - 3 and g - 2 into P (late enough for the
+  // PV run that carries the early slots to have read the previous tile's P fragment
+  // 0).  No op of a slot reads a result of the same slot, so a slot placed next to
+  // one MFMA issues without waiting on VALU latency; slots 32 and 33 finish the
+  // stream.  Each result goes through an empty asm so that the IR passes keep it in
+  // its slot (they would otherwise sink every op next to its first use).  The row sum
+  // is taken over the fp32 values.
   auto soft_slot = [&](const f32x16 (&s)[2], float& acc, bf16x8 (&pb)[4], float (&uq)[32], int g) {
     if (g < 32) {
       uq[g] = __builtin_amdgcn_exp2f(s[g / 16][g % 16]);
@@ -776,9 +774,9 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   // MFMA carrying one softmax stream slot (one exponential, a half-rate VALU op, and
   // two or three other VALU ops fill the MFMA shadow only when spread this thin):
   //   QK run  S of tile t, both halves (each K fragment feeds the two halves' MFMAs
-  //           back to back); slots 16-33 of tile t-1's two streams; DMA of tile t+2
+  //           back to back); slots 15-33 of tile t-1's two streams; DMA of tile t+2
   //   PV run  O += P V of tile t-1, both halves (each V^T fragment feeds two MFMAs);
-  //           slots 0-15 of tile t's two streams
+  //           slots 0-14 of tile t's two streams
   // with both halves' softmax checks of tile t-1 between the runs.  Operand fragments
   // are read just in time, so the registers hold S of two tiles and P of one.  One
   // barrier per iteration, at its end: tile t+1 has landed and every wave is past its
@@ -803,8 +801,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     pb0[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
     pb1[j] = pb0[j];
   }
-  uq0[13] = uq0[14] = uq0[15] = 0.f;  // the dummy tile's streams enter the loop at slot 16
-  uq1[13] = uq1[14] = uq1[15] = 0.f;
+  uq0[12] = uq0[13] = uq0[14] = 0.f;  // the dummy tile's streams enter the loop at slot 15
+  uq1[12] = uq1[13] = uq1[14] = 0.f;
   int prev_nvalid = 0;
 
   int2 cur = scalar_tile(next_tile_raw());
@@ -812,10 +810,19 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   issue(make_int2(0, 0), kStages - 1);  // V of tile -1
   issue(cur, 0);
   issue(t1, 1);
-  // Everything issued so far lands (the Q loads included): the compiler then knows
-  // no vector-memory load of its own is pending in the loop, where any wait it
-  // inserted would also drain the DMA in flight, which it does not see.
-  __builtin_amdgcn_s_waitcnt(vmcnt_only(0));
+#pragma unroll
+  for (int kk = 0; kk < KK; ++kk) {
+    q0[kk] = prescale(qx0[kk]);
+    q1[kk] = prescale(qx1[kk]);
+    // Q lives in AccVGPRs next to O; the VGPRs hold S, P and the operand fragments
+    asm volatile("" : "+a"(q0[kk]), "+a"(q1[kk]));
+  }
+  // The Q loads and the block-list reads have landed (the compiler waited for them
+  // before the decode and the scaling, so it knows of no load of its own pending in
+  // the loop, where any wait it inserted would also drain the DMA in flight, which it
+  // does not see); of the DMA, the dummy stage and tile 0 must land before the loop,
+  // tile 1 may still be in flight.
+  __builtin_amdgcn_s_waitcnt(vmcnt_only(2 * DMA_PER_WAVE));
   lds_barrier();
 
   // Iteration t (t mod 4 = T, a compile-time constant, as are the stages) with tile
@@ -839,17 +846,17 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         const int f = i / 2;
         if (i % 2 == 0) {
           sn0[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q0[f % KK], f % KK ? sn0[f / KK] : nm0, 0, 0, 0);
-          soft_slot(so0, acc0, pb0, uq0, 16 + f);
+          soft_slot(so0, acc0, pb0, uq0, 15 + f);
           if (f + 2 < 2 * KK) kf[f + 2] = k_frag(kst, f + 2);
         } else {
           sn1[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q1[f % KK], f % KK ? sn1[f / KK] : nm1, 0, 0, 0);
-          soft_slot(so1, acc1, pb1, uq1, 16 + f);
+          soft_slot(so1, acc1, pb1, uq1, 15 + f);
         }
         if (i % 8 == 5) issue_part(t2, st2, i / 8);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
-      for (int g = 32; g < 34; ++g) {
+      for (int g = 31; g < 34; ++g) {
         soft_slot(so0, acc0, pb0, uq0, g);
         soft_slot(so1, acc1, pb1, uq1, g);
       }
@@ -865,21 +872,33 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         mask_tail(sn0, cur_nvalid);
         mask_tail(sn1, cur_nvalid);
       }
-      // ---- PV run (each MFMA reads its P fragment before this slot's stream op can
-      // overwrite it with the next tile's)
+      // ---- PV run.  Stream slot (g, half) of tile t rides on MFMA 2 g + half + 2,
+      // past the last MFMA that reads the previous tile's P fragment it overwrites.
+      // An MFMA reads its A and B registers over its passes, so each MFMA's operands
+      // are held (an empty asm use) until the end of the next slot, when it has
+      // finished: the compiler, which does not see these MFMAs, would otherwise give
+      // the registers to the next value as soon as the MFMA is issued.
+      bf16x8 hold_a = vf[0], hold_b = pb0[0];
 #pragma unroll
       for (int i = 0; i < 32; ++i) {
         const int f = i / 2;
+        const bf16x8 op_a = vf[f], op_b = i % 2 ? pb1[f / DT] : pb0[f / DT];
         if (i % 2 == 0) {
-          pv_mfma(o0[f % DT], vf[f], pb0[f / DT], i == 0);
-          soft_slot(sn0, acc0, pb0, uq0, f);
+          pv_mfma(o0[f % DT], op_a, op_b);
           if (f + 2 < 4 * DT) vf[f + 2] = v_frag(vst, f + 2);
         } else {
-          pv_mfma(o1[f % DT], vf[f], pb1[f / DT], false);
-          soft_slot(sn1, acc1, pb1, uq1, f);
+          pv_mfma(o1[f % DT], op_a, op_b);
         }
+        if (i >= 2) {
+          if (i % 2 == 0) soft_slot(sn0, acc0, pb0, uq0, (i - 2) / 2);
+          else soft_slot(sn1, acc1, pb1, uq1, (i - 2) / 2);
+        }
+        if (i > 0) asm volatile("" ::"v"(hold_a), "v"(hold_b));
+        hold_a = op_a;
+        hold_b = op_b;
         __builtin_amdgcn_sched_barrier(0);
       }
+      asm volatile("s_nop 7\n\ts_nop 3" ::"v"(hold_a), "v"(hold_b));  // the last MFMA's operands
     } else {
       issue(t2, st2);
     }
