@@ -174,9 +174,9 @@ def main():
     attn_tflops = float(flops_steps.mean() / (att_ms.mean() * 1e-3) / 1e12)
     sbytes = select_bytes(w, n, awe)
     sel_gbs = float(sbytes / (sel_ms.mean() * 1e-3) / 1e9)
-    attn_roof = {"kernel": "k_attn_bf16", "bound": "mfma", "achieved": round(attn_tflops, 2),
+    attn_roof = {"kernel": "k_attn_bf16_r64", "bound": "mfma", "achieved": round(attn_tflops, 2),
                  "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
-                 "traffic": load_traffic("k_attn_bf16"),
+                 "traffic": load_traffic("k_attn_bf16_r64"),
                  "per_launch": {"flops": flops_steps.mean(), "avg_ms": round(float(att_ms.mean()), 4)}}
     sel_roof = {"kernel": "select (k_qmean_partial+k_qmean_final+k_pool_score+k_topk)", "bound": "hbm",
                 "achieved": round(sel_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
