@@ -543,20 +543,12 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
   const uint16_t* vp = static_cast<const uint16_t*>(a.v_pages);
 
-  // Q^T B operands of the two halves: lane holds query wrow + 32 g + lane % 32.
-  // Q is scaled by c = scale * log2(e) (rounded back to bf16), so that the MFMAs
-  // produce scores in the scaled log2 units of the softmax directly.
-  const float c = a.scale * kLog2e;
+  // Q^T B operands of the two halves: lane holds query wrow + 32 g + lane % 32
+  const float c = a.scale * kLog2e;  // scores to the softmax's log2 units, applied in fp32
   const int wrow = row0 + wave * 64;
   const bool wave_live = wrow < row_end;  // wave-uniform
-  auto prescale = [&](uint4 x) {
-    bf16x8 v = __builtin_bit_cast(bf16x8, x);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[e] = static_cast<__bf16>(static_cast<float>(v[e]) * c);
-    return v;
-  };
-  // the raw Q rows are loaded here and scaled once the first tiles' DMA is issued,
-  // so that their latency overlaps the block-list decode
+  // the Q rows are loaded here and moved to AccVGPRs once the first tiles' DMA is
+  // issued, so that their latency overlaps the block-list decode
   uint4 qx0[KK], qx1[KK];
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
@@ -579,11 +571,6 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     }
   // running max in scaled log2 units (max * scale * log2 e) and this lane's share of l
   float ms0 = kNoMax, ms1 = kNoMax, l0 = 0.f, l1 = 0.f;
-  // -max as the MFMA accumulator's initial value: S comes out as c s - max, the
-  // exponent itself
-  f32x16 nm0, nm1;
-#pragma unroll
-  for (int i = 0; i < 16; ++i) nm0[i] = nm1[i] = -kNoMax;
 
   // ---- tile sequence: (page, sub-tile << 8 | valid keys), from the decoded table
   int next_entry = 0, ntab = 0, ti = 0;
@@ -654,22 +641,28 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       }
   };
   // A half's softmax as a stream over its 32 S elements per lane (element E is
-  // s[E / 16][E % 16], already c s - max; it lands in P^T fragment E / 8 at position
-  // E % 8).  Slot g takes the exponential of element g, adds element g - 1 to the row
-  // sum and, on odd slots, packs elements g - 3 and g - 2 into P (late enough for the
-  // PV run that carries the early slots to have read the previous tile's P fragment
-  // 0).  No op of a slot reads a result of the same slot, so a slot placed next to
-  // one MFMA issues without waiting on VALU latency; slots 32 and 33 finish the
-  // stream.  Each result goes through an empty asm so that the IR passes keep it in
-  // its slot (they would otherwise sink every op next to its first use).  The row sum
-  // is taken over the fp32 values.
-  auto soft_slot = [&](const f32x16 (&s)[2], float& acc, bf16x8 (&pb)[4], float (&uq)[32], int g) {
+  // s[E / 16][E % 16]; it lands in P^T fragment E / 8 at position E % 8).  Slot g
+  // forms the exponent c s - max of element g (one fma: the scale is applied in
+  // fp32), takes the exponential of element g - 1, adds element g - 2 to the row sum
+  // and, on odd slots, packs elements g - 3 and g - 2 into P (late enough for the PV
+  // run that carries the early slots to have read the previous tile's P fragment 0).
+  // No op of a slot reads a result of the same slot, so a slot placed next to one
+  // MFMA issues without waiting on VALU latency; slots 32 and 33 finish the stream.
+  // Each result goes through an empty asm so that the IR passes keep it in its slot
+  // (they would otherwise sink every op next to its first use).  The row sum is taken
+  // over the fp32 values.
+  auto soft_slot = [&](const f32x16 (&s)[2], float ms, float& acc, bf16x8 (&pb)[4], float (&tq)[32],
+                       float (&uq)[32], int g) {
     if (g < 32) {
-      uq[g] = __builtin_amdgcn_exp2f(s[g / 16][g % 16]);
-      asm volatile("" : "+v"(uq[g]));
+      tq[g] = fmaf(s[g / 16][g % 16], c, -ms);
+      asm volatile("" : "+v"(tq[g]));
     }
     if (g >= 1 && g <= 32) {
-      acc += uq[g - 1];
+      uq[g - 1] = __builtin_amdgcn_exp2f(tq[g - 1]);
+      asm volatile("" : "+v"(uq[g - 1]));
+    }
+    if (g >= 2 && g <= 33) {
+      acc += uq[g - 2];
       asm volatile("" : "+v"(acc));
     }
     if (g % 2 == 1 && g >= 3 && g <= 33) {
@@ -713,12 +706,10 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   // tile's own max is known.  They stand (every p <= 2^8) unless some lane's sum of
   // them exceeds 2^8 or overflowed; only then is the tile's S formed again from the K
   // still in LDS (stage kst, nvalid keys), its max taken, O and l moved to the new max
-  // and the exponentials redone.  The next tile's S (sn), already formed against the
-  // old max, is moved to the new one too; while the old max is still the initial
-  // placeholder its values are meaningless, and they are left to overflow, which
-  // settles that tile the same way.
-  auto settle = [&](float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4], f32x16& nm,
-                    const bf16x8 (&q)[KK], int kst, int nvalid, f32x16 (&sn)[2]) {
+  // and the exponentials redone.  The next tile's exponentials are formed after this
+  // point, against the new max.
+  auto settle = [&](float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4], const bf16x8 (&q)[KK], int kst,
+                    int nvalid) {
     if (__any(acc > kSlackSum)) {
       f32x16 s[2];
 #pragma unroll
@@ -734,7 +725,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         m0 = fmaxf(m0, fmaxf(s[0][i], s[1][i]));
         m1 = fmaxf(m1, fmaxf(s[0][i + 1], s[1][i + 1]));
       }
-      const float m_new = fmaxf(ms, pair_max(fmaxf(m0, m1)));
+      const float m_new = fmaxf(ms, pair_max(fmaxf(m0, m1)) * c);
       const float alpha = __builtin_amdgcn_exp2f(ms - m_new);
       l *= alpha;
       acc_settled(o);
@@ -748,20 +739,12 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         o[dt] = t;
         asm volatile("" : "+a"(o[dt]));
       }
-      const float shift = ms == kNoMax ? 0.f : m_new - ms;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        sn[0][i] -= shift;
-        sn[1][i] -= shift;
-      }
       ms = m_new;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) nm[i] = -m_new;
       acc = 0.f;
 #pragma unroll
       for (int e = 0; e < 32; e += 2) {
-        const float p0 = __builtin_amdgcn_exp2f(s[e / 16][e % 16] - m_new);
-        const float p1 = __builtin_amdgcn_exp2f(s[e / 16][e % 16 + 1] - m_new);
+        const float p0 = __builtin_amdgcn_exp2f(fmaf(s[e / 16][e % 16], c, -m_new));
+        const float p1 = __builtin_amdgcn_exp2f(fmaf(s[e / 16][e % 16 + 1], c, -m_new));
         acc += p0 + p1;
         pb[e / 8][e % 8] = static_cast<__bf16>(p0);
         pb[e / 8][e % 8 + 1] = static_cast<__bf16>(p1);
@@ -788,7 +771,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   bf16x8 pb0[4], pb1[4];
   float acc0 = 0.f, acc1 = 0.f;
   // the two halves' softmax streams (only a few elements of each are live at a time)
-  float uq0[32], uq1[32];
+  float tq0[32], uq0[32], tq1[32], uq1[32];
 #pragma unroll
   for (int t2i = 0; t2i < 2; ++t2i)
 #pragma unroll
@@ -801,8 +784,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     pb0[j] = __builtin_bit_cast(bf16x8, make_uint4(0, 0, 0, 0));
     pb1[j] = pb0[j];
   }
-  uq0[12] = uq0[13] = uq0[14] = 0.f;  // the dummy tile's streams enter the loop at slot 15
-  uq1[12] = uq1[13] = uq1[14] = 0.f;
+  tq0[14] = tq1[14] = -INFINITY;  // the dummy tile's streams enter the loop at slot 15
+  uq0[12] = uq0[13] = uq1[12] = uq1[13] = 0.f;
   int prev_nvalid = 0;
 
   int2 cur = scalar_tile(next_tile_raw());
@@ -812,8 +795,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   issue(t1, 1);
 #pragma unroll
   for (int kk = 0; kk < KK; ++kk) {
-    q0[kk] = prescale(qx0[kk]);
-    q1[kk] = prescale(qx1[kk]);
+    q0[kk] = __builtin_bit_cast(bf16x8, qx0[kk]);
+    q1[kk] = __builtin_bit_cast(bf16x8, qx1[kk]);
     // Q lives in AccVGPRs next to O; the VGPRs hold S, P and the operand fragments
     asm volatile("" : "+a"(q0[kk]), "+a"(q1[kk]));
   }
@@ -845,27 +828,27 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       for (int i = 0; i < 32; ++i) {
         const int f = i / 2;
         if (i % 2 == 0) {
-          sn0[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q0[f % KK], f % KK ? sn0[f / KK] : nm0, 0, 0, 0);
-          soft_slot(so0, acc0, pb0, uq0, 15 + f);
+          sn0[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q0[f % KK], f % KK ? sn0[f / KK] : f32x16{}, 0, 0, 0);
+          soft_slot(so0, ms0, acc0, pb0, tq0, uq0, 15 + f);
           if (f + 2 < 2 * KK) kf[f + 2] = k_frag(kst, f + 2);
         } else {
-          sn1[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q1[f % KK], f % KK ? sn1[f / KK] : nm1, 0, 0, 0);
-          soft_slot(so1, acc1, pb1, uq1, 15 + f);
+          sn1[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q1[f % KK], f % KK ? sn1[f / KK] : f32x16{}, 0, 0, 0);
+          soft_slot(so1, ms1, acc1, pb1, tq1, uq1, 15 + f);
         }
         if (i % 8 == 5) issue_part(t2, st2, i / 8);
         __builtin_amdgcn_sched_barrier(0);
       }
 #pragma unroll
       for (int g = 31; g < 34; ++g) {
-        soft_slot(so0, acc0, pb0, uq0, g);
-        soft_slot(so1, acc1, pb1, uq1, g);
+        soft_slot(so0, ms0, acc0, pb0, tq0, uq0, g);
+        soft_slot(so1, ms1, acc1, pb1, tq1, uq1, g);
       }
       keep_here(pb0, acc0);
       keep_here(pb1, acc1);
       vf[0] = v_frag(vst, 0);
       vf[1] = v_frag(vst, 1);
-      settle(ms0, l0, acc0, o0, pb0, nm0, q0, vst, prev_nvalid, sn0);
-      settle(ms1, l1, acc1, o1, pb1, nm1, q1, vst, prev_nvalid, sn1);
+      settle(ms0, l0, acc0, o0, pb0, q0, vst, prev_nvalid);
+      settle(ms1, l1, acc1, o1, pb1, q1, vst, prev_nvalid);
       acc0 = 0.f;
       acc1 = 0.f;
       if (cur_nvalid < kTileKeys) {
@@ -890,8 +873,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
           pv_mfma(o1[f % DT], op_a, op_b);
         }
         if (i >= 2) {
-          if (i % 2 == 0) soft_slot(sn0, acc0, pb0, uq0, (i - 2) / 2);
-          else soft_slot(sn1, acc1, pb1, uq1, (i - 2) / 2);
+          if (i % 2 == 0) soft_slot(sn0, ms0, acc0, pb0, tq0, uq0, (i - 2) / 2);
+          else soft_slot(sn1, ms1, acc1, pb1, tq1, uq1, (i - 2) / 2);
         }
         if (i > 0) asm volatile("" ::"v"(hold_a), "v"(hold_b));
         hold_a = op_a;

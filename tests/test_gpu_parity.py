@@ -57,9 +57,7 @@ def attn_check(got_out, got_lse, ref_out, ref_lse, hs, qs, dtype, what):
         check_lse(lse, ref_lse, what + " lse", 1e-5)
     else:
         check_bf16(o, ref_out, what)
-        # LSE has no bar of its own: it takes the output's max-abs bar, the size of
-        # the error bf16 scores (Q scaled by scale * log2 e in bf16) leave in it
-        check_lse(lse, ref_lse, what + " lse", 2e-2)
+        check_lse(lse, ref_lse, what + " lse", 5e-3)
 
 
 # ----------------------------------------------------------------- tiny fp32
@@ -192,6 +190,44 @@ def test_edge_cases(dev):
     o2, l2 = omnimem_sparse_attn(cache, x.q, a1.idx, a1.cnt, w.group_size, w.scale)
     torch.cuda.synchronize()
     assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+
+
+# ------------------------------------------------------- running-max jumps
+
+def test_running_max_jumps(dev):
+    """Blocks whose scores jump far above and below the running max, in both list
+    orders: the bf16 kernel's speculative exponentials must settle every jump
+    (finite overshoot: rescale; overflow: recompute from the keys still in LDS)."""
+    H, d, S, Lq, B, n = 2, 128, 256, 300, 64, 4
+    g = torch.Generator().manual_seed(11)
+    u = torch.randn(H, d, generator=g)
+    u = u / u.norm(dim=-1, keepdim=True)
+    q = (3.0 * u[None] + 0.3 * torch.randn(Lq, H, d, generator=g)).to(torch.bfloat16)
+    nb = n * (S // B)
+    # per-block key scale: scaled scores about 0.8 m, so m = 40 overshoots the running
+    # max by ~46 in log2 units and m = 400 by ~460 (an overflow without settling)
+    m = torch.tensor([1.0, 40.0, 1.0, 0.5, 400.0, 2.0, 0.25, 60.0, 1.0, 3.0, 400.0, 1.0, 0.1, 8.0, 1.0, 50.0])[:nb]
+    k = (u[None, None] * 3.0 + 0.3 * torch.randn(n, S, H, d, generator=g))
+    k = k * m.repeat_interleave(B).view(n, S, 1, 1)
+    k = k.to(torch.bfloat16)
+    v = torch.randn(n, S, H, d, generator=g).to(torch.bfloat16)
+    scale = d ** -0.5
+    cache = synth.page_layer(k.to(dev), v.to(dev), B, seed=5, pad_value=NAN)
+    qd = q.to(dev)
+    say("jumps: dense over all blocks (ascending order)")
+    dout, dlse = omnimem_dense_attn(cache, qd, 0, n, scale)
+    d_ref, dl_ref, hs, qs = oracle.dense_attn(q, k, v, B, 0, n, scale)
+    attn_check(dout, dlse, d_ref, dl_ref, hs, qs, torch.bfloat16, "jumps dense")
+    for name, order in (("descending scale", torch.argsort(m, descending=True)),
+                        ("ascending scale", torch.argsort(m)),
+                        ("shuffled", torch.randperm(nb, generator=g))):
+        say(f"jumps: sparse, blocks in {name} order")
+        ids = order.to(torch.int32)
+        idx = ids.view(1, 1, nb).expand(H, 1, nb).contiguous().to(dev)
+        cnt = torch.full((H, 1), nb, dtype=torch.int32, device=dev)
+        out, lse = omnimem_sparse_attn(cache, qd, idx, cnt, Lq, scale)
+        o_ref, l_ref, hs, qs = oracle.sparse_attn(q, k, v, B, idx.cpu().numpy(), cnt.cpu().numpy(), Lq, scale)
+        attn_check(out, lse, o_ref, l_ref, hs, qs, torch.bfloat16, f"jumps sparse {name}")
 
 
 # ------------------------------------------------------------- long block lists
