@@ -37,8 +37,9 @@ __global__ __launch_bounds__(kQThreads) void k_qmean_partial(const T* __restrict
   constexpr int VEC = V::N;
   constexpr int CPR = D / VEC;             // 16-byte chunks per row
   constexpr int PHASES = kQThreads / CPR;  // rows summed side by side
-  constexpr int UNROLL = 4;
-  __shared__ float red[PHASES][D];
+  constexpr int UNROLL = (kQRowsPerSplit + PHASES - 1) / PHASES;  // one round of loads covers the split
+  constexpr int kWaves = kQThreads / kWave, PH_PER_WAVE = kWave / CPR;
+  __shared__ float red[kWaves][D];
 
   const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z;
   const int g0 = r * G, g1 = min(g0 + G, lq);
@@ -64,30 +65,51 @@ __global__ __launch_bounds__(kQThreads) void k_qmean_partial(const T* __restrict
       for (int j = 0; j < VEC; ++j) acc[j] += x[j];
     }
   }
+  // the row phases of a wave (lanes c, c + CPR, ...) by shuffles, then the waves through LDS
 #pragma unroll
-  for (int j = 0; j < VEC; ++j) red[ph][c * VEC + j] = acc[j];
+  for (int m = CPR; m < kWave; m <<= 1)
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) acc[j] += __shfl_xor(acc[j], m);
+  const int wave = threadIdx.x / kWave;
+  if (threadIdx.x % kWave < CPR) {
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) red[wave][c * VEC + j] = acc[j];
+  }
   __syncthreads();
+  static_assert(PH_PER_WAVE >= 1, "a wave spans whole rows");
   for (int col = threadIdx.x; col < D; col += kQThreads) {
     float sum = 0.f;
-    for (int p = 0; p < PHASES; ++p) sum += red[p][col];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) sum += red[w][col];
     partial[((static_cast<int64_t>(h) * R + r) * nsplit + s) * D + col] = sum;
   }
 }
 
 // Proxy query columns [col, col + N) of group r: the partial sums added in split
 // order (the same order everywhere, so every reader gets identical values), divided
-// by the group's row count.
+// by the group's row count.  The partials are fetched kBatch at a time, every load
+// of a batch in flight before its adds.
 template <int N>
 __device__ __forceinline__ void proxy_cols(const float* __restrict__ partial, int h, int r, int R, int nsplit, int D,
                                            int col, int lq, int G, float (&out)[N]) {
+  constexpr int kBatch = 16;
   const int g0 = r * G, rows = min(g0 + G, lq) - g0;
   const int used = (rows + kQRowsPerSplit - 1) / kQRowsPerSplit;
   const float* p = partial + (static_cast<int64_t>(h) * R + r) * nsplit * D + col;
 #pragma unroll
   for (int j = 0; j < N; ++j) out[j] = 0.f;
-  for (int s = 0; s < used; ++s)
+  for (int s0 = 0; s0 < used; s0 += kBatch) {
+    float v[kBatch][N];
 #pragma unroll
-    for (int j = 0; j < N; ++j) out[j] += p[static_cast<int64_t>(s) * D + j];
+    for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+      for (int j = 0; j < N; ++j) v[u][j] = s0 + u < used ? p[static_cast<int64_t>(s0 + u) * D + j] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+#pragma unroll
+      for (int j = 0; j < N; ++j)
+        if (s0 + u < used) out[j] += v[u][j];
+  }
   const float inv_rows = 1.0f / static_cast<float>(rows);
 #pragma unroll
   for (int j = 0; j < N; ++j) out[j] = out[j] * inv_rows;
@@ -120,18 +142,24 @@ struct SlabShape {
   static constexpr int PASSES = B / ROWS_PER_PASS;
 };
 
+// Issues every 16-byte load of a slab (rows past nvalid read as zero).
 template <typename T, int D, int B>
-__device__ __forceinline__ void pool_slab(const T* __restrict__ slab, int nvalid, int lane,
-                                          float (&colsum)[Vec16<T>::N]) {
+__device__ __forceinline__ void load_slab(const T* __restrict__ slab, int nvalid, int lane,
+                                          uint4 (&raw)[SlabShape<T, D, B>::PASSES]) {
   using Sh = SlabShape<T, D, B>;
   const int c = lane % Sh::CPR, ph = lane / Sh::CPR;
-  // issue every 16-byte load of the slab first (raw words, no widening yet)
-  uint4 raw[Sh::PASSES];
 #pragma unroll
   for (int i = 0; i < Sh::PASSES; ++i) {
     const int row = ph + i * Sh::ROWS_PER_PASS;
     raw[i] = row < nvalid ? *reinterpret_cast<const uint4*>(slab + row * D + c * Sh::VEC) : make_uint4(0, 0, 0, 0);
   }
+}
+
+// Column sums of a loaded slab; every lane ends with the sums of its column chunk.
+template <typename T, int D, int B>
+__device__ __forceinline__ void sum_slab(const uint4 (&raw)[SlabShape<T, D, B>::PASSES],
+                                         float (&colsum)[Vec16<T>::N]) {
+  using Sh = SlabShape<T, D, B>;
 #pragma unroll
   for (int j = 0; j < Sh::VEC; ++j) colsum[j] = 0.f;
 #pragma unroll
@@ -163,10 +191,12 @@ struct PoolArgs {
   int blocks_per_wave;
 };
 
-template <typename T, int D, int B, bool INLINE>
+// NR > 0: scores of up to NR groups computed in place; NR == 0: kbar written for k_score.
+template <typename T, int D, int B, int NR>
 __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
   using Sh = SlabShape<T, D, B>;
   constexpr int VEC = Sh::VEC;
+  constexpr int kMaxBlocksPerWave = 8;
   const int h = blockIdx.y;
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
   const int c = lane % Sh::CPR;
@@ -174,10 +204,28 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
   const int last = min(first + a.blocks_per_wave, a.nb);
   const T* pages = static_cast<const T*>(a.k_pages);
 
-  float q[INLINE ? kInlineGroups : 1][VEC];
-  if (INLINE) {
+  int32_t page_ids[kMaxBlocksPerWave];  // the wave's page ids, loaded together before any slab
+#pragma unroll
+  for (int i = 0; i < kMaxBlocksPerWave; ++i) page_ids[i] = first + i < last ? a.page_table[first + i] : -1;
+  auto live = [&](int i) {
+    const int64_t page = page_ids[i];
+    return first + i < last && first + i < a.first_excluded && page >= 0 && page < a.num_pages;
+  };
+  auto valid_rows = [&](int b) {
+    const int o = b % a.Bpc;
+    return o == a.Bpc - 1 ? a.S - o * B : B;
+  };
+  auto slab_of = [&](int i) { return pages + (static_cast<int64_t>(page_ids[i]) * a.H + h) * static_cast<int64_t>(B) * D; };
+
+  // the first slab's loads go out before the proxy-query prologue, so that its
+  // latency overlaps theirs
+  uint4 raw[Sh::PASSES];
+  if (live(0)) load_slab<T, D, B>(slab_of(0), valid_rows(first), lane, raw);
+
+  float q[NR > 0 ? NR : 1][VEC];
+  if (NR > 0) {
     // the workgroup's proxy queries, summed from the partials once and shared in LDS
-    __shared__ float qs[kInlineGroups][D];
+    __shared__ float qs[NR > 0 ? NR : 1][D];
     for (int i = threadIdx.x; i < a.R * D; i += kThreads) {
       float v[1];
       proxy_cols<1>(a.qpart, h, i / D, a.R, a.nsplit, D, i % D, a.lq, a.G, v);
@@ -185,36 +233,29 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int r = 0; r < kInlineGroups; ++r)
+    for (int r = 0; r < NR; ++r)
 #pragma unroll
       for (int j = 0; j < VEC; ++j) q[r][j] = r < a.R ? qs[r][c * VEC + j] : 0.f;
   }
 
-  constexpr int kMaxBlocksPerWave = 8;
-  int32_t page_ids[kMaxBlocksPerWave];  // the wave's page ids, loaded together before any slab
-#pragma unroll
-  for (int i = 0; i < kMaxBlocksPerWave; ++i) page_ids[i] = first + i < last ? a.page_table[first + i] : -1;
 #pragma unroll
   for (int i = 0; i < kMaxBlocksPerWave; ++i) {
     const int b = first + i;
     if (b >= last) break;
-    const int64_t page = page_ids[i];
-    const bool live = b < a.first_excluded && page >= 0 && page < a.num_pages;
-    if (!live) {
-      if (INLINE) {
+    if (!live(i)) {
+      if (NR > 0) {
         if (lane < a.R) a.keys[(static_cast<int64_t>(h) * a.R + lane) * a.nbp + b] = 0u;
       }
       continue;
     }
-    const int o = b % a.Bpc;
-    const int nvalid = o == a.Bpc - 1 ? a.S - o * B : B;
-    const T* slab = pages + (page * a.H + h) * static_cast<int64_t>(B) * D;
+    const int nvalid = valid_rows(b);
+    if (i > 0) load_slab<T, D, B>(slab_of(i), nvalid, lane, raw);
     float colsum[VEC];
-    pool_slab<T, D, B>(slab, nvalid, lane, colsum);
+    sum_slab<T, D, B>(raw, colsum);
     const float inv = 1.0f / static_cast<float>(nvalid);
-    if (INLINE) {
+    if (NR > 0) {
 #pragma unroll
-      for (int r = 0; r < kInlineGroups; ++r) {
+      for (int r = 0; r < (NR > 0 ? NR : 1); ++r) {
         if (r >= a.R) break;
         float dot = 0.f;
 #pragma unroll
@@ -290,11 +331,12 @@ constexpr int kTopkRegMax = kTopkMaxThreads * 4 * kTopkVecPerLane;        // lar
 constexpr int kTopkBinBits = 11;
 constexpr int kTopkBins = 1 << kTopkBinBits;
 constexpr int kTopkList = 256;
+constexpr int kPoolBlocksPerWave = 2;  // at most the pooling kernel's page-id batch (kMaxBlocksPerWave)
 
+// Called by all NT threads of a workgroup; out_score may be null.
 template <int NT>
-__global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
-                                                       int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
-                                                       float* __restrict__ score_out) {
+__device__ __forceinline__ void topk_row(const uint32_t* __restrict__ kp, int nb, int K, int32_t* __restrict__ out_idx,
+                         float* __restrict__ out_score, int32_t* __restrict__ out_cnt) {
   constexpr int kWaves = NT / kWave, kBinsPerThread = kTopkBins / NT;
   __shared__ int hist[kTopkBins];
   __shared__ __align__(16) uint32_t list[kTopkList];
@@ -303,8 +345,6 @@ __global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, 
   __shared__ int s_bin, s_above, s_m;
   __shared__ uint32_t s_kth;
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
-  const int64_t row = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
-  const uint32_t* kp = keys + row * nbp;
   const int J = min(kTopkVecPerLane, (nb + 4 * NT - 1) / (4 * NT));
   const int base = wave * J * 4 * kWave;
 
@@ -483,8 +523,6 @@ __global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, 
   }
   const int total = all ? ncand : K;
   const int need = all ? 0 : K - gt_all;  // ties at the K-th key still to take
-  int32_t* out_idx = idx + row * K;
-  float* out_score = score_out ? score_out + row * K : nullptr;
   int pos = gt_before + min(eq_before, need);
   int eq_run = eq_before;
 #pragma unroll
@@ -529,7 +567,15 @@ __global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, 
     out_idx[i] = -1;
     if (out_score) out_score[i] = -INFINITY;
   }
-  if (tid == 0) cnt[row] = total < K ? total : K;
+  if (tid == 0) *out_cnt = total < K ? total : K;
+}
+
+template <int NT>
+__global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
+                                             int32_t* __restrict__ idx, int32_t* __restrict__ cnt,
+                                             float* __restrict__ score_out) {
+  const int64_t row = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  topk_row<NT>(keys + row * nbp, nb, K, idx + row * K, score_out ? score_out + row * K : nullptr, cnt + row);
 }
 
 // Top-K for rows longer than the register-resident kernel holds: one wavefront,
@@ -628,19 +674,18 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     a.keys = keys;
     a.nbp = nbp;
     a.kbar = kbar;
-    a.blocks_per_wave = 2;  // at most the pooling kernel's page-id batch (kMaxBlocksPerWave)
+    a.blocks_per_wave = kPoolBlocksPerWave;
     const int waves = (g.nb + a.blocks_per_wave - 1) / a.blocks_per_wave;
     const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
+    auto pool = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, stream, a); };
     if (g.B == 64) {
-      if (p.inline_scores)
-        hipLaunchKernelGGL((k_pool_score<T, D, 64, true>), grid, dim3(kThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL((k_pool_score<T, D, 64, false>), grid, dim3(kThreads), 0, stream, a);
+      if (!p.inline_scores) pool(k_pool_score<T, D, 64, 0>);
+      else if (p.R == 1) pool(k_pool_score<T, D, 64, 1>);
+      else pool(k_pool_score<T, D, 64, kInlineGroups>);
     } else {
-      if (p.inline_scores)
-        hipLaunchKernelGGL((k_pool_score<T, D, 128, true>), grid, dim3(kThreads), 0, stream, a);
-      else
-        hipLaunchKernelGGL((k_pool_score<T, D, 128, false>), grid, dim3(kThreads), 0, stream, a);
+      if (!p.inline_scores) pool(k_pool_score<T, D, 128, 0>);
+      else if (p.R == 1) pool(k_pool_score<T, D, 128, 1>);
+      else pool(k_pool_score<T, D, 128, kInlineGroups>);
     }
     if (!p.inline_scores) {
       const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
