@@ -51,6 +51,8 @@ def parse():
     p.add_argument("--no-sweep", action="store_true", help="skip the history-length sweep")
     p.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
     p.add_argument("--stress", action="store_true", help="add the 14B-shaped union-gather comparison")
+    p.add_argument("--no-ramp", action="store_true", help="skip the 30-layer, 1 -> 60 chunk ramp")
+    p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
     return p.parse_args()
 
 
@@ -265,6 +267,19 @@ def main():
         result["sweep"] = sweep
         del cl
 
+    # ---------------------------------------------------------------- 30-layer ramp
+    if not args.no_ramp:
+        log("30-layer ramp, history 1 -> 60 chunks (generating 30 x 60 chunks)")
+        if "layers" in locals():
+            del layers, sels, outs, lses
+        torch.cuda.empty_cache()
+        result["ramp"] = ramp_measure(dev)
+
+    # ---------------------------------------------------------------- achievable peaks
+    if not args.no_probe:
+        log("achievable-peak probes: HBM copy, bf16 GEMM")
+        result["achievable"] = probe_peaks(dev, result)
+
     # ---------------------------------------------------------------- 14B comparator
     if args.stress:
         log("14B-shaped union-gather comparison")
@@ -276,6 +291,111 @@ def main():
         result["cpu_baseline"] = cpu_baseline(x0, w, flops_per_layer[0] + sflops)
 
     print(json.dumps(result), flush=True)
+
+
+def ramp_measure(dev, layers_n=30, warm_passes=20):
+    """The full chunk step of a 30-layer model as its history grows from 1 to 60
+    chunks: for each history length n, select + sparse attention over all 30 layers
+    (independent seeds, every layer's K/V resident), timed as one pass."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select, omnimem_select_workspace_bytes, omnimem_sparse_attn, synth
+    from paper_2605_30519_amd import select_params
+    from paper_2605_30519_amd.omnimem import Selection, workspace_tensor
+    w = synth.WORKLOADS["wan1.3b_30layer"]
+    H, R, K, N = w.heads, w.groups, w.top_k, w.history_chunks
+    caches, rels = [], []
+    for layer in range(layers_n):
+        x = synth.make_layer(w, layer, device=dev)
+        caches.append(synth.page_layer(x.k, x.v, w.block_size, seed=300 + layer))
+        rels.append(x.rel)
+        del x
+    resident_gb = sum(c.k_pages.numel() * c.k_pages.element_size() * 2 for c in caches) / 1e9
+    params = select_params(K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    ws = workspace_tensor(omnimem_select_workspace_bytes(caches[0], w.query_tokens, params), dev)
+    sel = Selection(torch.empty((H, R, K), dtype=torch.int32, device=dev),
+                    torch.empty((H, R), dtype=torch.int32, device=dev), None, 0)
+    out = torch.empty((w.query_tokens, H, w.head_dim), dtype=w.dtype, device=dev)
+    lse = torch.empty((H, w.query_tokens), dtype=torch.float32, device=dev)
+
+    def chunk_step(n, qs, flops=None):
+        awe = 0
+        for layer in range(layers_n):
+            omnimem_select(caches[layer], qs[layer], K, w.group_size, w.window_chunks, w.awe_min_outside_chunks,
+                           w.scale, num_chunks=n, workspace=ws, out=sel, want_score=False)
+            omnimem_sparse_attn(caches[layer], qs[layer], sel.idx, sel.cnt, w.group_size, w.scale, num_chunks=n,
+                                out=out, lse=lse)
+            if flops is not None:
+                flops.append(attn_flops(sel.idx, sel.cnt, w, n) + score_flops(w, n))
+            awe = sel.awe_active
+        return awe
+
+    q60 = [synth.queries(w, layer, N, rels[layer], dev) for layer in range(layers_n)]
+    for _ in range(warm_passes):  # the clock's ramp, on the longest history
+        chunk_step(N, q60)
+    del q60
+    torch.cuda.synchronize()
+    steps = []
+    for n in range(1, N + 1):
+        qs = [synth.queries(w, layer, n, rels[layer], dev) for layer in range(layers_n)]
+        flops = []
+        chunk_step(n, qs, flops)  # untimed: selection results for the flop count
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        awe = chunk_step(n, qs)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        steps.append({"history_chunks": n, "awe_active": int(awe),
+                      "ms_per_chunk_layer": round(ms / layers_n, 4),
+                      "effective_tflops": round(float(np.sum(flops)) / (ms * 1e-3) / 1e12, 2)})
+        del qs
+    total = sum(x["ms_per_chunk_layer"] for x in steps) * layers_n
+    return {"workload": "30 layers of the Wan2.1-1.3B-shaped attention layer, history 1 -> 60 chunks, "
+                        "one chunk step (select + sparse attention over every layer) per history length",
+            "layers": layers_n, "resident_kv_gb": round(resident_gb, 1), "total_ms": round(total, 2),
+            "awe_first_on": next((x["history_chunks"] for x in steps if x["awe_active"]), None),
+            "steps": steps}
+
+
+def probe_peaks(dev, result):
+    """Achievable peaks on this GPU, measured next to the spec ones: a device copy
+    (HBM read + write) and a large bf16 GEMM (the vendor library's MFMA rate)."""
+    import torch
+    out = {}
+    a = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)  # 1 GiB
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    reps = 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        b.copy_(a)
+    e1.record()
+    torch.cuda.synchronize()
+    out["hbm_copy_gbs"] = round(2 * a.numel() * 2 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    del a, b
+    m = 8192
+    x = torch.randn((m, m), device=dev).to(torch.bfloat16)
+    y = torch.randn((m, m), device=dev).to(torch.bfloat16)
+    z = torch.empty((m, m), dtype=torch.bfloat16, device=dev)
+    for _ in range(20):
+        torch.matmul(x, y, out=z)
+    e0.record()
+    for _ in range(reps):
+        torch.matmul(x, y, out=z)
+    e1.record()
+    torch.cuda.synchronize()
+    out["bf16_gemm_tflops"] = round(2.0 * m ** 3 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e12, 1)
+    out["gemm_shape"] = f"{m}x{m}x{m} bf16, torch.matmul"
+    att = result["stages"]["attention_roofline"]["achieved"]
+    sel = result["stages"]["select_roofline"]["achieved"]
+    out["attention_frac_of_gemm"] = round(att / out["bf16_gemm_tflops"], 4)
+    out["select_frac_of_copy"] = round(sel / out["hbm_copy_gbs"], 4)
+    return out
 
 
 def stress_comparison(dev):
@@ -338,12 +458,29 @@ def cpu_baseline(x, w, step_flops, reps=3):
         times.append(t2 - t0)
         sel_t.append(t1 - t0)
     full_s = float(np.median(times))
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = oracle.lib().oracle_max_threads()
+    # the same on one core: selection whole, attention on every 16th query row
+    # (all heads), scaled to all rows
+    with oracle.threads(1):
+        t0 = time.perf_counter()
+        ref = oracle.select(q, k, w.block_size, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks,
+                            w.scale)
+        t1 = time.perf_counter()
+        sub = qq.ravel() % 16 == 0
+        oracle.sparse_attn(q, k, v, w.block_size, ref["idx"], ref["cnt"], w.group_size, w.scale,
+                           hs=hh.ravel()[sub], qs=qq.ravel()[sub])
+        t2 = time.perf_counter()
+    attn1 = (t2 - t1) * sub.size / int(sub.sum())
     return {"value": round(step_flops / full_s / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
             "sample": f"one whole chunk-layer of the same workload (selection for all {w.heads} heads over the "
                       f"20-chunk history + selection attention for all {w.heads * w.query_tokens} (head, row) "
                       f"pairs), fp64, median of {reps} runs, {sum(times):.1f} s in total",
-            "ms_per_chunk_layer": round(full_s * 1e3, 1), "select_s": round(float(np.median(sel_t)), 3)}
+            "ms_per_chunk_layer": round(full_s * 1e3, 1), "select_s": round(float(np.median(sel_t)), 3),
+            "sparse_attn_s": round(float(np.median(times) - np.median(sel_t)), 3),
+            "one_core": {"select_s": round(t1 - t0, 3), "sparse_attn_s_extrapolated": round(attn1, 2),
+                         "ms_per_chunk_layer_extrapolated": round((t1 - t0 + attn1) * 1e3, 1),
+                         "sample": "selection whole; attention on every 16th query row of every head, "
+                                   "time scaled to all rows (extrapolated)"}}
 
 
 if __name__ == "__main__":

@@ -61,7 +61,21 @@ def _configure(L):
     L.oracle_dense_attn.argtypes = ([c_int] * 6 + [c_int, _vp, c_int, _vp, _vp, _u8p, c_int, c_int,
                                     ctypes.c_double, c_int, _i32p, _i32p, _f64p, _f64p])
     L.oracle_union.argtypes = [c_int, c_int, c_int, ctypes.c_int64, _i32p, _i32p, _i32p, _i32p]
+    L.oracle_set_threads.argtypes = [c_int]
+    L.oracle_max_threads.restype = c_int
     return L
+
+
+@contextlib.contextmanager
+def threads(n: int):
+    """Run the oracle's OpenMP regions on n threads inside the block (timing only)."""
+    L = lib()
+    prev = L.oracle_max_threads()
+    L.oracle_set_threads(n)
+    try:
+        yield
+    finally:
+        L.oracle_set_threads(prev)
 
 
 def lib():

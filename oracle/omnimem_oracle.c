@@ -28,6 +28,7 @@
  * Return value of every entry point: 0 on success, -1 on invalid arguments.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -429,3 +430,7 @@ int oracle_union(int H, int R, int top_k, int64_t nb, const int32_t* idx, const 
   free(mine);
   return 0;
 }
+
+/* Thread count of the OpenMP regions above (timing only; results do not depend on it). */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+int oracle_max_threads(void) { return omp_get_max_threads(); }
