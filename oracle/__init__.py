@@ -285,6 +285,46 @@ def dense_attn(q, k, v, B: int, chunk_begin: int, chunk_end: int, scale: float, 
     return out[:m], lse[:m], hs_a, qs_a
 
 
+def round_bf16(x):
+    """Round float64 values to the nearest bfloat16 (ties to even), returned as float64.
+    An 8-bit significand: the frexp mantissa m in [0.5, 1) is rounded to a multiple of
+    2^-8 with numpy's half-to-even rounding (normal range; values are not clamped)."""
+    x = np.asarray(x, dtype=np.float64)
+    m, e = np.frexp(x)
+    return np.ldexp(np.round(m * 256.0) / 256.0, e)
+
+
+def cmp_cache(k, v, B: int, round_to=None):
+    """The compressed history of App. C: one pooled key and value per block of every
+    chunk, the plain block mean of Sec. 3.1 / App. B (pool_keys applied to K and to V),
+    in block order: [H, n*Bpc, d] each.  round_to="bf16" rounds them to the stored
+    dtype (a bf16 cache holds the pooled values in bf16)."""
+    kc, vc = pool_keys(k, B), pool_keys(v, B)
+    if round_to == "bf16":
+        kc, vc = round_bf16(kc), round_bf16(vc)
+    elif round_to is not None:
+        raise ValueError(f"unknown rounding {round_to!r}")
+    return kc, vc
+
+
+def cmp_attn(q, kc, vc, scale: float, hs=None, qs=None):
+    """Compression attention, the CMP branch of Eq. 1: query i of head h attends to the
+    N pooled tokens kc[h], vc[h] ([H, N, d]) as one contiguous sequence (plain softmax
+    attention over them).  Evaluated as dense attention over a one-chunk history of N
+    tokens.  Returns (out [m, d], lse [m], hs, qs); N = 0 gives O = 0 and lse = -inf."""
+    kc = np.asarray(kc, dtype=np.float64)
+    vc = np.asarray(vc, dtype=np.float64)
+    H, N, d = kc.shape
+    Lq = int(q.shape[0])
+    if N == 0:
+        (hs_a, _), (qs_a, _) = _rows(H, Lq, hs, qs)
+        m = int(hs_a.shape[0])
+        return np.zeros((m, d)), np.full(m, -np.inf), hs_a, qs_a
+    k1 = np.ascontiguousarray(kc.transpose(1, 0, 2))[None]   # [1, N, H, d]
+    v1 = np.ascontiguousarray(vc.transpose(1, 0, 2))[None]
+    return dense_attn(q, k1, v1, N, 0, 1, scale, hs=hs, qs=qs)
+
+
 def union(idx, cnt, n_blocks: int):
     """Eq. 4 unions: returns (per-head |U_h| [H], cross-head |U|)."""
     idx_a, idx_p = _i32(idx)

@@ -273,6 +273,58 @@ def pin_sparse_all_blocks_equals_dense():
     assert np.allclose(o1, o2, atol=1e-12) and np.allclose(l1, l2, atol=1e-12)
 
 
+def pin_cmp_constant_blocks_equals_full():
+    # Compression attention (Eq. 1's CMP branch over App. C's pooled history): with
+    # every token of a block equal and every block full (S a multiple of B), a
+    # block's pooled token is that token, and full attention gives each block B equal
+    # logits, so the softmax weights of the two agree and their LSEs differ by ln B.
+    rng = np.random.default_rng(61)
+    n, S, H, d, B = 3, 8, 2, 5, 4
+    k = np.repeat(rng.standard_normal((n, S // B, H, d)), B, axis=1)
+    v = np.repeat(rng.standard_normal((n, S // B, H, d)), B, axis=1)
+    q = rng.standard_normal((6, H, d))
+    kc, vc = O.cmp_cache(k, v, B)
+    assert kc.shape == (H, n * S // B, d)
+    o1, l1, _, _ = O.cmp_attn(q, kc, vc, 0.4)
+    o2, l2, _, _ = O.dense_attn(q, k, v, B, 0, n, 0.4)
+    assert np.allclose(o1, o2, atol=1e-12) and np.allclose(l1 + math.log(B), l2, atol=1e-12)
+
+
+def pin_cmp_vs_library():
+    # Pooled tokens as numpy block means (partial tail blocks included), then
+    # textbook softmax attention by library routines over them.
+    q, k, v = _case(62, n=3, S=10, H=2, d=6, Lq=5)
+    B, scale = 4, 0.45
+    kc, vc = O.cmp_cache(k, v, B)
+    out, lse, hs, qs = O.cmp_attn(q, kc, vc, scale)
+    nb = 3 * O.blocks_per_chunk(10, B)
+    for i, (h, qi) in enumerate(zip(hs, qs)):
+        keys = np.stack([k[c, list(t), h].mean(axis=0) for c, t in (_block_tokens(b, 10, B) for b in range(nb))])
+        vals = np.stack([v[c, list(t), h].mean(axis=0) for c, t in (_block_tokens(b, 10, B) for b in range(nb))])
+        ref, ref_lse = _library_attention(q[qi, h], keys, vals, scale)
+        assert np.allclose(out[i], ref, atol=1e-12) and abs(lse[i] - ref_lse) < 1e-12, (h, qi)
+    # no history: O = 0, LSE = -inf
+    out, lse, _, _ = O.cmp_attn(q, kc[:, :0], vc[:, :0], scale)
+    assert np.all(out == 0) and np.all(np.isneginf(lse))
+
+
+def pin_bf16_rounding():
+    # bfloat16 keeps 8 significant bits; ties go to the even significand.
+    one = 1.0
+    cases = {one + 2.0 ** -8: one,                       # tie, even below
+             one + 3 * 2.0 ** -8: one + 2.0 ** -6,       # tie, even above
+             one + 2.0 ** -8 + 2.0 ** -20: one + 2.0 ** -7,
+             -(2.0 + 2.0 ** -7): -2.0,                   # tie at a larger exponent
+             255.5: 256.0, 0.0: 0.0}
+    for x, want in cases.items():
+        assert O.round_bf16(x) == want, (x, O.round_bf16(x), want)
+    # against a library conversion on values that fp32 holds exactly
+    import torch
+    x = np.random.default_rng(63).standard_normal(4096).astype(np.float32).astype(np.float64)
+    lib = torch.from_numpy(x).to(torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    assert np.array_equal(O.round_bf16(x), lib)
+
+
 def pin_attention_special_cases():
     rng = np.random.default_rng(31)
     n, S, H, d = 2, 6, 1, 4
