@@ -52,6 +52,7 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
     p.add_argument("--stress", action="store_true", help="add the 14B-shaped union-gather comparison")
     p.add_argument("--no-ramp", action="store_true", help="skip the 30-layer, 1 -> 60 chunk ramp")
+    p.add_argument("--no-compressed", action="store_true", help="skip the compressed-history path")
     p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
     return p.parse_args()
 
@@ -221,6 +222,11 @@ def main():
                    "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe},
     }
 
+    # ---------------------------------------------------------------- compressed history
+    if not args.no_compressed:
+        log("compressed-history path (pool the newest chunk + select from pooled keys + sparse attention)")
+        result["compressed"] = compressed_measure(dev, layers, sels, outs, lses, w, args)
+
     # ---------------------------------------------------------------- sweep
     if not args.no_sweep:
         wl = synth.WORKLOADS["wan1.3b_long"]
@@ -232,6 +238,13 @@ def main():
         del xl.k, xl.v
         wsl = workspace_tensor(omnimem_select_workspace_bytes(cl, wl.query_tokens, params), dev)
         sweep = []
+        ccl = None
+        if not args.no_compressed:
+            from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk,
+                                              omnimem_select_compressed)
+            ccl = CompressedCache.allocate(cl, 120)
+            for c in range(120):
+                omnimem_compress_chunk(cl, c, ccl)
         for hn in (10, 30, 60, 120):
             q = synth.queries(wl, 0, hn, xl.rel, dev)
             s = Selection(torch.empty((H, R, K), dtype=torch.int32, device=dev),
@@ -264,6 +277,23 @@ def main():
                           "dense_ms": round(float(td), 4),
                           "dense_tflops": round(dense_fl / (td * 1e-3) / 1e12, 2),
                           "speedup_vs_dense": round(float(td / (ts + ta)), 2)})
+            if ccl is not None:
+                e = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps + 1)]
+                for r in range(reps + 1):
+                    e[r][0].record()
+                    omnimem_select_compressed(cl, ccl, q, K, wl.group_size, wl.window_chunks,
+                                              wl.awe_min_outside_chunks, wl.scale, num_chunks=hn, workspace=wsl,
+                                              out=s, want_score=False)
+                    e[r][1].record()
+                    omnimem_cmp_attn(ccl, hn, q, wl.scale, out=out, lse=ls)
+                    e[r][2].record()
+                torch.cuda.synchronize()
+                tsc = np.median([e[r][0].elapsed_time(e[r][1]) for r in range(1, reps + 1)])
+                tcm = np.median([e[r][1].elapsed_time(e[r][2]) for r in range(1, reps + 1)])
+                cmp_fl = 4.0 * wl.head_dim * wl.heads * wl.query_tokens * hn * wl.blocks_per_chunk
+                sweep[-1].update({"select_compressed_ms": round(float(tsc), 4),
+                                  "cmp_attn_ms": round(float(tcm), 4),
+                                  "cmp_attn_tflops": round(cmp_fl / (tcm * 1e-3) / 1e12, 2)})
         result["sweep"] = sweep
         del cl
 
@@ -291,6 +321,80 @@ def main():
         result["cpu_baseline"] = cpu_baseline(x0, w, flops_per_layer[0] + sflops)
 
     print(json.dumps(result), flush=True)
+
+
+def compressed_measure(dev, layers, sels, outs, lses, w, args):
+    """The chunk step with App. C's compressed history: each step pools only the
+    newest chunk into the layer's compressed cache, selects from the pooled keys and
+    runs the same sparse attention.  Same rotated layer caches and steps as the main
+    measurement; the pooled history of the older chunks was built beforehand, as it
+    is when each chunk is appended."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk,
+                                      omnimem_select_compressed, omnimem_select_workspace_bytes,
+                                      omnimem_sparse_attn, select_params)
+    from paper_2605_30519_amd.omnimem import workspace_tensor
+    n, K = w.history_chunks, w.top_k
+    ccs = [CompressedCache.allocate(cache, n) for _, cache in layers]
+    for (q, cache), cc in zip(layers, ccs):
+        for c in range(n):
+            omnimem_compress_chunk(cache, c, cc)
+    params = select_params(K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    ws = workspace_tensor(omnimem_select_workspace_bytes(layers[0][1], w.query_tokens, params), dev)
+
+    def step(i, ev=None):
+        q, cache = layers[i % len(layers)]
+        cc, s = ccs[i % len(layers)], sels[i % len(layers)]
+        if ev is not None:
+            ev[0].record()
+        omnimem_compress_chunk(cache, n - 1, cc)
+        if ev is not None:
+            ev[1].record()
+        omnimem_select_compressed(cache, cc, q, K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                                  workspace=ws, out=s, want_score=False)
+        if ev is not None:
+            ev[2].record()
+        omnimem_sparse_attn(cache, q, s.idx, s.cnt, w.group_size, w.scale, out=outs[i % len(layers)],
+                            lse=lses[i % len(layers)])
+        if ev is not None:
+            ev[3].record()
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    flops = [attn_flops(s.idx, s.cnt, w, n) + score_flops(w, n) for s in sels]
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(args.steps):
+        step(i)
+    t1.record()
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / args.steps
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    for i in range(args.steps):
+        step(i, evs[i])
+    torch.cuda.synchronize()
+    med = lambda a, b: float(np.median([e[a].elapsed_time(e[b]) for e in evs]))
+    # compression attention over the same pooled history (Eq. 1's CMP branch)
+    q0, _ = layers[0]
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    for _ in range(5):
+        omnimem_cmp_attn(ccs[0], n, q0, w.scale, out=outs[0], lse=lses[0])
+    e[0].record()
+    for _ in range(20):
+        omnimem_cmp_attn(ccs[0], n, q0, w.scale, out=outs[0], lse=lses[0])
+    e[1].record()
+    torch.cuda.synchronize()
+    cmp_ms = e[0].elapsed_time(e[1]) / 20
+    cmp_fl = 4.0 * w.head_dim * w.heads * w.query_tokens * n * w.blocks_per_chunk
+    return {"step": "pool the newest chunk + select from the pooled keys + sparse attention",
+            "ms_per_chunk_layer": round(ms, 4),
+            "effective_tflops": round(float(np.mean(flops)) / (ms * 1e-3) / 1e12, 2),
+            "compress_chunk_ms": round(med(0, 1), 4), "select_compressed_ms": round(med(1, 2), 4),
+            "sparse_attn_ms": round(med(2, 3), 4),
+            "cmp_attn_ms": round(cmp_ms, 4), "cmp_attn_tflops": round(cmp_fl / (cmp_ms * 1e-3) / 1e12, 2)}
 
 
 def ramp_measure(dev, layers_n=30, warm_passes=20):

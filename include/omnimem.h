@@ -14,6 +14,10 @@
  * history (the full-attention reference of Sec. 4.3) or the sliding window (App. C).
  * omnimem_union_gather_attn is the naive comparator of Sec. 3.3 that materialises
  * the cross-head union of selected blocks in a head-aligned buffer first.
+ * The compressed history (App. C's first cache level) pools each chunk once, when
+ * it is appended (omnimem_compress_chunk); omnimem_select_compressed then scores
+ * from the pooled keys instead of streaming all of K, and omnimem_cmp_attn is the
+ * compression branch of Eq. 1 over the pooled keys and values.
  *
  * Conventions shared by every entry point
  *  - Every buffer pointer is a DEVICE pointer unless marked (host).  The caller
@@ -189,6 +193,75 @@ omnimem_status_t omnimem_union_gather_attn(const omnimem_kv_cache_t* kv, const v
 
 /* Static, human-readable text for a status code. */
 const char* omnimem_status_string(int32_t status);
+
+/*
+ * Compressed history of one layer (App. C: the compact first cache level; Sec. 3.1:
+ * the compression branch pools with a plain mean, App. B).  Each block of each
+ * appended chunk is pooled once into one pooled key and one pooled value, the
+ * means over the block's valid tokens.  Pooled token t is history block t
+ * (t = c*Bpc + o, Alg. 1's block numbering), so n chunks hold pooled tokens
+ * [0, n*Bpc) in append order.
+ *
+ *   k_mean      [H][capacity_chunks*Bpc][d] float: the pooled keys in fp32, read by
+ *               omnimem_select_compressed (the scores then equal omnimem_select's).
+ *   k_pages,    [num_pages][H][64][d] of dtype: the pooled keys and values rounded
+ *   v_pages     to dtype (bf16: to nearest even), 64 pooled tokens per page, page p
+ *               holding tokens [64p, 64p + 64); read by omnimem_cmp_attn.
+ *               num_pages >= ceil(capacity_chunks*Bpc / 64).
+ *   page_table  [num_pages] int32: entry p = p, written by omnimem_compress_chunk
+ *               for every page its chunk touches.
+ * The caller allocates and owns every buffer (16-byte aligned; page_table 4-byte).
+ * Geometry (dtype, H, d, B, S) must equal the full cache's.
+ */
+typedef struct {
+  omnimem_dtype_t dtype;        /* of k_pages and v_pages: the full cache's dtype */
+  int32_t num_heads, head_dim;  /* H, d */
+  int32_t block_size;           /* B of the full cache: one pooled token per block */
+  int32_t chunk_tokens;         /* S of the full cache: Bpc = ceil(S/B) pooled tokens per chunk */
+  int32_t capacity_chunks;      /* chunks the buffers hold */
+  float* k_mean;
+  void* k_pages;
+  void* v_pages;
+  int32_t* page_table;
+  int64_t num_pages;            /* pages of k_pages / v_pages */
+} omnimem_cmp_cache_t;
+
+/*
+ * Pools history chunk `chunk` (0 <= chunk < kv->num_chunks, < capacity_chunks) of
+ * the full cache into the compressed cache (App. C: each generated chunk's KV is
+ * pooled once and appended).  For each block b = chunk*Bpc + o and head h:
+ *   k_mean[h][b] = (1/|b|) sum over the block's valid tokens of K   (fp32)
+ *   pooled token b of k_pages / v_pages = the means of K / V rounded to dtype.
+ * A block whose page is not resident (page id < 0 or >= kv->num_pages) pools to 0.
+ * Re-pooling a chunk overwrites it with the same values.
+ */
+omnimem_status_t omnimem_compress_chunk(const omnimem_kv_cache_t* kv, int32_t chunk, const omnimem_cmp_cache_t* cc,
+                                        void* stream);
+
+/*
+ * omnimem_select over the compressed history: the same contract, arguments and
+ * outputs, with the pooled keys read from cc->k_mean (chunks [0, kv->num_chunks)
+ * must have been pooled; kv->num_chunks <= capacity_chunks) instead of pooled from
+ * the full cache's pages.  kv still supplies the geometry, the history length and
+ * residency (a block whose page is not resident is not a candidate).  The workspace
+ * is sized by omnimem_select_workspace_bytes(kv, lq, p).
+ */
+omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const omnimem_cmp_cache_t* cc,
+                                           const void* q, int32_t lq, const omnimem_select_params_t* p,
+                                           int32_t* idx, int32_t* cnt, float* score, int32_t* awe_active,
+                                           void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Compression attention, the CMP branch of Eq. 1 (Sec. 3.1, App. C): every query
+ * attends to the n_chunks*Bpc pooled tokens of the compressed history,
+ *   O[i][h]   = sum_t softmax_t(scale * <q_i, kc_t>) vc_t
+ *   lse[h][i] = ln sum_t exp(scale * <q_i, kc_t>)
+ * with kc, vc the pooled keys and values as stored in k_pages / v_pages.
+ * 0 <= n_chunks <= capacity_chunks; n_chunks = 0 gives O = 0 and lse = -inf.
+ * q, out, lse and the arithmetic are as in omnimem_dense_attn.
+ */
+omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int32_t n_chunks, const void* q, int32_t lq,
+                                  float scale, void* out, float* lse, void* stream);
 
 #ifdef __cplusplus
 }

@@ -7,6 +7,7 @@ library is opened on the first call.
 """
 from .omnimem import (  # noqa: F401
     EXPORTED,
+    CompressedCache,
     OmniMemError,
     PagedKVCache,
     Selection,
@@ -14,8 +15,11 @@ from .omnimem import (  # noqa: F401
     library_path,
     omnimem_awe_active,
     omnimem_blocks_per_chunk,
+    omnimem_cmp_attn,
+    omnimem_compress_chunk,
     omnimem_dense_attn,
     omnimem_select,
+    omnimem_select_compressed,
     omnimem_select_workspace_bytes,
     omnimem_sparse_attn,
     omnimem_status_string,

@@ -170,6 +170,117 @@ OMNIMEM_API omnimem_status_t omnimem_dense_attn(const omnimem_kv_cache_t* kv, co
   return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
 }
 
+namespace {
+
+// Validates a compressed cache against the full cache's geometry.
+omnimem_status_t resolve_cmp(const omnimem_cmp_cache_t* cc, const CacheGeom& g, omnimem::CmpCache& c) {
+  if (cc == nullptr) return OMNIMEM_EINVAL;
+  if ((cc->dtype == OMNIMEM_BF16 ? 0 : cc->dtype == OMNIMEM_F32 ? 1 : -1) != g.dtype) return OMNIMEM_EINVAL;
+  if (cc->num_heads != g.H || cc->head_dim != g.D || cc->block_size != g.B || cc->chunk_tokens != g.S)
+    return OMNIMEM_EINVAL;
+  if (cc->capacity_chunks < 0 || cc->num_pages < 0) return OMNIMEM_EINVAL;
+  const int64_t cap = static_cast<int64_t>(cc->capacity_chunks) * g.Bpc;
+  if (cap > (int64_t{1} << 30)) return OMNIMEM_EINVAL;
+  const int64_t pages = (cap + omnimem::kCmpPageTokens - 1) / omnimem::kCmpPageTokens;
+  if (cc->num_pages < pages) return OMNIMEM_EINVAL;
+  if (cap > 0 && (cc->k_mean == nullptr || cc->k_pages == nullptr || cc->v_pages == nullptr ||
+                  cc->page_table == nullptr))
+    return OMNIMEM_EINVAL;
+  if (!aligned16(cc->k_mean) || !aligned16(cc->k_pages) || !aligned16(cc->v_pages) ||
+      (reinterpret_cast<uintptr_t>(cc->page_table) & 3u))
+    return OMNIMEM_EINVAL;
+  c.k_mean = cc->k_mean;
+  c.k_pages = cc->k_pages;
+  c.v_pages = cc->v_pages;
+  c.page_table = cc->page_table;
+  c.num_pages = cc->num_pages;
+  c.cap_blocks = static_cast<int>(cap);
+  return OMNIMEM_OK;
+}
+
+}  // namespace
+
+OMNIMEM_API omnimem_status_t omnimem_compress_chunk(const omnimem_kv_cache_t* kv, int32_t chunk,
+                                                    const omnimem_cmp_cache_t* cc, void* stream) {
+  CacheGeom g;
+  omnimem_status_t st = resolve_cache(kv, g);
+  if (st != OMNIMEM_OK) return st;
+  omnimem::CmpCache c;
+  st = resolve_cmp(cc, g, c);
+  if (st != OMNIMEM_OK) return st;
+  if (chunk < 0 || chunk >= g.n || chunk >= cc->capacity_chunks) return OMNIMEM_EINVAL;
+  return hip_status(omnimem::launch_compress_chunk(g, c, chunk, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const omnimem_cmp_cache_t* cc,
+                                                       const void* q, int32_t lq, const omnimem_select_params_t* p,
+                                                       int32_t* idx, int32_t* cnt, float* score, int32_t* awe_active,
+                                                       void* workspace, size_t workspace_bytes, void* stream) {
+  CacheGeom g;
+  omnimem::SelectPlan plan;
+  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
+  if (st != OMNIMEM_OK) return st;
+  omnimem::CmpCache c;
+  st = resolve_cmp(cc, g, c);
+  if (st != OMNIMEM_OK) return st;
+  if (g.n > cc->capacity_chunks) return OMNIMEM_EINVAL;
+  if (awe_active) *awe_active = plan.awe;
+  if (lq == 0) return OMNIMEM_OK;
+  if (q == nullptr || idx == nullptr || cnt == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
+  if (!aligned16(q) || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
+  if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
+  return hip_status(omnimem::launch_select_compressed(g, c, plan, q, idx, cnt, score, workspace,
+                                                      static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int32_t n_chunks, const void* q,
+                                              int32_t lq, float scale, void* out, float* lse, void* stream) {
+  if (cc == nullptr) return OMNIMEM_EINVAL;
+  // the pooled sequence as a one-chunk paged cache of n_chunks * Bpc tokens
+  omnimem_kv_cache_t seq{};
+  seq.dtype = cc->dtype;
+  seq.num_heads = cc->num_heads;
+  seq.head_dim = cc->head_dim;
+  seq.block_size = cc->block_size;
+  seq.chunk_tokens = cc->chunk_tokens;
+  seq.num_chunks = 0;
+  seq.num_pages = 0;
+  CacheGeom full;
+  omnimem_status_t st = resolve_cache(&seq, full);
+  if (st != OMNIMEM_OK) return st;
+  omnimem::CmpCache c;
+  st = resolve_cmp(cc, full, c);
+  if (st != OMNIMEM_OK) return st;
+  if (n_chunks < 0 || n_chunks > cc->capacity_chunks || !good_scale(scale)) return OMNIMEM_EINVAL;
+  const int64_t tokens = static_cast<int64_t>(n_chunks) * full.Bpc;
+  CacheGeom g = full;
+  g.B = omnimem::kCmpPageTokens;
+  g.S = tokens > 0 ? static_cast<int>(tokens) : 1;
+  g.n = tokens > 0 ? 1 : 0;
+  g.Bpc = (g.S + g.B - 1) / g.B;
+  g.nb = g.n * g.Bpc;
+  g.num_pages = c.num_pages;
+  g.k_pages = c.k_pages;
+  g.v_pages = c.v_pages;
+  g.page_table = c.page_table;
+  st = check_attn_common(g, q, lq, out);
+  if (st != OMNIMEM_OK || lq == 0) return st;
+  omnimem::AttnLaunch a{};
+  a.q = q;
+  a.out = out;
+  a.lse = lse;
+  a.lq = lq;
+  a.group_size = lq;
+  a.R = 1;
+  a.idx = nullptr;
+  a.cnt = nullptr;
+  a.top_k = 1;
+  a.dense_first_block = 0;
+  a.dense_num_blocks = g.nb;
+  a.scale = scale;
+  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+}
+
 OMNIMEM_API size_t omnimem_union_workspace_bytes(const omnimem_kv_cache_t* kv) {
   CacheGeom g;
   if (resolve_cache(kv, g) != OMNIMEM_OK) return 0;

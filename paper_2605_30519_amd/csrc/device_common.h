@@ -28,6 +28,13 @@ __device__ __forceinline__ int xcd_contiguous_id(int bid, int nblocks) {
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
 
+// fp32 -> bf16 bit pattern, rounded to nearest even (NaN stays a quiet NaN).
+__device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
+  const uint32_t u = __float_as_uint(x);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+}
+
 // 16-byte vector load widened to fp32: 8 bf16 or 4 fp32 values.
 template <typename T>
 struct Vec16;

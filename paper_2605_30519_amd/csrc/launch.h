@@ -40,6 +40,24 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
 hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
                          float* score, void* workspace, hipStream_t stream);
 
+// ---------------------------------------------------------------- compressed history
+// One pooled key/value per history block, in block order (token t = block t).
+struct CmpCache {
+  float* k_mean;         // [H][cap_blocks][D] fp32 pooled keys
+  void* k_pages;         // [num_pages][H][64][D] pooled keys in the cache dtype
+  void* v_pages;         // same, pooled values
+  int32_t* page_table;   // [num_pages], entry p = p
+  int64_t num_pages;
+  int cap_blocks;        // capacity in pooled tokens
+};
+constexpr int kCmpPageTokens = 64;
+
+hipError_t launch_compress_chunk(const CacheGeom& g, const CmpCache& cc, int chunk, hipStream_t stream);
+
+// Selection with the pooled keys read from cc.k_mean (plan from plan_select).
+hipError_t launch_select_compressed(const CacheGeom& g, const CmpCache& cc, const SelectPlan& p, const void* q,
+                                    int32_t* idx, int32_t* cnt, float* score, void* workspace, hipStream_t stream);
+
 // ---------------------------------------------------------------- attention
 struct AttnLaunch {
   const void* q;

@@ -276,7 +276,8 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
 
 // score keys for many groups: tile of 64 blocks x 16 groups per workgroup
 template <int D>
-__global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kbar, const float* __restrict__ qpart,
+__global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kbar, int64_t kbar_stride,
+                                                    const float* __restrict__ qpart,
                                                     int nsplit, int lq, int G, const int32_t* __restrict__ page_table,
                                                     int64_t num_pages, int nb, int nbp, int first_excluded, int R,
                                                     float scale, uint32_t* __restrict__ keys) {
@@ -286,7 +287,7 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
   const int b0 = blockIdx.x * TB, r0 = blockIdx.y * TR, h = blockIdx.z;
   for (int i = threadIdx.x; i < TB * D; i += kThreads) {
     const int bb = i / D, j = i % D;
-    ks[bb][j] = b0 + bb < nb ? kbar[(static_cast<int64_t>(h) * nb + b0 + bb) * D + j] : 0.f;
+    ks[bb][j] = b0 + bb < nb ? kbar[(static_cast<int64_t>(h) * kbar_stride + b0 + bb) * D + j] : 0.f;
   }
   for (int i = threadIdx.x; i < TR * D; i += kThreads) {
     const int rr = i / D, j = i % D;
@@ -304,6 +305,82 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
     const int32_t p = page_table[b];
     const bool live = b < first_excluded && p >= 0 && p < num_pages;
     keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * dot) : 0u;
+  }
+}
+
+// -------------------------------------------------------------- compressed history
+// Pools one history chunk into the compressed cache: one wave per (block, head)
+// slab; the block's K and V column means go to k_mean (fp32) and, rounded to the
+// cache dtype, to pooled token b of the paged pooled sequence.
+struct CompressArgs {
+  const void* k_pages;
+  const void* v_pages;
+  const int32_t* page_table;
+  int64_t num_pages;
+  int H, S, Bpc, chunk;
+  float* k_mean;
+  void* ck_pages;
+  void* cv_pages;
+  int32_t* c_page_table;
+  int cap_blocks;
+};
+
+template <typename T>
+__device__ __forceinline__ void store_rounded(T* dst, const float (&x)[Vec16<T>::N]);
+
+template <>
+__device__ __forceinline__ void store_rounded<uint16_t>(uint16_t* dst, const float (&x)[8]) {
+  uint4 w;
+  w.x = f32_to_bf16_rne(x[0]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[1])) << 16);
+  w.y = f32_to_bf16_rne(x[2]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[3])) << 16);
+  w.z = f32_to_bf16_rne(x[4]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[5])) << 16);
+  w.w = f32_to_bf16_rne(x[6]) | (static_cast<uint32_t>(f32_to_bf16_rne(x[7])) << 16);
+  *reinterpret_cast<uint4*>(dst) = w;
+}
+
+template <>
+__device__ __forceinline__ void store_rounded<float>(float* dst, const float (&x)[4]) {
+  *reinterpret_cast<float4*>(dst) = make_float4(x[0], x[1], x[2], x[3]);
+}
+
+template <typename T, int D, int B>
+__global__ __launch_bounds__(kThreads) void k_compress_chunk(CompressArgs a) {
+  using Sh = SlabShape<T, D, B>;
+  constexpr int VEC = Sh::VEC;
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int o = blockIdx.x * (kThreads / kWave) + wave, h = blockIdx.y;
+  if (o >= a.Bpc) return;
+  const int b = a.chunk * a.Bpc + o;
+  const int c = lane % Sh::CPR;
+  const int64_t page = a.page_table[b];
+  const bool live = page >= 0 && page < a.num_pages;
+  const int nvalid = o == a.Bpc - 1 ? a.S - o * B : B;
+  float ks[VEC], vs[VEC];
+#pragma unroll
+  for (int j = 0; j < VEC; ++j) ks[j] = vs[j] = 0.f;
+  if (live) {
+    const int64_t off = (page * a.H + h) * static_cast<int64_t>(B) * D;
+    uint4 raw[Sh::PASSES];
+    load_slab<T, D, B>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, raw);
+    sum_slab<T, D, B>(raw, ks);
+    load_slab<T, D, B>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, raw);
+    sum_slab<T, D, B>(raw, vs);
+    const float inv = 1.0f / static_cast<float>(nvalid);
+#pragma unroll
+    for (int j = 0; j < VEC; ++j) {
+      ks[j] *= inv;
+      vs[j] *= inv;
+    }
+  }
+  if (lane < Sh::CPR) {
+    float* km = a.k_mean + (static_cast<int64_t>(h) * a.cap_blocks + b) * D + c * VEC;
+#pragma unroll
+    for (int j = 0; j < VEC; j += 4) *reinterpret_cast<float4*>(km + j) = make_float4(ks[j], ks[j + 1], ks[j + 2], ks[j + 3]);
+    const int64_t cp = b / kCmpPageTokens, slot = b % kCmpPageTokens;
+    const int64_t at = ((cp * a.H + h) * kCmpPageTokens + slot) * D + c * VEC;
+    store_rounded<T>(static_cast<T*>(a.ck_pages) + at, ks);
+    store_rounded<T>(static_cast<T*>(a.cv_pages) + at, vs);
+    if (lane == 0 && h == 0 && (slot == 0 || o == 0)) a.c_page_table[cp] = static_cast<int32_t>(cp);
   }
 }
 
@@ -644,6 +721,19 @@ __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict_
 
 inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* keys, int nbp, int32_t* idx,
+                       int32_t* cnt, float* score, hipStream_t stream) {
+  const dim3 tgrid(p.R, g.H);
+  // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice that
+  if (g.nb <= 512 * 4 * kTopkVecPerLane)
+    hipLaunchKernelGGL(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  else if (g.nb <= kTopkRegMax)
+    hipLaunchKernelGGL(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  else
+    hipLaunchKernelGGL(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  return hipGetLastError();
+}
+
 template <typename T, int D>
 hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
                                float* score, void* workspace, hipStream_t stream) {
@@ -689,19 +779,12 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     }
     if (!p.inline_scores) {
       const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
-      hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, kbar, qpart, p.qsplit, p.lq, p.G,
+      hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, kbar, static_cast<int64_t>(g.nb), qpart,
+                         p.qsplit, p.lq, p.G,
                          g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
     }
   }
-  const dim3 tgrid(p.R, g.H);
-  // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice that
-  if (g.nb <= 512 * 4 * kTopkVecPerLane)
-    hipLaunchKernelGGL(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  else if (g.nb <= kTopkRegMax)
-    hipLaunchKernelGGL(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  else
-    hipLaunchKernelGGL(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  return hipGetLastError();
+  return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
 
 }  // namespace
@@ -728,6 +811,68 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
   off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
   p.total = off;
   return p;
+}
+
+template <typename T, int D>
+hipError_t launch_compress_typed(const CacheGeom& g, const CmpCache& cc, int chunk, hipStream_t stream) {
+  CompressArgs a;
+  a.k_pages = g.k_pages;
+  a.v_pages = g.v_pages;
+  a.page_table = g.page_table;
+  a.num_pages = g.num_pages;
+  a.H = g.H;
+  a.S = g.S;
+  a.Bpc = g.Bpc;
+  a.chunk = chunk;
+  a.k_mean = cc.k_mean;
+  a.ck_pages = cc.k_pages;
+  a.cv_pages = cc.v_pages;
+  a.c_page_table = cc.page_table;
+  a.cap_blocks = cc.cap_blocks;
+  const dim3 grid((g.Bpc + kThreads / kWave - 1) / (kThreads / kWave), g.H);
+  if (g.B == 64)
+    hipLaunchKernelGGL((k_compress_chunk<T, D, 64>), grid, dim3(kThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_compress_chunk<T, D, 128>), grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc, const SelectPlan& p, const void* q,
+                                          int32_t* idx, int32_t* cnt, float* score, void* workspace,
+                                          hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  float* qpart = reinterpret_cast<float*>(ws + p.off_qpart);
+  uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
+  const int nbp = (g.nb + 3) / 4 * 4;
+  hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kQThreads), 0, stream,
+                     static_cast<const T*>(q), p.lq, g.H, p.G, p.R, p.qsplit, qpart);
+  if (g.nb > 0) {
+    const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
+    hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, cc.k_mean, static_cast<int64_t>(cc.cap_blocks),
+                       qpart, p.qsplit, p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R,
+                       p.scale, keys);
+  }
+  return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
+}
+
+hipError_t launch_compress_chunk(const CacheGeom& g, const CmpCache& cc, int chunk, hipStream_t stream) {
+  if (g.dtype == 0) {
+    if (g.D == 128) return launch_compress_typed<uint16_t, 128>(g, cc, chunk, stream);
+    return launch_compress_typed<uint16_t, 64>(g, cc, chunk, stream);
+  }
+  if (g.D == 128) return launch_compress_typed<float, 128>(g, cc, chunk, stream);
+  return launch_compress_typed<float, 64>(g, cc, chunk, stream);
+}
+
+hipError_t launch_select_compressed(const CacheGeom& g, const CmpCache& cc, const SelectPlan& p, const void* q,
+                                    int32_t* idx, int32_t* cnt, float* score, void* workspace, hipStream_t stream) {
+  if (g.dtype == 0) {
+    if (g.D == 128) return launch_select_compressed_typed<uint16_t, 128>(g, cc, p, q, idx, cnt, score, workspace, stream);
+    return launch_select_compressed_typed<uint16_t, 64>(g, cc, p, q, idx, cnt, score, workspace, stream);
+  }
+  if (g.D == 128) return launch_select_compressed_typed<float, 128>(g, cc, p, q, idx, cnt, score, workspace, stream);
+  return launch_select_compressed_typed<float, 64>(g, cc, p, q, idx, cnt, score, workspace, stream);
 }
 
 hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,

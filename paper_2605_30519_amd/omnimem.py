@@ -3,7 +3,9 @@ step of the computation runs in the HIP kernels behind the C ABI declared in
 include/omnimem.h.  PyTorch supplies device memory and the current stream.
 
 The functions carry the C names: omnimem_select, omnimem_sparse_attn,
-omnimem_dense_attn, omnimem_union_gather_attn, plus the host-side helpers.
+omnimem_dense_attn, omnimem_union_gather_attn, the compressed-history calls
+omnimem_compress_chunk, omnimem_select_compressed and omnimem_cmp_attn, plus the
+host-side helpers.
 """
 from __future__ import annotations
 
@@ -56,6 +58,22 @@ class omnimem_select_params_t(ctypes.Structure):
     ]
 
 
+class omnimem_cmp_cache_t(ctypes.Structure):
+    _fields_ = [
+        ("dtype", ctypes.c_int32),
+        ("num_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("block_size", ctypes.c_int32),
+        ("chunk_tokens", ctypes.c_int32),
+        ("capacity_chunks", ctypes.c_int32),
+        ("k_mean", ctypes.c_void_p),
+        ("k_pages", ctypes.c_void_p),
+        ("v_pages", ctypes.c_void_p),
+        ("page_table", ctypes.c_void_p),
+        ("num_pages", ctypes.c_int64),
+    ]
+
+
 EXPORTED = [
     "omnimem_blocks_per_chunk",
     "omnimem_awe_active",
@@ -66,6 +84,9 @@ EXPORTED = [
     "omnimem_union_workspace_bytes",
     "omnimem_union_gather_attn",
     "omnimem_status_string",
+    "omnimem_compress_chunk",
+    "omnimem_select_compressed",
+    "omnimem_cmp_attn",
 ]
 
 
@@ -91,6 +112,13 @@ def _configure(L):
     L.omnimem_union_gather_attn.restype = i32
     L.omnimem_status_string.argtypes = [i32]
     L.omnimem_status_string.restype = ctypes.c_char_p
+    ccp = ctypes.POINTER(omnimem_cmp_cache_t)
+    L.omnimem_compress_chunk.argtypes = [kvp, i32, ccp, vp]
+    L.omnimem_compress_chunk.restype = i32
+    L.omnimem_select_compressed.argtypes = [kvp, ccp, vp, i32, pp, vp, vp, vp, ctypes.POINTER(i32), vp, sz, vp]
+    L.omnimem_select_compressed.restype = i32
+    L.omnimem_cmp_attn.argtypes = [ccp, i32, vp, i32, f32, vp, vp, vp]
+    L.omnimem_cmp_attn.restype = i32
     return L
 
 
@@ -309,3 +337,89 @@ def omnimem_union_gather_attn(cache: PagedKVCache, q: torch.Tensor, idx: torch.T
                                          _ptr(union_blocks), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "omnimem_union_gather_attn")
     return out, lse, union_blocks
+
+
+# ------------------------------------------------------- compressed history
+
+CMP_PAGE_TOKENS = 64
+
+
+@dataclass
+class CompressedCache:
+    """One layer's compressed history (device tensors): k_mean [H, cap*Bpc, d] fp32,
+    k_pages / v_pages [pages, H, 64, d] in the full cache's dtype, page_table [pages]."""
+    k_mean: torch.Tensor
+    k_pages: torch.Tensor
+    v_pages: torch.Tensor
+    page_table: torch.Tensor
+    block_size: int
+    chunk_tokens: int
+    capacity_chunks: int
+
+    @classmethod
+    def allocate(cls, cache: PagedKVCache, capacity_chunks: int) -> "CompressedCache":
+        H, d, dev = cache.num_heads, cache.head_dim, cache.k_pages.device
+        tokens = capacity_chunks * cache.blocks_per_chunk
+        pages = max(1, -(-tokens // CMP_PAGE_TOKENS))
+        return cls(torch.zeros((H, max(tokens, 1), d), dtype=torch.float32, device=dev),
+                   torch.zeros((pages, H, CMP_PAGE_TOKENS, d), dtype=cache.dtype, device=dev),
+                   torch.zeros((pages, H, CMP_PAGE_TOKENS, d), dtype=cache.dtype, device=dev),
+                   torch.zeros(pages, dtype=torch.int32, device=dev),
+                   cache.block_size, cache.chunk_tokens, int(capacity_chunks))
+
+    def descriptor(self) -> omnimem_cmp_cache_t:
+        return omnimem_cmp_cache_t(
+            _DTYPES[self.k_pages.dtype], int(self.k_pages.shape[1]), int(self.k_pages.shape[3]), self.block_size,
+            self.chunk_tokens, self.capacity_chunks, self.k_mean.data_ptr(), self.k_pages.data_ptr(),
+            self.v_pages.data_ptr(), self.page_table.data_ptr(), int(self.k_pages.shape[0]))
+
+
+def omnimem_compress_chunk(cache: PagedKVCache, chunk: int, cc: CompressedCache, *,
+                           num_chunks: Optional[int] = None, stream=None) -> None:
+    desc = cache.descriptor(num_chunks)
+    cdesc = cc.descriptor()
+    _check(lib().omnimem_compress_chunk(ctypes.byref(desc), int(chunk), ctypes.byref(cdesc), _stream(stream)),
+           "omnimem_compress_chunk")
+
+
+def omnimem_select_compressed(cache: PagedKVCache, cc: CompressedCache, q: torch.Tensor, top_k: int, group_size: int,
+                              window_chunks: int, awe_min_outside_chunks: int, scale: Optional[float] = None, *,
+                              num_chunks: Optional[int] = None, want_score: bool = True,
+                              workspace: Optional[torch.Tensor] = None, out: Optional[Selection] = None,
+                              stream=None) -> Selection:
+    lq, H, d = (int(s) for s in q.shape)
+    params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
+    desc = cache.descriptor(num_chunks)
+    cdesc = cc.descriptor()
+    R = -(-lq // group_size)
+    dev = q.device
+    if out is None:
+        out = Selection(torch.empty((H, R, top_k), dtype=torch.int32, device=dev),
+                        torch.empty((H, R), dtype=torch.int32, device=dev),
+                        torch.empty((H, R, top_k), dtype=torch.float32, device=dev) if want_score else None, 0)
+    need = int(lib().omnimem_select_workspace_bytes(ctypes.byref(desc), lq, ctypes.byref(params)))
+    if workspace is None:
+        workspace = workspace_tensor(need, dev)
+    awe = ctypes.c_int32(0)
+    st = lib().omnimem_select_compressed(ctypes.byref(desc), ctypes.byref(cdesc), _ptr(q), lq, ctypes.byref(params),
+                                         _ptr(out.idx), _ptr(out.cnt), _ptr(out.score), ctypes.byref(awe),
+                                         _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "omnimem_select_compressed")
+    out.awe_active = int(awe.value)
+    return out
+
+
+def omnimem_cmp_attn(cc: CompressedCache, n_chunks: int, q: torch.Tensor, scale: Optional[float] = None, *,
+                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
+                     stream=None):
+    lq, H, d = (int(s) for s in q.shape)
+    if out is None:
+        out = torch.empty_like(q)
+    if lse is None and want_lse:
+        lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
+    sc = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    cdesc = cc.descriptor()
+    st = lib().omnimem_cmp_attn(ctypes.byref(cdesc), int(n_chunks), _ptr(q), lq, sc, _ptr(out), _ptr(lse),
+                                _stream(stream))
+    _check(st, "omnimem_cmp_attn")
+    return out, lse
