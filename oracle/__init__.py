@@ -325,6 +325,25 @@ def cmp_attn(q, kc, vc, scale: float, hs=None, qs=None):
     return dense_attn(q, k1, v1, N, 0, 1, scale, hs=hs, qs=qs)
 
 
+def gated_combine(o_cmp, o_slc, o_swa, gate_logits):
+    """Eq. 1's fusion of the three branches: o = sum over c in (CMP, SLC, SWA) of
+    g^c * Attn_c, each coefficient g^c in [0, 1] a sigmoid of its gate logit (App. B:
+    learned per-branch sigmoid gates).  o_*: [Lq, H, d] or None (an absent branch
+    contributes nothing); gate_logits: [Lq, H, 3] in the order CMP, SLC, SWA.
+    float64 throughout."""
+    gl = np.asarray(gate_logits, dtype=np.float64)
+    out = None
+    for c, o in enumerate((o_cmp, o_slc, o_swa)):
+        if o is None:
+            continue
+        g = 1.0 / (1.0 + np.exp(-gl[..., c]))
+        term = g[..., None] * np.asarray(o, dtype=np.float64)
+        out = term if out is None else out + term
+    if out is None:
+        raise ValueError("no branch given")
+    return out
+
+
 def union(idx, cnt, n_blocks: int):
     """Eq. 4 unions: returns (per-head |U_h| [H], cross-head |U|)."""
     idx_a, idx_p = _i32(idx)

@@ -325,6 +325,27 @@ def pin_bf16_rounding():
     assert np.array_equal(O.round_bf16(x), lib)
 
 
+def pin_gated_combine():
+    # Eq. 1 with sigmoid gates: a saturated gate keeps or drops a branch exactly,
+    # a zero logit weighs a branch by 1/2, and sigmoid(x) + sigmoid(-x) = 1.
+    rng = np.random.default_rng(64)
+    a, b, c = (rng.standard_normal((5, 2, 4)) for _ in range(3))
+    big = np.full((5, 2, 3), -800.0)
+    only = big.copy()
+    only[..., 1] = 800.0                                       # SLC alone
+    assert np.array_equal(O.gated_combine(a, b, c, only), b)
+    half = np.zeros((5, 2, 3))
+    assert np.allclose(O.gated_combine(a, b, c, half), (a + b + c) / 2, atol=1e-15)
+    x = rng.standard_normal((5, 2))
+    sym = np.stack([x, -x, np.full_like(x, -800.0)], axis=-1)
+    assert np.allclose(O.gated_combine(a, a, c, sym), a, atol=1e-15)
+    # a missing branch contributes nothing
+    assert np.allclose(O.gated_combine(None, b, c, only), b, atol=0)
+    g = rng.standard_normal((5, 2, 3))
+    assert np.allclose(O.gated_combine(a, b, None, g) + O.gated_combine(None, None, c, g),
+                       O.gated_combine(a, b, c, g), atol=1e-14)
+
+
 def pin_attention_special_cases():
     rng = np.random.default_rng(31)
     n, S, H, d = 2, 6, 1, 4
