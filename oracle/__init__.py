@@ -336,7 +336,8 @@ def gated_combine(o_cmp, o_slc, o_swa, gate_logits):
     for c, o in enumerate((o_cmp, o_slc, o_swa)):
         if o is None:
             continue
-        g = 1.0 / (1.0 + np.exp(-gl[..., c]))
+        z = np.exp(-np.abs(gl[..., c]))                  # sigmoid without overflow
+        g = np.where(gl[..., c] >= 0, 1.0 / (1.0 + z), z / (1.0 + z))
         term = g[..., None] * np.asarray(o, dtype=np.float64)
         out = term if out is None else out + term
     if out is None:
