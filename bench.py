@@ -332,9 +332,9 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
     import numpy as np
     import torch
 
-    from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk,
-                                      omnimem_select_compressed, omnimem_select_workspace_bytes,
-                                      omnimem_sparse_attn, select_params)
+    from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk, omnimem_dense_attn,
+                                      omnimem_gated_combine, omnimem_select_compressed,
+                                      omnimem_select_workspace_bytes, omnimem_sparse_attn, select_params)
     from paper_2605_30519_amd.omnimem import workspace_tensor
     n, K = w.history_chunks, w.top_k
     ccs = [CompressedCache.allocate(cache, n) for _, cache in layers]
@@ -389,12 +389,58 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
     torch.cuda.synchronize()
     cmp_ms = e[0].elapsed_time(e[1]) / 20
     cmp_fl = 4.0 * w.head_dim * w.heads * w.query_tokens * n * w.blocks_per_chunk
+
+    # Eq. 1 in full: the selection step above, then CMP and SWA (the window's chunks)
+    # and the sigmoid-gated sum of the three branches (synthetic gate logits)
+    o_cmp = [torch.empty_like(o) for o in outs]
+    o_swa = [torch.empty_like(o) for o in outs]
+    gates = torch.randn((w.query_tokens, w.heads, 3), generator=torch.Generator(device=dev).manual_seed(7),
+                        device=dev)
+    fused = [torch.empty_like(o) for o in outs]
+
+    def three_branch(i, ev=None):
+        j = i % len(layers)
+        q, cache = layers[j]
+        if ev is not None:
+            ev[0].record()
+        step(i)
+        if ev is not None:
+            ev[1].record()
+        omnimem_cmp_attn(ccs[j], n, q, w.scale, out=o_cmp[j], want_lse=False)
+        if ev is not None:
+            ev[2].record()
+        omnimem_dense_attn(cache, q, n - w.window_chunks, n, w.scale, out=o_swa[j], want_lse=False)
+        if ev is not None:
+            ev[3].record()
+        omnimem_gated_combine(o_cmp[j], outs[j], o_swa[j], gates, out=fused[j])
+        if ev is not None:
+            ev[4].record()
+
+    for i in range(200):
+        three_branch(i)
+    torch.cuda.synchronize()
+    reps = 100
+    evs3 = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(reps)]
+    t0.record()
+    for i in range(reps):
+        three_branch(i)
+    t1.record()
+    torch.cuda.synchronize()
+    tb_ms = t0.elapsed_time(t1) / reps
+    for i in range(reps):
+        three_branch(i, evs3[i])
+    torch.cuda.synchronize()
+    med3 = lambda a, b: float(np.median([e[a].elapsed_time(e[b]) for e in evs3]))
     return {"step": "pool the newest chunk + select from the pooled keys + sparse attention",
             "ms_per_chunk_layer": round(ms, 4),
             "effective_tflops": round(float(np.mean(flops)) / (ms * 1e-3) / 1e12, 2),
             "compress_chunk_ms": round(med(0, 1), 4), "select_compressed_ms": round(med(1, 2), 4),
             "sparse_attn_ms": round(med(2, 3), 4),
-            "cmp_attn_ms": round(cmp_ms, 4), "cmp_attn_tflops": round(cmp_fl / (cmp_ms * 1e-3) / 1e12, 2)}
+            "cmp_attn_ms": round(cmp_ms, 4), "cmp_attn_tflops": round(cmp_fl / (cmp_ms * 1e-3) / 1e12, 2),
+            "three_branch": {"step": "the compressed chunk step + CMP + SWA over the window + gated fusion (Eq. 1)",
+                             "ms_per_chunk_layer": round(tb_ms, 4), "selection_step_ms": round(med3(0, 1), 4),
+                             "cmp_attn_ms": round(med3(1, 2), 4), "swa_attn_ms": round(med3(2, 3), 4),
+                             "gated_combine_ms": round(med3(3, 4), 4)}}
 
 
 def ramp_measure(dev, layers_n=30, warm_passes=20):

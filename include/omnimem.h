@@ -263,6 +263,22 @@ omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const o
 omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int32_t n_chunks, const void* q, int32_t lq,
                                   float scale, void* out, float* lse, void* stream);
 
+/*
+ * Eq. 1's fusion of the three branches (Sec. 3.1): for every query row i and head h
+ *   out[i][h] = sum over c in (CMP, SLC, SWA) of g^c[i][h] * o_c[i][h],
+ *   g^c[i][h] = 1 / (1 + exp(-gate_logits[i][h][c]))  in [0, 1]
+ * (App. B: learned per-branch sigmoid gates; the logits are the caller's).
+ * o_cmp, o_slc, o_swa: [lq][num_heads][head_dim] of dtype (omnimem_cmp_attn,
+ * omnimem_sparse_attn and omnimem_dense_attn over the window give them); a NULL
+ * branch is absent and contributes nothing (at least one must be given).
+ * gate_logits: [lq][num_heads][3] float, branch order CMP, SLC, SWA.
+ * out: [lq][num_heads][head_dim] of dtype; it may be one of the branch buffers.
+ * Arithmetic in fp32, the result rounded to dtype (bf16: nearest even).
+ */
+omnimem_status_t omnimem_gated_combine(int32_t dtype, int32_t lq, int32_t num_heads, int32_t head_dim,
+                                       const void* o_cmp, const void* o_slc, const void* o_swa,
+                                       const float* gate_logits, void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

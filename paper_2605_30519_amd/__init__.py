@@ -18,6 +18,7 @@ from .omnimem import (  # noqa: F401
     omnimem_cmp_attn,
     omnimem_compress_chunk,
     omnimem_dense_attn,
+    omnimem_gated_combine,
     omnimem_select,
     omnimem_select_compressed,
     omnimem_select_workspace_bytes,

@@ -281,6 +281,23 @@ OMNIMEM_API omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int
   return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
 }
 
+OMNIMEM_API omnimem_status_t omnimem_gated_combine(int32_t dtype, int32_t lq, int32_t num_heads, int32_t head_dim,
+                                                   const void* o_cmp, const void* o_slc, const void* o_swa,
+                                                   const float* gate_logits, void* out, void* stream) {
+  if (dtype != OMNIMEM_BF16 && dtype != OMNIMEM_F32) return OMNIMEM_EUNSUPPORTED;
+  if (head_dim != 64 && head_dim != 128) return OMNIMEM_EUNSUPPORTED;
+  if (lq < 0 || num_heads < 1) return OMNIMEM_EINVAL;
+  if (lq == 0) return OMNIMEM_OK;
+  if (out == nullptr || gate_logits == nullptr || (o_cmp == nullptr && o_slc == nullptr && o_swa == nullptr))
+    return OMNIMEM_EINVAL;
+  if (!aligned16(out) || !aligned16(o_cmp) || !aligned16(o_slc) || !aligned16(o_swa) ||
+      (reinterpret_cast<uintptr_t>(gate_logits) & 3u))
+    return OMNIMEM_EINVAL;
+  const int64_t rows = static_cast<int64_t>(lq) * num_heads;
+  return hip_status(omnimem::launch_gated_combine(dtype == OMNIMEM_BF16 ? 0 : 1, rows, head_dim, o_cmp, o_slc, o_swa,
+                                                  gate_logits, out, static_cast<hipStream_t>(stream)));
+}
+
 OMNIMEM_API size_t omnimem_union_workspace_bytes(const omnimem_kv_cache_t* kv) {
   CacheGeom g;
   if (resolve_cache(kv, g) != OMNIMEM_OK) return 0;

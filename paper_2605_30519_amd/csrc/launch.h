@@ -75,6 +75,12 @@ struct AttnLaunch {
 
 hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& a, hipStream_t stream);
 
+// ---------------------------------------------------------------- gated fusion (Eq. 1)
+// out = sum_c sigmoid(gate[row][c]) * o_c over the present branches (null = absent);
+// rows = lq * H rows of D elements, dtype 0 = bf16, 1 = f32.
+hipError_t launch_gated_combine(int dtype, int64_t rows, int D, const void* o_cmp, const void* o_slc,
+                                const void* o_swa, const float* gate, void* out, hipStream_t stream);
+
 // ---------------------------------------------------------------- union gather
 struct UnionPlan {
   size_t off_flags, off_pos, off_table, off_kbuf, off_vbuf, total;

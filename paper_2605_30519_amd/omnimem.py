@@ -4,8 +4,8 @@ include/omnimem.h.  PyTorch supplies device memory and the current stream.
 
 The functions carry the C names: omnimem_select, omnimem_sparse_attn,
 omnimem_dense_attn, omnimem_union_gather_attn, the compressed-history calls
-omnimem_compress_chunk, omnimem_select_compressed and omnimem_cmp_attn, plus the
-host-side helpers.
+omnimem_compress_chunk, omnimem_select_compressed and omnimem_cmp_attn, Eq. 1's
+gated fusion omnimem_gated_combine, plus the host-side helpers.
 """
 from __future__ import annotations
 
@@ -87,6 +87,7 @@ EXPORTED = [
     "omnimem_compress_chunk",
     "omnimem_select_compressed",
     "omnimem_cmp_attn",
+    "omnimem_gated_combine",
 ]
 
 
@@ -119,6 +120,8 @@ def _configure(L):
     L.omnimem_select_compressed.restype = i32
     L.omnimem_cmp_attn.argtypes = [ccp, i32, vp, i32, f32, vp, vp, vp]
     L.omnimem_cmp_attn.restype = i32
+    L.omnimem_gated_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
+    L.omnimem_gated_combine.restype = i32
     return L
 
 
@@ -423,3 +426,23 @@ def omnimem_cmp_attn(cc: CompressedCache, n_chunks: int, q: torch.Tensor, scale:
                                 _stream(stream))
     _check(st, "omnimem_cmp_attn")
     return out, lse
+
+
+def omnimem_gated_combine(o_cmp: Optional[torch.Tensor], o_slc: Optional[torch.Tensor],
+                          o_swa: Optional[torch.Tensor], gate_logits: torch.Tensor, *,
+                          out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """Eq. 1: out = sum_c sigmoid(gate_logits[..., c]) * o_c over the given branches
+    (CMP, SLC, SWA); gate_logits [lq, H, 3] float32."""
+    ref = next(o for o in (o_cmp, o_slc, o_swa) if o is not None)
+    lq, H, d = (int(s) for s in ref.shape)
+    for o in (o_cmp, o_slc, o_swa):
+        if o is not None and (o.shape != ref.shape or o.dtype != ref.dtype or not o.is_contiguous()):
+            raise ValueError("branch outputs must share shape, dtype and be contiguous")
+    if gate_logits.dtype != torch.float32 or tuple(gate_logits.shape) != (lq, H, 3) or not gate_logits.is_contiguous():
+        raise ValueError("gate_logits must be a contiguous float32 [lq, H, 3] tensor")
+    if out is None:
+        out = torch.empty_like(ref)
+    st = lib().omnimem_gated_combine(_DTYPES[ref.dtype], lq, H, d, _ptr(o_cmp), _ptr(o_slc), _ptr(o_swa),
+                                     _ptr(gate_logits), _ptr(out), _stream(stream))
+    _check(st, "omnimem_gated_combine")
+    return out

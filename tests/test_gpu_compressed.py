@@ -1,8 +1,9 @@
-"""Parity of the compressed-history path (App. C's first cache level) with the
-fp64 oracle, through the C ABI: chunks pooled one by one as they are appended
-(omnimem_compress_chunk), selection from the pooled keys
-(omnimem_select_compressed) at every history length, and compression attention
-over the pooled sequence (omnimem_cmp_attn, Eq. 1's CMP branch).
+"""Parity of the compressed-history path (App. C's first cache level) and of Eq. 1's
+gated three-branch fusion with the fp64 oracle, through the C ABI: chunks pooled
+one by one as they are appended (omnimem_compress_chunk), selection from the
+pooled keys (omnimem_select_compressed) at every history length, compression
+attention over the pooled sequence (omnimem_cmp_attn, Eq. 1's CMP branch), and
+the sigmoid-gated sum of the CMP, SLC and SWA branches (omnimem_gated_combine).
 
 The oracle pools the same logical K/V in fp64 (oracle.cmp_cache) and rounds the
 pooled tokens to bf16 for a bf16 cache, as the stored pooled sequence is.  A block
@@ -13,9 +14,10 @@ import pytest
 import torch
 
 import oracle
-from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk, omnimem_select,
-                                  omnimem_select_compressed, synth)
-from parity import check_selection, say
+from paper_2605_30519_amd import (CompressedCache, omnimem_cmp_attn, omnimem_compress_chunk, omnimem_dense_attn,
+                                  omnimem_gated_combine, omnimem_select, omnimem_select_compressed,
+                                  omnimem_sparse_attn, synth)
+from parity import check_bf16, check_f32, check_selection, say
 from test_gpu_parity import attn_check, host, oracle_select, sample_rows
 
 pytestmark = pytest.mark.gpu
@@ -162,3 +164,78 @@ def test_compressed_wan13b_n20(dev):
     hs, qs = sample_rows(w.heads, w.query_tokens, 96, 5)
     o_ref, l_ref, _, _ = oracle.cmp_attn(host(x.q), kc, vc, w.scale, hs=hs, qs=qs)
     attn_check(out, lse, o_ref, l_ref, hs, qs, w.dtype, "cmp wan1.3b_n20")
+
+
+# ------------------------------------------------ Eq. 1: the three branches fused
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_gated_combine_kernel(dev, dtype):
+    """The fusion kernel alone, on seeded branch outputs and gate logits (saturated,
+    zero and random), against the oracle's fusion of the same values."""
+    say(f"gated combine kernel {dtype}")
+    lq, H, d = 301, 3, 128
+    g = torch.Generator(device=dev).manual_seed(81)
+    outs = [torch.randn((lq, H, d), generator=g, device=dev).to(dtype) for _ in range(3)]
+    logits = 4 * torch.randn((lq, H, 3), generator=g, device=dev)
+    logits[:50] = 0.0
+    logits[50:60, :, 0] = 1e4
+    logits[60:70, :, 1] = -1e4
+    host_outs = [host(o).float().numpy().astype(np.float64) for o in outs]
+    for drop in (None, 0, 2):
+        args = [None if c == drop else outs[c] for c in range(3)]
+        got = omnimem_gated_combine(*args, logits)
+        torch.cuda.synchronize()
+        want = oracle.gated_combine(*[None if c == drop else host_outs[c] for c in range(3)], host(logits).numpy())
+        gotf = host(got).float().numpy()
+        # fp32 evaluation: a few fp32 ulps of the sum of |terms| (cancellation can
+        # leave a tiny sum of O(1) terms), then one rounding to the output dtype
+        absum = oracle.gated_combine(*[None if c == drop else np.abs(host_outs[c]) for c in range(3)],
+                                     host(logits).numpy())
+        fp32_err = 8 * 2.0 ** -24 * absum
+        if dtype == torch.float32:
+            assert (np.abs(gotf - want) <= fp32_err + 2.0 ** -24 * np.abs(want)).all(), np.abs(gotf - want).max()
+        else:  # within one bf16 step of the fp64 value, plus the fp32 evaluation error
+            step = np.ldexp(1.0, np.frexp(np.maximum(np.abs(want), 1e-30))[1] - 8)
+            assert (np.abs(gotf - want) <= step + fp32_err).all(), np.abs(gotf - want).max()
+    # in place: out is one of the branches
+    b = outs[1].clone()
+    omnimem_gated_combine(outs[0], b, outs[2], logits, out=b)
+    ref = omnimem_gated_combine(outs[0], outs[1], outs[2], logits)
+    torch.cuda.synchronize()
+    assert torch.equal(b, ref)
+
+
+@pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
+def test_three_branch_forward(dev, dtype):
+    """Eq. 1 end to end: CMP over the compressed history, SLC over the selected
+    blocks, SWA over the window chunks, fused with sigmoid gates; against the oracle's
+    three branches and fusion computed from the same inputs."""
+    H, d, S, Lq, B, n, K, G, E, T = 2, 128, 300, 257, 64, 6, 5, 100, 1, 2
+    say(f"three-branch forward {dtype}")
+    w = synth.Workload("three", H, d, S, Lq, B, n, n, K, G, E, T, dtype, dtype == torch.bfloat16, 1, 9)
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, B, seed=4, pad_value=NAN)
+    cc = CompressedCache.allocate(cache, n)
+    for c in range(n):
+        omnimem_compress_chunk(cache, c, cc)
+    sel = omnimem_select_compressed(cache, cc, x.q, K, G, E, T, w.scale)
+    o_cmp, _ = omnimem_cmp_attn(cc, n, x.q, w.scale)
+    o_slc, _ = omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, G, w.scale)
+    o_swa, _ = omnimem_dense_attn(cache, x.q, n - E, n, w.scale)
+    logits = torch.randn((Lq, H, 3), generator=torch.Generator(device=dev).manual_seed(82), device=dev)
+    out = omnimem_gated_combine(o_cmp, o_slc, o_swa, logits)
+    torch.cuda.synchronize()
+    ref = oracle_select(x, w, n)
+    check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref)
+    kbar, kc, vc = oracle_pooled(x, w, n)
+    r_cmp, _, hs, qs = oracle.cmp_attn(host(x.q), kc, vc, w.scale)
+    r_slc, _, _, _ = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), B, ref["idx"], ref["cnt"], G, w.scale)
+    r_swa, _, _, _ = oracle.dense_attn(host(x.q), host(x.k), host(x.v), B, n - E, n, w.scale)
+    shape = (H, Lq, d)   # oracle rows come head-major: (h, q) pairs in order
+    fused = oracle.gated_combine(*(r.reshape(shape).transpose(1, 0, 2) for r in (r_cmp, r_slc, r_swa)),
+                                 host(logits).numpy())
+    got = host(out).float().numpy()
+    if dtype == torch.float32:
+        check_f32(got, fused, "three-branch fused")
+    else:
+        check_bf16(got, fused, "three-branch fused")
