@@ -53,6 +53,7 @@ def parse():
     p.add_argument("--stress", action="store_true", help="add the 14B-shaped union-gather comparison")
     p.add_argument("--no-ramp", action="store_true", help="skip the 30-layer, 1 -> 60 chunk ramp")
     p.add_argument("--no-compressed", action="store_true", help="skip the compressed-history path")
+    p.add_argument("--no-lru", action="store_true", help="skip the LRU hot-cache measurement")
     p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
     return p.parse_args()
 
@@ -226,6 +227,11 @@ def main():
     if not args.no_compressed:
         log("compressed-history path (pool the newest chunk + select from pooled keys + sparse attention)")
         result["compressed"] = compressed_measure(dev, layers, sels, outs, lses, w, args)
+
+    # ---------------------------------------------------------------- LRU hot cache
+    if not args.no_lru:
+        log("LRU hot cache: reload bandwidth and LRU size vs a drifting working set")
+        result["lru"] = lru_measure(dev, x0, w)
 
     # ---------------------------------------------------------------- sweep
     if not args.no_sweep:
@@ -441,6 +447,85 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
                              "ms_per_chunk_layer": round(tb_ms, 4), "selection_step_ms": round(med3(0, 1), 4),
                              "cmp_attn_ms": round(med3(1, 2), 4), "swa_attn_ms": round(med3(2, 3), 4),
                              "gated_combine_ms": round(med3(3, 4), 4)}}
+
+
+def lru_measure(dev, x, w, steps=60, working=4, sizes=(4, 5, 7, 10), seed=17):
+    """The GPU hot cache of App. B / App. F on the bench layer (20 chunks in pinned
+    host pools).  Access pattern (synthetic, with the locality the paper reports):
+    each step reads a working set of `working` chunks -- three anchors that change
+    every 15 steps plus one chunk drawn at random -- and each head's 64 blocks are
+    drawn from the working set's blocks.  Per LRU size: require + selection attention
+    per step (HIP events around the step, PCIe copies included), hit rate, and the
+    GPU pool's bytes."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import LruOffload, PagedKVCache, omnimem_sparse_attn
+    n, S, H, d = (int(s) for s in x.k.shape)
+    B, K, Bpc = w.block_size, w.top_k, w.blocks_per_chunk
+    pools = []
+    for t in (x.k, x.v):
+        pad = Bpc * B - S
+        y = torch.cat([t, torch.zeros((n, pad, H, d), dtype=t.dtype, device=t.device)], dim=1) if pad else t
+        pinned = torch.empty((n * Bpc, H, B, d), dtype=t.dtype, pin_memory=True)
+        pinned.copy_(y.reshape(n * Bpc, B, H, d).permute(0, 2, 1, 3).cpu())
+        pools.append(pinned)
+        del y
+    rng = np.random.default_rng(seed)
+    plan = []
+    anchors = []
+    for step in range(steps):
+        if step % 15 == 0:
+            anchors = rng.choice(n, working - 1, replace=False).tolist()
+        extra = int(rng.choice([c for c in range(n) if c not in anchors]))
+        ws = anchors + [extra]
+        blocks = np.array([c * Bpc + o for c in ws for o in range(Bpc)])
+        idx = np.stack([np.sort(rng.choice(blocks, K, replace=False)) for _ in range(H)])[:, None, :]
+        plan.append((ws, torch.tensor(idx, dtype=torch.int32, device=dev)))
+    cnt = torch.full((H, 1), K, dtype=torch.int32, device=dev)
+    out = torch.empty_like(x.q)
+    lse = torch.empty((H, w.query_tokens), dtype=torch.float32, device=dev)
+    page_bytes = H * B * d * x.k.element_size()
+    res = {"workload": f"bench layer, {n} chunks in pinned host pools; {steps} steps, working set of {working} "
+                       f"chunks (3 anchors changing every 15 steps + 1 random), {K} blocks per head drawn from it",
+           "sizes": []}
+    # raw reload rate: the whole history, slot by slot
+    big = PagedKVCache(torch.empty((n * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                       torch.empty((n * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                       torch.zeros((n, Bpc), dtype=torch.int32, device=dev), S)
+    lru = LruOffload(big, n, pools[0], pools[1])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    lru.require(list(range(n)))
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    res["reload_gbs"] = round(2 * n * Bpc * page_bytes / (ms * 1e-3) / 1e9, 1)
+    res["reload_ms_per_chunk"] = round(ms / n, 3)
+    lru.close()
+    del big
+    for slots in sizes:
+        gpu = PagedKVCache(torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                           torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                           torch.zeros((n, Bpc), dtype=torch.int32, device=dev), S)
+        lru = LruOffload(gpu, slots, pools[0], pools[1])
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+        for step, (ws, idx) in enumerate(plan):
+            evs[step][0].record()
+            lru.require(ws)
+            omnimem_sparse_attn(gpu, x.q, idx, cnt, w.group_size, w.scale, out=out, lse=lse)
+            evs[step][1].record()
+        torch.cuda.synchronize()
+        st = lru.stats()
+        t = [e[0].elapsed_time(e[1]) for e in evs]
+        res["sizes"].append({"lru_chunks": slots, "hit_rate": round(st["hits"] / max(1, st["hits"] + st["misses"]), 4),
+                             "reloaded_chunks": st["misses"], "ms_per_step": round(float(np.mean(t)), 4),
+                             "ms_per_step_median": round(float(np.median(t)), 4),
+                             "gpu_pool_gb": round(2 * slots * Bpc * page_bytes / 1e9, 3)})
+        lru.close()
+        del gpu
+    return res
 
 
 def ramp_measure(dev, layers_n=30, warm_passes=20):

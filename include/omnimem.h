@@ -120,7 +120,8 @@ int32_t omnimem_blocks_per_chunk(int32_t chunk_tokens, int32_t block_size);
 int32_t omnimem_awe_active(int32_t num_chunks, int32_t window_chunks, int32_t awe_min_outside_chunks, int32_t top_k,
                            int32_t blocks_per_chunk);
 
-/* Bytes of device workspace omnimem_select needs (0 on invalid arguments). */
+/* Bytes of device workspace omnimem_select (and omnimem_select_compressed) needs
+   (0 on invalid arguments); kv->page_table may be NULL here. */
 size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq, const omnimem_select_params_t* p);
 
 /*
@@ -243,7 +244,9 @@ omnimem_status_t omnimem_compress_chunk(const omnimem_kv_cache_t* kv, int32_t ch
  * outputs, with the pooled keys read from cc->k_mean (chunks [0, kv->num_chunks)
  * must have been pooled; kv->num_chunks <= capacity_chunks) instead of pooled from
  * the full cache's pages.  kv still supplies the geometry, the history length and
- * residency (a block whose page is not resident is not a candidate).  The workspace
+ * residency (a block whose page is not resident is not a candidate); with
+ * kv->page_table == NULL every block is a candidate, residency being handled by
+ * the caller (omnimem_lru_require before the selection attention).  The workspace
  * is sized by omnimem_select_workspace_bytes(kv, lq, p).
  */
 omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const omnimem_cmp_cache_t* cc,
@@ -278,6 +281,55 @@ omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int32_t n_chunk
 omnimem_status_t omnimem_gated_combine(int32_t dtype, int32_t lq, int32_t num_heads, int32_t head_dim,
                                        const void* o_cmp, const void* o_slc, const void* o_swa,
                                        const float* gate_logits, void* out, void* stream);
+
+/*
+ * GPU hot cache of full-resolution history chunks with LRU eviction (App. B,
+ * "Inference and Offloading": the GPU keeps a few chunks, the rest sit in pinned
+ * host memory and are reloaded over PCIe when selected; App. F studies its size;
+ * Alg. 1's WaitUntilReload).  Host-side runtime state for one layer.
+ *
+ * The caller allocates and owns every buffer:
+ *   kv->k_pages, kv->v_pages  the GPU page pool: slot t holds a chunk in pages
+ *                             [t*Bpc, (t+1)*Bpc); kv->num_pages >= slots*Bpc;
+ *   kv->page_table            [kv->num_chunks][Bpc] on the device, written by this
+ *                             runtime only: a chunk's row holds its slot's pages while
+ *                             it is resident and -1 (not resident) otherwise;
+ *   k_host, v_host            pinned host pools (hipHostMalloc) holding every chunk:
+ *                             chunk c in pages [c*Bpc, (c+1)*Bpc), the page layout of
+ *                             kv ([page][H][B][d]); host_chunks chunks.
+ * The residency unit is a chunk of all heads (a page holds every head's copy of a
+ * block).  The object keeps host bookkeeping only (no device or pinned memory of its
+ * own); it is not thread-safe.  Selection over the compressed history
+ * (omnimem_select_compressed with kv->page_table == NULL) needs no chunk resident.
+ */
+typedef struct omnimem_lru omnimem_lru_t;
+
+typedef struct {
+  int64_t hits, misses, evictions; /* chunks found resident / reloaded / evicted */
+  int64_t bytes_reloaded;          /* host-to-device bytes (K and V) */
+} omnimem_lru_stats_t;
+
+/* Creates the state (*out, released by omnimem_lru_destroy) and enqueues on
+   `stream` the write of -1 to every page-table row.  slots >= 1 (G_LRU). */
+omnimem_status_t omnimem_lru_create(const omnimem_kv_cache_t* kv, int32_t slots, const void* k_host,
+                                    const void* v_host, int32_t host_chunks, void* stream, omnimem_lru_t** out);
+void omnimem_lru_destroy(omnimem_lru_t* lru);
+
+/* Makes every chunk in chunks[0:count] (host array; repeats allowed) resident
+   before whatever follows on `stream`: resident chunks count as hits and become
+   most recently used; each other chunk evicts the least recently used chunk not in
+   the request (its row becomes -1), is copied host-to-device into the freed slot
+   (hipMemcpyAsync on `stream`) and gets its row.  The distinct chunks of a request
+   must fit in the slots (else OMNIMEM_EINVAL, nothing changed).  *reloaded (host,
+   may be NULL) receives the number of chunks copied. */
+omnimem_status_t omnimem_lru_require(omnimem_lru_t* lru, const int32_t* chunks, int32_t count, int32_t* reloaded,
+                                     void* stream);
+
+/* Counters since creation (host). */
+omnimem_status_t omnimem_lru_stats(const omnimem_lru_t* lru, omnimem_lru_stats_t* out);
+
+/* The slot holding `chunk`, or -1 when it is not resident (host). */
+int32_t omnimem_lru_slot_of(const omnimem_lru_t* lru, int32_t chunk);
 
 #ifdef __cplusplus
 }

@@ -8,6 +8,7 @@ library is opened on the first call.
 from .omnimem import (  # noqa: F401
     EXPORTED,
     CompressedCache,
+    LruOffload,
     OmniMemError,
     PagedKVCache,
     Selection,
@@ -27,4 +28,5 @@ from .omnimem import (  # noqa: F401
     omnimem_union_gather_attn,
     omnimem_union_workspace_bytes,
     select_params,
+    selected_chunks,
 )

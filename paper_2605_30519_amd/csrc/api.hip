@@ -16,7 +16,8 @@ using omnimem::CacheGeom;
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Resolves and validates a cache descriptor.  Returns OMNIMEM_OK or an error.
-omnimem_status_t resolve_cache(const omnimem_kv_cache_t* kv, CacheGeom& g) {
+// table_optional: a NULL page table is accepted (selection from pooled keys only).
+omnimem_status_t resolve_cache(const omnimem_kv_cache_t* kv, CacheGeom& g, bool table_optional = false) {
   if (kv == nullptr) return OMNIMEM_EINVAL;
   if (kv->dtype != OMNIMEM_BF16 && kv->dtype != OMNIMEM_F32) return OMNIMEM_EUNSUPPORTED;
   if (kv->num_heads < 1 || kv->chunk_tokens < 1 || kv->num_chunks < 0 || kv->num_pages < 0) return OMNIMEM_EINVAL;
@@ -39,7 +40,7 @@ omnimem_status_t resolve_cache(const omnimem_kv_cache_t* kv, CacheGeom& g) {
   g.v_pages = kv->v_pages;
   g.page_table = kv->page_table;
   if (g.nb > 0) {
-    if (g.page_table == nullptr) return OMNIMEM_EINVAL;
+    if (g.page_table == nullptr && !table_optional) return OMNIMEM_EINVAL;
     if (g.num_pages > 0 && (g.k_pages == nullptr || g.v_pages == nullptr)) return OMNIMEM_EINVAL;
     if (!aligned16(g.k_pages) || !aligned16(g.v_pages) || (reinterpret_cast<uintptr_t>(g.page_table) & 3u))
       return OMNIMEM_EINVAL;
@@ -75,8 +76,8 @@ OMNIMEM_API int32_t omnimem_awe_active(int32_t n, int32_t E, int32_t T_out, int3
 namespace {
 
 omnimem_status_t resolve_select(const omnimem_kv_cache_t* kv, int32_t lq, const omnimem_select_params_t* p,
-                                CacheGeom& g, omnimem::SelectPlan& plan) {
-  omnimem_status_t st = resolve_cache(kv, g);
+                                CacheGeom& g, omnimem::SelectPlan& plan, bool table_optional = false) {
+  omnimem_status_t st = resolve_cache(kv, g, table_optional);
   if (st != OMNIMEM_OK) return st;
   if (p == nullptr || lq < 0) return OMNIMEM_EINVAL;
   if (p->top_k < 1 || p->group_size < 1 || p->window_chunks < 0 || p->awe_min_outside_chunks < 0 ||
@@ -99,7 +100,8 @@ OMNIMEM_API size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, 
                                                   const omnimem_select_params_t* p) {
   CacheGeom g;
   omnimem::SelectPlan plan;
-  if (resolve_select(kv, lq, p, g, plan) != OMNIMEM_OK) return 0;
+  // the size does not depend on the page table (NULL for omnimem_select_compressed)
+  if (resolve_select(kv, lq, p, g, plan, /*table_optional=*/true) != OMNIMEM_OK) return 0;
   return lq == 0 ? 256 : plan.total;
 }
 
@@ -218,7 +220,7 @@ OMNIMEM_API omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t*
                                                        void* workspace, size_t workspace_bytes, void* stream) {
   CacheGeom g;
   omnimem::SelectPlan plan;
-  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
+  omnimem_status_t st = resolve_select(kv, lq, p, g, plan, /*table_optional=*/true);
   if (st != OMNIMEM_OK) return st;
   omnimem::CmpCache c;
   st = resolve_cmp(cc, g, c);

@@ -302,8 +302,9 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
     if (b >= nb || r >= R) continue;
     float dot = 0.f;
     for (int j = 0; j < D; ++j) dot += qs[rr][j] * ks[bb][j];
-    const int32_t p = page_table[b];
-    const bool live = b < first_excluded && p >= 0 && p < num_pages;
+    // no page table: every block is a candidate (residency is managed elsewhere)
+    const int32_t p = page_table != nullptr ? page_table[b] : 0;
+    const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
     keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * dot) : 0u;
   }
 }

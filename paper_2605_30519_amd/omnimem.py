@@ -58,6 +58,15 @@ class omnimem_select_params_t(ctypes.Structure):
     ]
 
 
+class omnimem_lru_stats_t(ctypes.Structure):
+    _fields_ = [
+        ("hits", ctypes.c_int64),
+        ("misses", ctypes.c_int64),
+        ("evictions", ctypes.c_int64),
+        ("bytes_reloaded", ctypes.c_int64),
+    ]
+
+
 class omnimem_cmp_cache_t(ctypes.Structure):
     _fields_ = [
         ("dtype", ctypes.c_int32),
@@ -88,6 +97,11 @@ EXPORTED = [
     "omnimem_select_compressed",
     "omnimem_cmp_attn",
     "omnimem_gated_combine",
+    "omnimem_lru_create",
+    "omnimem_lru_destroy",
+    "omnimem_lru_require",
+    "omnimem_lru_stats",
+    "omnimem_lru_slot_of",
 ]
 
 
@@ -122,6 +136,16 @@ def _configure(L):
     L.omnimem_cmp_attn.restype = i32
     L.omnimem_gated_combine.argtypes = [i32, i32, i32, i32, vp, vp, vp, vp, vp, vp]
     L.omnimem_gated_combine.restype = i32
+    L.omnimem_lru_create.argtypes = [kvp, i32, vp, vp, i32, vp, ctypes.POINTER(vp)]
+    L.omnimem_lru_create.restype = i32
+    L.omnimem_lru_destroy.argtypes = [vp]
+    L.omnimem_lru_destroy.restype = None
+    L.omnimem_lru_require.argtypes = [vp, ctypes.POINTER(i32), i32, ctypes.POINTER(i32), vp]
+    L.omnimem_lru_require.restype = i32
+    L.omnimem_lru_stats.argtypes = [vp, ctypes.POINTER(omnimem_lru_stats_t)]
+    L.omnimem_lru_stats.restype = i32
+    L.omnimem_lru_slot_of.argtypes = [vp, i32]
+    L.omnimem_lru_slot_of.restype = i32
     return L
 
 
@@ -182,8 +206,9 @@ class PagedKVCache:
     def dtype(self) -> torch.dtype:
         return self.k_pages.dtype
 
-    def descriptor(self, num_chunks: Optional[int] = None) -> omnimem_kv_cache_t:
-        """C descriptor; `num_chunks` < n exposes only the oldest chunks (a shorter history)."""
+    def descriptor(self, num_chunks: Optional[int] = None, with_table: bool = True) -> omnimem_kv_cache_t:
+        """C descriptor; `num_chunks` < n exposes only the oldest chunks (a shorter history);
+        with_table=False passes a NULL page table (selection from pooled keys only)."""
         if self.k_pages.dtype not in _DTYPES or self.v_pages.dtype != self.k_pages.dtype:
             raise TypeError(f"unsupported page dtype {self.k_pages.dtype}")
         for t in (self.k_pages, self.v_pages, self.page_table):
@@ -197,7 +222,7 @@ class PagedKVCache:
         return omnimem_kv_cache_t(
             _DTYPES[self.k_pages.dtype], self.num_heads, self.head_dim, self.block_size, self.chunk_tokens, n,
             int(self.k_pages.shape[0]), self.k_pages.data_ptr(), self.v_pages.data_ptr(),
-            self.page_table.data_ptr())
+            self.page_table.data_ptr() if with_table else None)
 
 
 def _stream(stream):
@@ -389,10 +414,12 @@ def omnimem_select_compressed(cache: PagedKVCache, cc: CompressedCache, q: torch
                               window_chunks: int, awe_min_outside_chunks: int, scale: Optional[float] = None, *,
                               num_chunks: Optional[int] = None, want_score: bool = True,
                               workspace: Optional[torch.Tensor] = None, out: Optional[Selection] = None,
-                              stream=None) -> Selection:
+                              all_candidates: bool = False, stream=None) -> Selection:
+    """all_candidates=True ignores residency (NULL page table): every block of the
+    history is a candidate, as when an LRU hot cache reloads what is selected."""
     lq, H, d = (int(s) for s in q.shape)
     params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
-    desc = cache.descriptor(num_chunks)
+    desc = cache.descriptor(num_chunks, with_table=not all_candidates)
     cdesc = cc.descriptor()
     R = -(-lq // group_size)
     dev = q.device
@@ -446,3 +473,61 @@ def omnimem_gated_combine(o_cmp: Optional[torch.Tensor], o_slc: Optional[torch.T
                                      _ptr(gate_logits), _ptr(out), _stream(stream))
     _check(st, "omnimem_gated_combine")
     return out
+
+
+# ------------------------------------------------------------ LRU hot cache
+
+class LruOffload:
+    """GPU hot cache of full-resolution history chunks with LRU eviction (the
+    library's host runtime).  `gpu` is the GPU pool as a PagedKVCache: k_pages /
+    v_pages of slots*Bpc pages, page_table [n, Bpc] (written by the runtime only).
+    k_host / v_host: pinned CPU tensors [host_chunks*Bpc, H, B, d], chunk c in pages
+    [c*Bpc, (c+1)*Bpc)."""
+
+    def __init__(self, gpu: PagedKVCache, slots: int, k_host: torch.Tensor, v_host: torch.Tensor, stream=None):
+        for t in (k_host, v_host):
+            if t.device.type != "cpu" or not t.is_pinned() or not t.is_contiguous() or t.dtype != gpu.dtype:
+                raise ValueError("host pools must be contiguous pinned CPU tensors of the cache dtype")
+            if tuple(t.shape[1:]) != tuple(gpu.k_pages.shape[1:]) or t.shape[0] % gpu.blocks_per_chunk:
+                raise ValueError("host pools must hold whole chunks in the cache's page layout")
+        self.gpu, self.k_host, self.v_host = gpu, k_host, v_host   # kept alive with the state
+        self.slots = int(slots)
+        self.host_chunks = int(k_host.shape[0]) // gpu.blocks_per_chunk
+        desc = gpu.descriptor()
+        h = ctypes.c_void_p()
+        _check(lib().omnimem_lru_create(ctypes.byref(desc), self.slots, k_host.data_ptr(), v_host.data_ptr(),
+                                        self.host_chunks, _stream(stream), ctypes.byref(h)), "omnimem_lru_create")
+        self._h = h
+
+    def require(self, chunks, stream=None) -> int:
+        arr = (ctypes.c_int32 * max(len(chunks), 1))(*[int(c) for c in chunks])
+        got = ctypes.c_int32(0)
+        _check(lib().omnimem_lru_require(self._h, arr, len(chunks), ctypes.byref(got), _stream(stream)),
+               "omnimem_lru_require")
+        return int(got.value)
+
+    def stats(self) -> dict:
+        st = omnimem_lru_stats_t()
+        _check(lib().omnimem_lru_stats(self._h, ctypes.byref(st)), "omnimem_lru_stats")
+        return {"hits": st.hits, "misses": st.misses, "evictions": st.evictions, "bytes_reloaded": st.bytes_reloaded}
+
+    def slot_of(self, chunk: int) -> int:
+        return int(lib().omnimem_lru_slot_of(self._h, int(chunk)))
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            lib().omnimem_lru_destroy(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def selected_chunks(sel: Selection, blocks_per_chunk: int) -> list:
+    """The distinct history chunks a selection reads (host list; synchronises)."""
+    idx = sel.idx.reshape(-1)
+    ids = idx[idx >= 0]
+    return sorted(set((ids // blocks_per_chunk).tolist()))
