@@ -22,8 +22,9 @@
  * Conventions shared by every entry point
  *  - Every buffer pointer is a DEVICE pointer unless marked (host).  The caller
  *    allocates and owns every buffer, including workspaces; the library allocates
- *    no memory and keeps no mutable global state, so calls on different streams
- *    may run concurrently on disjoint outputs.
+ *    no memory (except omnimem_lru_create's host bookkeeping object, released by
+ *    omnimem_lru_destroy) and keeps no mutable global state, so calls on
+ *    different streams may run concurrently on disjoint outputs.
  *  - All work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *    is asynchronous: no entry point synchronises with the host.
  *  - Arguments are validated on the host before anything is enqueued; on failure
