@@ -54,6 +54,7 @@ def parse():
     p.add_argument("--no-ramp", action="store_true", help="skip the 30-layer, 1 -> 60 chunk ramp")
     p.add_argument("--no-compressed", action="store_true", help="skip the compressed-history path")
     p.add_argument("--no-lru", action="store_true", help="skip the LRU hot-cache measurement")
+    p.add_argument("--no-small-group", action="store_true", help="skip the paper's small-group setting")
     p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
     return p.parse_args()
 
@@ -227,6 +228,11 @@ def main():
     if not args.no_compressed:
         log("compressed-history path (pool the newest chunk + select from pooled keys + sparse attention)")
         result["compressed"] = compressed_measure(dev, layers, sels, outs, lses, w, args)
+
+    # ---------------------------------------------------------------- small query groups
+    if not args.no_small_group:
+        log("small query groups (G_q = 15, top-4 per group, 3-chunk window)")
+        result["small_group"] = small_group_measure(dev)
 
     # ---------------------------------------------------------------- LRU hot cache
     if not args.no_lru:
@@ -447,6 +453,48 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
                              "ms_per_chunk_layer": round(tb_ms, 4), "selection_step_ms": round(med3(0, 1), 4),
                              "cmp_attn_ms": round(med3(1, 2), 4), "swa_attn_ms": round(med3(2, 3), 4),
                              "gated_combine_ms": round(med3(3, 4), 4)}}
+
+
+def small_group_measure(dev, reps=50):
+    """The paper's memory-module setting on the Wan2.1-1.3B-shaped layer: query
+    groups of 15 rows (312 groups), the top-4 blocks per (head, group), a window of
+    3 chunks excluded once 3 chunks lie outside it; 20 cached chunks in 64-token
+    blocks.  Select and selection attention timed as in the main run."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select, omnimem_sparse_attn, synth
+    w = synth.Workload("wan1.3b_g15", 12, 128, 4680, 4680, 64, 20, 20, 4, 15, 3, 3, torch.bfloat16, True, 1, 21)
+    x = synth.make_layer(w, 0, device=dev)
+    c = synth.page_layer(x.k, x.v, w.block_size, seed=3)
+    del x.k, x.v
+    sel = omnimem_select(c, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    out = torch.empty_like(x.q)
+    lse = torch.empty((w.heads, w.query_tokens), dtype=torch.float32, device=dev)
+    for _ in range(100):
+        omnimem_select(c, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale, out=sel,
+                       want_score=False)
+        omnimem_sparse_attn(c, x.q, sel.idx, sel.cnt, w.group_size, w.scale, out=out, lse=lse)
+    torch.cuda.synchronize()
+    e = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(reps)]
+    for r in range(reps):
+        e[r][0].record()
+        omnimem_select(c, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale, out=sel,
+                       want_score=False)
+        e[r][1].record()
+        omnimem_sparse_attn(c, x.q, sel.idx, sel.cnt, w.group_size, w.scale, out=out, lse=lse)
+        e[r][2].record()
+    torch.cuda.synchronize()
+    ts = float(np.median([x_[0].elapsed_time(x_[1]) for x_ in e]))
+    ta = float(np.median([x_[1].elapsed_time(x_[2]) for x_ in e]))
+    fl = attn_flops(sel.idx, sel.cnt, w, w.history_chunks)
+    idx = sel.idx.cpu().numpy()
+    gather = int((idx >= 0).sum()) * w.block_size * w.head_dim * 2 * 2
+    return {"workload": "Wan2.1-1.3B-shaped layer, query groups of 15 rows (312 groups), top-4 blocks per "
+                        "(head, group), 3-chunk window, 20 chunks of 64-token blocks",
+            "select_ms": round(ts, 4), "sparse_attn_ms": round(ta, 4), "ms_per_chunk_layer": round(ts + ta, 4),
+            "sparse_attn_tflops": round(fl / (ta * 1e-3) / 1e12, 2),
+            "gathered_kv_bytes": gather, "gather_gbs": round(gather / (ta * 1e-3) / 1e9, 1)}
 
 
 def lru_measure(dev, x, w, steps=60, working=4, sizes=(4, 5, 7, 10), seed=17):

@@ -309,6 +309,68 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
   }
 }
 
+// Score keys for many groups (R >= kScoreTiledMinGroups): a tile of 64 groups x 64
+// blocks per workgroup, each thread a 4 x 4 patch of dot products held in registers;
+// the proxy queries and pooled keys of the tile pass through LDS 32 dimensions at a
+// time, so every LDS read feeds four FMAs.  Each dot product still sums its d terms
+// in order 0..d-1.
+constexpr int kScoreTiledMinGroups = 32;
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void k_score_tiled(const float* __restrict__ kbar, int64_t kbar_stride,
+                                                          const float* __restrict__ qpart, int nsplit, int lq, int G,
+                                                          const int32_t* __restrict__ page_table, int64_t num_pages,
+                                                          int nb, int nbp, int first_excluded, int R, float scale,
+                                                          uint32_t* __restrict__ keys) {
+  constexpr int TB = 64, TR = 64, KC = 32, PAD = 4;
+  __shared__ __align__(16) float ks[KC][TB + PAD];  // [dimension][block]
+  __shared__ __align__(16) float qs[KC][TR + PAD];  // [dimension][group]
+  const int b0 = blockIdx.x * TB, r0 = blockIdx.y * TR, h = blockIdx.z;
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;  // blocks 4tx.., groups 4ty..
+  float acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int k = 0; k < 4; ++k) acc[i][k] = 0.f;
+  for (int j0 = 0; j0 < D; j0 += KC) {
+    for (int i = threadIdx.x; i < TB * KC; i += kThreads) {
+      const int bb = i / KC, j = i % KC;
+      ks[j][bb] = b0 + bb < nb ? kbar[(static_cast<int64_t>(h) * kbar_stride + b0 + bb) * D + j0 + j] : 0.f;
+    }
+    for (int i = threadIdx.x; i < TR * KC; i += kThreads) {
+      const int rr = i / KC, j = i % KC;
+      float v[1] = {0.f};
+      if (r0 + rr < R) proxy_cols<1>(qpart, h, r0 + rr, R, nsplit, D, j0 + j, lq, G, v);
+      qs[j][rr] = v[0];
+    }
+    __syncthreads();
+#pragma unroll 8
+    for (int j = 0; j < KC; ++j) {
+      const float4 a = *reinterpret_cast<const float4*>(&qs[j][4 * ty]);
+      const float4 b = *reinterpret_cast<const float4*>(&ks[j][4 * tx]);
+      const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int k = 0; k < 4; ++k) acc[i][k] = fmaf(av[i], bv[k], acc[i][k]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int r = r0 + 4 * ty + i;
+    if (r >= R) break;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int b = b0 + 4 * tx + k;
+      if (b >= nb) break;
+      const int32_t p = page_table != nullptr ? page_table[b] : 0;
+      const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
+      keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * acc[i][k]) : 0u;
+    }
+  }
+}
+
 // -------------------------------------------------------------- compressed history
 // Pools one history chunk into the compressed cache: one wave per (block, head)
 // slab; the block's K and V column means go to k_mean (fp32) and, rounded to the
@@ -722,6 +784,20 @@ __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict_
 
 inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+template <int D>
+void launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride, const float* qpart,
+                  int nbp, uint32_t* keys, hipStream_t stream) {
+  if (p.R >= kScoreTiledMinGroups) {
+    const dim3 grid((g.nb + 63) / 64, (p.R + 63) / 64, g.H);
+    hipLaunchKernelGGL((k_score_tiled<D>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq,
+                       p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+  } else {
+    const dim3 grid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
+    hipLaunchKernelGGL((k_score<D>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq, p.G,
+                       g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+  }
+}
+
 hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* keys, int nbp, int32_t* idx,
                        int32_t* cnt, float* score, hipStream_t stream) {
   const dim3 tgrid(p.R, g.H);
@@ -778,12 +854,8 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
       else if (p.R == 1) pool(k_pool_score<T, D, 128, 1>);
       else pool(k_pool_score<T, D, 128, kInlineGroups>);
     }
-    if (!p.inline_scores) {
-      const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
-      hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, kbar, static_cast<int64_t>(g.nb), qpart,
-                         p.qsplit, p.lq, p.G,
-                         g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
-    }
+    if (!p.inline_scores)
+      launch_score<D>(g, p, kbar, static_cast<int64_t>(g.nb), qpart, nbp, keys, stream);
   }
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
@@ -848,12 +920,7 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
   const int nbp = (g.nb + 3) / 4 * 4;
   hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kQThreads), 0, stream,
                      static_cast<const T*>(q), p.lq, g.H, p.G, p.R, p.qsplit, qpart);
-  if (g.nb > 0) {
-    const dim3 sgrid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
-    hipLaunchKernelGGL((k_score<D>), sgrid, dim3(kThreads), 0, stream, cc.k_mean, static_cast<int64_t>(cc.cap_blocks),
-                       qpart, p.qsplit, p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R,
-                       p.scale, keys);
-  }
+  if (g.nb > 0) launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
 

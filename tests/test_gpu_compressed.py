@@ -76,6 +76,7 @@ SMALL = [
     (2, 64, 200, 333, 64, 5, 5, 333, 1, 3, torch.bfloat16),    # d = 64
     (2, 128, 300, 257, 128, 4, 3, 100, 1, 2, torch.bfloat16),  # B = 128, 44-token tail
     (2, 128, 300, 300, 64, 5, 4, 15, 1, 3, torch.bfloat16),    # the paper's G = 15
+    (2, 128, 300, 1000, 64, 14, 4, 15, 1, 3, torch.bfloat16),  # G = 15, R = 67: tiled scoring
     (2, 128, 300, 100, 128, 4, 3, 40, 0, 0, torch.float32),    # fp32
     (1, 64, 64, 1, 64, 3, 2, 1, 2, 0, torch.float32),          # one query row, exact-block chunks
 ]

@@ -94,6 +94,7 @@ SMALL = [
     (2, 128, 300, 257, 128, 4, 3, 100, 1, 2, torch.bfloat16),  # B = 128 (two 64-key halves, 44-token tail)
     (2, 128, 130, 70, 64, 3, 2, 1, 1, 1, torch.bfloat16),      # per-query selection (G = 1, R = 70)
     (2, 128, 300, 300, 64, 5, 4, 15, 1, 3, torch.bfloat16),    # the paper's G = 15 (R = 20)
+    (2, 128, 300, 1000, 64, 14, 4, 15, 1, 3, torch.bfloat16),  # G = 15, R = 67: tiled scoring, ragged tiles
     (2, 128, 300, 100, 128, 4, 3, 40, 0, 0, torch.float32),    # fp32, d = 128, B = 128, no window
     (1, 64, 64, 1, 64, 3, 2, 1, 2, 0, torch.float32),          # one query row, exact-block chunks
 ]
