@@ -78,10 +78,15 @@ OMNIMEM_API omnimem_status_t omnimem_lru_create(const omnimem_kv_cache_t* kv, in
   L->k_host = static_cast<const char*>(k_host);
   L->v_host = static_cast<const char*>(v_host);
   L->page_table = const_cast<int32_t*>(kv->page_table);
-  L->slot_chunk.assign(slots, -1);
-  L->chunk_slot.assign(host_chunks, -1);
-  L->last_use.assign(slots, 0);
-  L->pinned_at.assign(slots, 0);
+  try {  // no exception may cross the C boundary
+    L->slot_chunk.assign(slots, -1);
+    L->chunk_slot.assign(host_chunks, -1);
+    L->last_use.assign(slots, 0);
+    L->pinned_at.assign(slots, 0);
+  } catch (...) {
+    delete L;
+    return OMNIMEM_EINVAL;
+  }
   // nothing resident yet: every row of the page table is -1
   hipStream_t s = static_cast<hipStream_t>(stream);
   for (int c = 0; c < L->table_chunks; ++c)
@@ -102,18 +107,20 @@ OMNIMEM_API omnimem_status_t omnimem_lru_require(omnimem_lru_t* L, const int32_t
   for (int i = 0; i < count; ++i)
     if (chunks[i] < 0 || chunks[i] >= L->host_chunks || chunks[i] >= L->table_chunks) return OMNIMEM_EINVAL;
   // the distinct chunks of the request must fit in the slots together
-  const uint64_t call = ++L->calls;
   std::vector<int> want;
-  want.reserve(count);
-  {
+  try {  // no exception may cross the C boundary
+    want.reserve(count);
     std::vector<char> seen(L->host_chunks, 0);
     for (int i = 0; i < count; ++i)
       if (!seen[chunks[i]]) {
         seen[chunks[i]] = 1;
         want.push_back(chunks[i]);
       }
+  } catch (...) {
+    return OMNIMEM_EINVAL;
   }
   if (static_cast<int>(want.size()) > L->slots) return OMNIMEM_EINVAL;
+  const uint64_t call = ++L->calls;
   // hits first: they are pinned for this call so that no miss evicts them
   for (int c : want) {
     const int slot = L->chunk_slot[c];
