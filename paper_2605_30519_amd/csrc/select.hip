@@ -309,6 +309,59 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
   }
 }
 
+// Score keys for few groups (R <= kInlineGroups) from stored pooled keys: one wave
+// per run of kScoreRowsPerWave blocks of a head; lane l holds dimensions
+// [D/64 * l, D/64 * (l + 1)) of every proxy query in registers and of each pooled key
+// row as it is read (one coalesced row read per block), then the dot products are
+// reduced across the wave by shuffles.
+constexpr int kScoreRowsPerWave = 8;
+
+template <int D, int NR>
+__global__ __launch_bounds__(kThreads) void k_score_rows(const float* __restrict__ kbar, int64_t kbar_stride,
+                                                         const float* __restrict__ qpart, int nsplit, int lq, int G,
+                                                         const int32_t* __restrict__ page_table, int64_t num_pages,
+                                                         int nb, int nbp, int first_excluded, int R, float scale,
+                                                         uint32_t* __restrict__ keys) {
+  constexpr int PL = D / kWave;  // dimensions per lane: 2 (d = 128) or 1 (d = 64)
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, h = blockIdx.y;
+  const int first = (blockIdx.x * (kThreads / kWave) + wave) * kScoreRowsPerWave;
+  float q[NR][PL];
+#pragma unroll
+  for (int r = 0; r < NR; ++r) {
+    float v[PL];
+#pragma unroll
+    for (int j = 0; j < PL; ++j) v[j] = 0.f;
+    if (r < R) proxy_cols<PL>(qpart, h, r, R, nsplit, D, PL * lane, lq, G, v);
+#pragma unroll
+    for (int j = 0; j < PL; ++j) q[r][j] = v[j];
+  }
+  float k[kScoreRowsPerWave][PL];  // every row's loads in flight before the products
+#pragma unroll
+  for (int i = 0; i < kScoreRowsPerWave; ++i) {
+    const int b = first + i;
+#pragma unroll
+    for (int j = 0; j < PL; ++j)
+      k[i][j] = b < nb ? kbar[(static_cast<int64_t>(h) * kbar_stride + b) * D + PL * lane + j] : 0.f;
+  }
+#pragma unroll
+  for (int i = 0; i < kScoreRowsPerWave; ++i) {
+    const int b = first + i;
+    if (b >= nb) break;
+    const int32_t p = page_table != nullptr ? page_table[b] : 0;
+    const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      if (r >= R) break;
+      float dot = 0.f;
+#pragma unroll
+      for (int j = 0; j < PL; ++j) dot = fmaf(q[r][j], k[i][j], dot);
+#pragma unroll
+      for (int m = 1; m < kWave; m <<= 1) dot += __shfl_xor(dot, m);
+      if (lane == 0) keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * dot) : 0u;
+    }
+  }
+}
+
 // Score keys for many groups (R >= kScoreTiledMinGroups): a tile of 64 groups x 64
 // blocks per workgroup, each thread a 4 x 4 patch of dot products held in registers;
 // the proxy queries and pooled keys of the tile pass through LDS 32 dimensions at a
@@ -423,11 +476,11 @@ __global__ __launch_bounds__(kThreads) void k_compress_chunk(CompressArgs a) {
   for (int j = 0; j < VEC; ++j) ks[j] = vs[j] = 0.f;
   if (live) {
     const int64_t off = (page * a.H + h) * static_cast<int64_t>(B) * D;
-    uint4 raw[Sh::PASSES];
-    load_slab<T, D, B>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, raw);
-    sum_slab<T, D, B>(raw, ks);
-    load_slab<T, D, B>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, raw);
-    sum_slab<T, D, B>(raw, vs);
+    uint4 kraw[Sh::PASSES], vraw[Sh::PASSES];  // both slabs' loads in flight before the sums
+    load_slab<T, D, B>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, kraw);
+    load_slab<T, D, B>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, vraw);
+    sum_slab<T, D, B>(kraw, ks);
+    sum_slab<T, D, B>(vraw, vs);
     const float inv = 1.0f / static_cast<float>(nvalid);
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
@@ -787,7 +840,17 @@ inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255);
 template <int D>
 void launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride, const float* qpart,
                   int nbp, uint32_t* keys, hipStream_t stream) {
-  if (p.R >= kScoreTiledMinGroups) {
+  if (p.R <= kInlineGroups) {
+    const int waves = (g.nb + kScoreRowsPerWave - 1) / kScoreRowsPerWave;
+    const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
+    if (p.R == 1)
+      hipLaunchKernelGGL((k_score_rows<D, 1>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit,
+                         p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+    else
+      hipLaunchKernelGGL((k_score_rows<D, kInlineGroups>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart,
+                         p.qsplit, p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale,
+                         keys);
+  } else if (p.R >= kScoreTiledMinGroups) {
     const dim3 grid((g.nb + 63) / 64, (p.R + 63) / 64, g.H);
     hipLaunchKernelGGL((k_score_tiled<D>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq,
                        p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
