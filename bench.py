@@ -221,6 +221,10 @@ def main():
         "roofline": dominant,
         "stages": {"select_ms": round(float(np.median(sel_ms)), 4),
                    "sparse_attn_ms": round(float(np.median(att_ms)), 4),
+                   "select_ms_p10_p90": [round(float(np.percentile(sel_ms, 10)), 4),
+                                         round(float(np.percentile(sel_ms, 90)), 4)],
+                   "sparse_attn_ms_p10_p90": [round(float(np.percentile(att_ms, 10)), 4),
+                                              round(float(np.percentile(att_ms, 90)), 4)],
                    "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe},
     }
 
@@ -331,6 +335,10 @@ def main():
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a bounded sample")
         result["cpu_baseline"] = cpu_baseline(x0, w, flops_per_layer[0] + sflops)
+        log("oracle on subsamples of the 120-chunk dense attention and the 30-layer ramp (extrapolated)")
+        del x0
+        torch.cuda.empty_cache()
+        result["cpu_baseline"]["extrapolated"] = oracle_extrapolations(dev)
 
     print(json.dumps(result), flush=True)
 
@@ -716,6 +724,59 @@ def stress_comparison(dev):
             "union_fraction": round(U / (nb - w.window_chunks * w.blocks_per_chunk), 4),
             "scattered_kv_bytes": int(sum(per_head)) * slab, "merged_buffer_bytes": w.heads * U * slab,
             "outputs_bit_equal": bool(torch.equal(uo.view(torch.int16), out.view(torch.int16)))}
+
+
+def oracle_extrapolations(dev, rows=48, seed=9):
+    """The fp64 oracle where a whole run is far too long for the CPU: timed on a
+    deterministic sample and scaled up, each result labelled extrapolated.
+    - dense attention over 120 chunks (561,600 keys): `rows` sampled (head, row)
+      pairs, scaled to all 56,160;
+    - the 30-layer ramp: one layer's selection (whole) and sparse attention
+      (`rows` sampled pairs) at history 1, 4, 30 and 60, interpolated linearly over
+      n = 1..60 and multiplied by 30 layers."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2605_30519_amd import synth
+    rng = np.random.default_rng(seed)
+    out = {}
+    wl = synth.WORKLOADS["wan1.3b_long"]
+    x = synth.make_layer(wl, 0, device=dev)
+    q, k, v = x.q.cpu(), x.k.cpu(), x.v.cpu()
+    del x
+    torch.cuda.empty_cache()
+    total = wl.heads * wl.query_tokens
+    hs, qs = rng.integers(0, wl.heads, rows), rng.integers(0, wl.query_tokens, rows)
+    t0 = time.perf_counter()
+    oracle.dense_attn(q, k, v, wl.block_size, 0, wl.history_chunks, wl.scale, hs=hs, qs=qs)
+    dt = time.perf_counter() - t0
+    out["dense_n120_s"] = {"value": round(dt * total / rows, 1), "sample_rows": rows, "sample_s": round(dt, 2),
+                           "label": "extrapolated"}
+    del q, k, v
+    w = synth.WORKLOADS["wan1.3b_30layer"]
+    x = synth.make_layer(w, 0, device=dev)
+    k, v = x.k.cpu(), x.v.cpu()
+    total = w.heads * w.query_tokens
+    per_step = {}
+    for n in (1, 4, 30, 60):
+        q = synth.queries(w, 0, n, x.rel, dev).cpu()
+        t0 = time.perf_counter()
+        ref = oracle.select(q, k[:n], w.block_size, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks,
+                            w.scale)
+        t1 = time.perf_counter()
+        hs, qs = rng.integers(0, w.heads, rows), rng.integers(0, w.query_tokens, rows)
+        oracle.sparse_attn(q, k[:n], v[:n], w.block_size, ref["idx"], ref["cnt"], w.group_size, w.scale, hs=hs, qs=qs)
+        t2 = time.perf_counter()
+        per_step[n] = (t1 - t0) + (t2 - t1) * total / rows
+    del x, k, v
+    torch.cuda.empty_cache()
+    ns = sorted(per_step)
+    ramp = sum(float(np.interp(n, ns, [per_step[m] for m in ns])) for n in range(1, w.history_chunks + 1))
+    out["ramp_30_layers_s"] = {"value": round(ramp * w.layers, 1),
+                               "per_step_s": {str(n): round(t, 2) for n, t in per_step.items()},
+                               "label": "extrapolated"}
+    return out
 
 
 def cpu_baseline(x, w, step_flops, reps=3):
