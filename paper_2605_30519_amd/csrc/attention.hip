@@ -150,7 +150,8 @@ __device__ int decode_tiles(const AttnArgs& a, const int32_t* list, int count, i
 }
 
 // ------------------------------------------------------------------ bf16 / MFMA
-constexpr int kWaves = 8;  // 256 query rows per workgroup, two waves per SIMD
+constexpr int kWaves = 8;       // 256 query rows per workgroup, two waves per SIMD
+constexpr int kSmallWaves = 4;  // groups of at most 32 rows: one wave per SIMD, two workgroups per CU
 
 // A-operand row order for S^T = K Q^T: swapping bits 2 and 3 of the row makes the
 // accumulator element i of lane l hold key 8*(l/32)+i (i < 8) or 16+8*(l/32)+(i-8).
@@ -162,22 +163,27 @@ __device__ __forceinline__ int s_row_perm(int x) { return (x & ~12) | ((x & 4) <
 //  V rows are read by ds_read_b64_tr_b16, 4 rows x 32 B per 16-lane group and two
 //    groups per pass: a stride of 16 or 48 (mod 64) dwords makes the 8 row segments of a
 //    pass disjoint.
-template <int D>
+template <int D, bool PHASED>
 struct AttnLds {
   static constexpr int K_STRIDE = D == 128 ? 136 : 72;
   static constexpr int V_STRIDE = D == 128 ? 160 : 96;
   static constexpr int K_ELEMS = kTileKeys * K_STRIDE;
   static constexpr int V_ELEMS = kTileKeys * V_STRIDE;
   static constexpr int K_STAGES = 2;
-  static constexpr int V_STAGES = 3;  // the phase-shifted waves still read the previous tile's V
+  static constexpr int V_STAGES = PHASED ? 3 : 2;  // the phase-shifted waves still read the previous tile's V
   static constexpr int TOTAL_ELEMS = K_STAGES * K_ELEMS + V_STAGES * V_ELEMS;
 };
 
-template <int D>
-__global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
-  using L = AttnLds<D>;
-  constexpr int NT = kWaves * kWave;
-  constexpr int ROWS = kWaves * 32;
+// NW waves of 32 query rows.  PHASED: the upper half of the waves runs half a tile
+// behind the lower half (see below).  Groups of at most 32 rows fill only wave 0, so
+// they take the unshifted four-wave variant: its smaller LDS ring (two V stages) and
+// tile table, and one wave per SIMD, let two workgroups share a CU, so that two
+// groups' loads are in flight at once.
+template <int D, bool PHASED, int NW>
+__global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
+  using L = AttnLds<D, PHASED>;
+  constexpr int NT = NW * kWave;
+  constexpr int ROWS = NW * 32;
   constexpr int CHUNKS_PER_ROW = D / 8;                        // 16-byte chunks per key row
   constexpr int CPT = kTileKeys * CHUNKS_PER_ROW / NT;         // chunks per thread per tile (K and V each)
   constexpr int DT = D / 32;                                   // 32-wide output tiles along d
@@ -185,7 +191,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   static_assert(CPT >= 1, "tile too small for the workgroup");
   __shared__ __attribute__((aligned(16))) uint16_t lds[L::TOTAL_ELEMS];
   __shared__ int2 table[2 * NT];  // decoded tiles of up to NT list entries
-  __shared__ int scan_tmp[kWaves];
+  __shared__ int scan_tmp[NW];
   uint16_t* const k_ring = lds;
   uint16_t* const v_ring = lds + L::K_STAGES * L::K_ELEMS;
 
@@ -256,7 +262,7 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
   // The two waves that share a SIMD (w and w + 4) run the same tile half a step
   // apart: waves 0-3 do QK(t), softmax(t), PV(t); waves 4-7 do PV(t-1), QK(t),
   // softmax(t).  While one of them is in its softmax (VALU) the other issues MFMAs.
-  const bool late = wave >= kWaves / 2;
+  const bool late = PHASED && wave >= NW / 2;
   bf16x8 pb[4];
   auto pv = [&](const uint16_t* v_lds) {
 #pragma unroll
@@ -310,10 +316,10 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       prefetch(cur_tile.x, cur_tile.y);  // next tile: global loads in flight during this tile's math
     }
     const uint16_t* k_lds = k_ring + (t % 2) * L::K_ELEMS;
-    const uint16_t* v_lds = v_ring + (t % 3) * L::V_ELEMS;
+    const uint16_t* v_lds = v_ring + (t % L::V_STAGES) * L::V_ELEMS;
 
     if (wave_live) {
-      if (late && t > 0) pv(v_ring + ((t + 2) % 3) * L::V_ELEMS);  // PV of the previous tile
+      if (late && t > 0) pv(v_ring + ((t + L::V_STAGES - 1) % L::V_STAGES) * L::V_ELEMS);  // PV of the previous tile
       // ---- S^T = K Q^T for keys [0, 64): two 32-key accumulators
       f32x16 s_acc[2];
 #pragma unroll
@@ -367,18 +373,18 @@ __global__ __launch_bounds__(kWaves* kWave) void k_attn_bf16(AttnArgs a) {
       l_run += psum;
       if (!late) pv(v_lds);
     }
-    if (have) stage((t + 1) % 2, (t + 1) % 3);  // stages not read in this step
+    if (have) stage((t + 1) % 2, (t + 1) % L::V_STAGES);  // stages not read in this step
     __syncthreads();
     ++t;
   }
-  if (late && wave_live && t > 0) pv(v_ring + ((t + 2) % 3) * L::V_ELEMS);  // the last tile's PV
+  if (late && wave_live && t > 0) pv(v_ring + ((t + L::V_STAGES - 1) % L::V_STAGES) * L::V_ELEMS);  // the last tile's PV
   __syncthreads();  // the rings are reused below for the output
 
   // ---- epilogue: normalise, stage O through LDS, store rows with 16-byte writes
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   constexpr int SSTRIDE = D + 8;
-  static_assert(kWaves * 32 * SSTRIDE <= L::TOTAL_ELEMS, "output staging does not fit");
+  static_assert(NW * 32 * SSTRIDE <= L::TOTAL_ELEMS, "output staging does not fit");
   uint16_t* stage_o = lds + wave * 32 * SSTRIDE;
 #pragma unroll
   for (int dt = 0; dt < DT; ++dt)
@@ -1040,7 +1046,8 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   const int rows = L.group_size < L.lq ? L.group_size : L.lq;
   // bf16, d = 128 and groups of more than 32 rows: 64 rows per wave; else 32
   const bool r64 = g.dtype == 0 && g.D == 128 && rows > 32;
-  const int rows_per_wg = g.dtype != 0 ? kWave : r64 ? kR64Waves * 64 : kWaves * 32;
+  const bool small = rows <= 32;  // one wave's rows per group: the four-wave unshifted variant
+  const int rows_per_wg = g.dtype != 0 ? kWave : r64 ? kR64Waves * 64 : (small ? kSmallWaves : kWaves) * 32;
   a.tiles_per_group = (rows + rows_per_wg - 1) / rows_per_wg;
   const int64_t nwg = static_cast<int64_t>(g.H) * L.R * a.tiles_per_group;
   if (nwg <= 0) return hipSuccess;
@@ -1048,10 +1055,18 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   if (r64) {
     hipLaunchKernelGGL(k_attn_bf16_r64<128>, dim3(static_cast<unsigned>(nwg)), dim3(kR64Waves * kWave), 0, stream, a);
   } else if (g.dtype == 0) {
-    if (g.D == 128)
-      hipLaunchKernelGGL(k_attn_bf16<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWaves * kWave), 0, stream, a);
-    else
-      hipLaunchKernelGGL(k_attn_bf16<64>, dim3(static_cast<unsigned>(nwg)), dim3(kWaves * kWave), 0, stream, a);
+    const dim3 grid(static_cast<unsigned>(nwg));
+    if (!small) {
+      if (g.D == 128)
+        hipLaunchKernelGGL((k_attn_bf16<128, true, kWaves>), grid, dim3(kWaves * kWave), 0, stream, a);
+      else
+        hipLaunchKernelGGL((k_attn_bf16<64, true, kWaves>), grid, dim3(kWaves * kWave), 0, stream, a);
+    } else {
+      if (g.D == 128)
+        hipLaunchKernelGGL((k_attn_bf16<128, false, kSmallWaves>), grid, dim3(kSmallWaves * kWave), 0, stream, a);
+      else
+        hipLaunchKernelGGL((k_attn_bf16<64, false, kSmallWaves>), grid, dim3(kSmallWaves * kWave), 0, stream, a);
+    }
   } else {
     if (g.D == 128)
       hipLaunchKernelGGL(k_attn_f32<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWave), 0, stream, a);
