@@ -29,16 +29,20 @@ constexpr int kThreads = 256;
 
 // -------------------------------------------------------------- proxy queries
 constexpr int kQThreads = 1024;
+constexpr int kQSmallThreads = 64;   // groups of at most kQSmallRows rows: one wave per split
+constexpr int kQSmallRows = 64;
 
-template <typename T, int D>
-__global__ __launch_bounds__(kQThreads) void k_qmean_partial(const T* __restrict__ q, int lq, int H, int G, int R,
-                                                             int nsplit, float* __restrict__ partial) {
+// NT threads per split; UNROLL rows per thread in flight (the big variant covers a
+// 512-row split in one round, the one-wave variant small groups).
+template <typename T, int D, int NT>
+__global__ __launch_bounds__(NT) void k_qmean_partial(const T* __restrict__ q, int lq, int H, int G, int R,
+                                                      int nsplit, float* __restrict__ partial) {
   using V = Vec16<T>;
   constexpr int VEC = V::N;
-  constexpr int CPR = D / VEC;             // 16-byte chunks per row
-  constexpr int PHASES = kQThreads / CPR;  // rows summed side by side
-  constexpr int UNROLL = (kQRowsPerSplit + PHASES - 1) / PHASES;  // one round of loads covers the split
-  constexpr int kWaves = kQThreads / kWave, PH_PER_WAVE = kWave / CPR;
+  constexpr int CPR = D / VEC;       // 16-byte chunks per row
+  constexpr int PHASES = NT / CPR;   // rows summed side by side
+  constexpr int UNROLL = NT == kQThreads ? (kQRowsPerSplit + PHASES - 1) / PHASES : (kQSmallRows + PHASES - 1) / PHASES;
+  constexpr int kWaves = NT / kWave, PH_PER_WAVE = kWave / CPR;
   __shared__ float red[kWaves][D];
 
   const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z;
@@ -77,7 +81,7 @@ __global__ __launch_bounds__(kQThreads) void k_qmean_partial(const T* __restrict
   }
   __syncthreads();
   static_assert(PH_PER_WAVE >= 1, "a wave spans whole rows");
-  for (int col = threadIdx.x; col < D; col += kQThreads) {
+  for (int col = threadIdx.x; col < D; col += NT) {
     float sum = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) sum += red[w][col];
@@ -362,11 +366,13 @@ __global__ __launch_bounds__(kThreads) void k_score_rows(const float* __restrict
   }
 }
 
-// Score keys for many groups (R >= kScoreTiledMinGroups): a tile of 64 groups x 64
-// blocks per workgroup, each thread a 4 x 4 patch of dot products held in registers;
-// the proxy queries and pooled keys of the tile pass through LDS 32 dimensions at a
-// time, so every LDS read feeds four FMAs.  Each dot product still sums its d terms
-// in order 0..d-1.
+// Score keys for many groups (R >= kScoreTiledMinGroups): the products q_r . k_b form
+// a dense R x N_b contraction per head, run on fp32 MFMA (v_mfma_f32_32x32x2_f32,
+// fp32 products and accumulation).  A workgroup takes 64 groups x 64 blocks, each of
+// its four waves a 32 x 32 quarter; proxy queries and pooled keys pass through LDS
+// 32 dimensions at a time, stored dimension-major with a row stride of 96 floats so
+// that the two half-waves of an operand read (dimensions 2s and 2s + 1) fall on
+// disjoint banks.
 constexpr int kScoreTiledMinGroups = 32;
 
 template <int D>
@@ -375,52 +381,79 @@ __global__ __launch_bounds__(kThreads) void k_score_tiled(const float* __restric
                                                           const int32_t* __restrict__ page_table, int64_t num_pages,
                                                           int nb, int nbp, int first_excluded, int R, float scale,
                                                           uint32_t* __restrict__ keys) {
-  constexpr int TB = 64, TR = 64, KC = 32, PAD = 4;
-  __shared__ __align__(16) float ks[KC][TB + PAD];  // [dimension][block]
-  __shared__ __align__(16) float qs[KC][TR + PAD];  // [dimension][group]
+  constexpr int TB = 64, TR = 64, KC = 32, STRIDE = 96;
+  __shared__ __align__(16) float ks[KC][STRIDE];  // [dimension][block]
+  __shared__ __align__(16) float qs[KC][STRIDE];  // [dimension][group]
   const int b0 = blockIdx.x * TB, r0 = blockIdx.y * TR, h = blockIdx.z;
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;  // blocks 4tx.., groups 4ty..
-  float acc[4][4];
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int wr = 32 * (wave / 2), wb = 32 * (wave % 2);  // this wave's quarter
+  f32x16 acc = {};
+  // one row per lane, four dimensions per load (the LDS stores of a wave are then
+  // conflict-free); the next chunk's loads are in flight during this chunk's MFMAs
+  constexpr int PER = TB * (KC / 4) / kThreads;  // loads per thread per chunk
+  float4 kv[PER], qv[PER];
+  // groups of one split (the usual case here: small groups) hold their sum in one
+  // partial: one load, scaled by the group's reciprocal row count
+  float inv_rows[PER];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int u = 0; u < PER; ++u) {
+    const int r = r0 + (threadIdx.x + u * kThreads) % TB;
+    inv_rows[u] = r < R ? 1.0f / static_cast<float>(min(r * G + G, lq) - r * G) : 0.f;
+  }
+  auto fetch = [&](int j0) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k) acc[i][k] = 0.f;
-  for (int j0 = 0; j0 < D; j0 += KC) {
-    for (int i = threadIdx.x; i < TB * KC; i += kThreads) {
-      const int bb = i / KC, j = i % KC;
-      ks[j][bb] = b0 + bb < nb ? kbar[(static_cast<int64_t>(h) * kbar_stride + b0 + bb) * D + j0 + j] : 0.f;
+    for (int u = 0; u < PER; ++u) {
+      const int i = threadIdx.x + u * kThreads, row = i % TB, jq = i / TB;
+      kv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (b0 + row < nb)
+        kv[u] = *reinterpret_cast<const float4*>(kbar + (static_cast<int64_t>(h) * kbar_stride + b0 + row) * D + j0 +
+                                                 4 * jq);
+      qv[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r0 + row < R) {
+        if (nsplit == 1) {
+          const float4 sum = *reinterpret_cast<const float4*>(
+              qpart + (static_cast<int64_t>(h) * R + r0 + row) * D + j0 + 4 * jq);
+          qv[u] = make_float4(sum.x * inv_rows[u], sum.y * inv_rows[u], sum.z * inv_rows[u], sum.w * inv_rows[u]);
+        } else {
+          float q4[4];
+          proxy_cols<4>(qpart, h, r0 + row, R, nsplit, D, j0 + 4 * jq, lq, G, q4);
+          qv[u] = make_float4(q4[0], q4[1], q4[2], q4[3]);
+        }
+      }
     }
-    for (int i = threadIdx.x; i < TR * KC; i += kThreads) {
-      const int rr = i / KC, j = i % KC;
-      float v[1] = {0.f};
-      if (r0 + rr < R) proxy_cols<1>(qpart, h, r0 + rr, R, nsplit, D, j0 + j, lq, G, v);
-      qs[j][rr] = v[0];
+  };
+  fetch(0);
+  for (int j0 = 0; j0 < D; j0 += KC) {
+#pragma unroll
+    for (int u = 0; u < PER; ++u) {
+      const int i = threadIdx.x + u * kThreads, row = i % TB, jq = i / TB;
+      ks[4 * jq + 0][row] = kv[u].x;
+      ks[4 * jq + 1][row] = kv[u].y;
+      ks[4 * jq + 2][row] = kv[u].z;
+      ks[4 * jq + 3][row] = kv[u].w;
+      qs[4 * jq + 0][row] = qv[u].x;
+      qs[4 * jq + 1][row] = qv[u].y;
+      qs[4 * jq + 2][row] = qv[u].z;
+      qs[4 * jq + 3][row] = qv[u].w;
     }
     __syncthreads();
-#pragma unroll 8
-    for (int j = 0; j < KC; ++j) {
-      const float4 a = *reinterpret_cast<const float4*>(&qs[j][4 * ty]);
-      const float4 b = *reinterpret_cast<const float4*>(&ks[j][4 * tx]);
-      const float av[4] = {a.x, a.y, a.z, a.w}, bv[4] = {b.x, b.y, b.z, b.w};
+    if (j0 + KC < D) fetch(j0 + KC);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int k = 0; k < 4; ++k) acc[i][k] = fmaf(av[i], bv[k], acc[i][k]);
+    for (int st = 0; st < KC / 2; ++st) {
+      const int j = 2 * st + lane / 32;
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(qs[j][wr + lane % 32], ks[j][wb + lane % 32], acc, 0, 0, 0);
     }
     __syncthreads();
   }
+  // accumulator element i of lane l: group wr + 8 (i / 4) + 4 (l / 32) + i % 4, block wb + l % 32
+  const int b = b0 + wb + lane % 32;
+  if (b >= nb) return;
+  const int32_t p = page_table != nullptr ? page_table[b] : 0;
+  const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int r = r0 + 4 * ty + i;
-    if (r >= R) break;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const int b = b0 + 4 * tx + k;
-      if (b >= nb) break;
-      const int32_t p = page_table != nullptr ? page_table[b] : 0;
-      const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
-      keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * acc[i][k]) : 0u;
-    }
+  for (int i = 0; i < 16; ++i) {
+    const int r = r0 + wr + 8 * (i / 4) + 4 * (lane / 32) + i % 4;
+    if (r < R) keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * acc[i]) : 0u;
   }
 }
 
@@ -524,6 +557,7 @@ constexpr int kTopkRegMax = kTopkMaxThreads * 4 * kTopkVecPerLane;        // lar
 constexpr int kTopkBinBits = 11;
 constexpr int kTopkBins = 1 << kTopkBinBits;
 constexpr int kTopkList = 256;
+constexpr int kTopkManyRows = 1024;  // (head, group) rows from which k_topk<256> is used
 constexpr int kPoolBlocksPerWave = 2;  // at most the pooling kernel's page-id batch (kMaxBlocksPerWave)
 
 // Called by all NT threads of a workgroup; out_score may be null.
@@ -861,11 +895,28 @@ void launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, in
   }
 }
 
+// Proxy-query partial sums: 1,024 threads per 512-row split, or one wave per
+// group when groups hold at most kQSmallRows rows (one split each).
+template <typename T, int D>
+void launch_qmean(const SelectPlan& p, const CacheGeom& g, const T* q, float* qpart, hipStream_t stream) {
+  const dim3 grid(p.qsplit, p.R, g.H);
+  if (p.G <= kQSmallRows)
+    hipLaunchKernelGGL((k_qmean_partial<T, D, kQSmallThreads>), grid, dim3(kQSmallThreads), 0, stream, q, p.lq, g.H,
+                       p.G, p.R, p.qsplit, qpart);
+  else
+    hipLaunchKernelGGL((k_qmean_partial<T, D, kQThreads>), grid, dim3(kQThreads), 0, stream, q, p.lq, g.H, p.G, p.R,
+                       p.qsplit, qpart);
+}
+
 hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* keys, int nbp, int32_t* idx,
                        int32_t* cnt, float* score, hipStream_t stream) {
   const dim3 tgrid(p.R, g.H);
-  // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice that
-  if (g.nb <= 512 * 4 * kTopkVecPerLane)
+  // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice
+  // that; with many rows (small query groups) 256-thread workgroups pack more rows
+  // per CU
+  if (p.R * g.H >= kTopkManyRows && g.nb <= 256 * 4 * kTopkVecPerLane)
+    hipLaunchKernelGGL(k_topk<256>, tgrid, dim3(256), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  else if (g.nb <= 512 * 4 * kTopkVecPerLane)
     hipLaunchKernelGGL(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
   else if (g.nb <= kTopkRegMax)
     hipLaunchKernelGGL(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
@@ -883,8 +934,7 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
   uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
   const int nbp = (g.nb + 3) / 4 * 4;
 
-  hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kQThreads), 0, stream,
-                     static_cast<const T*>(q), p.lq, g.H, p.G, p.R, p.qsplit, qpart);
+  launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
   if (g.nb > 0) {
     PoolArgs a;
     a.k_pages = g.k_pages;
@@ -981,8 +1031,7 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
   float* qpart = reinterpret_cast<float*>(ws + p.off_qpart);
   uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
   const int nbp = (g.nb + 3) / 4 * 4;
-  hipLaunchKernelGGL((k_qmean_partial<T, D>), dim3(p.qsplit, p.R, g.H), dim3(kQThreads), 0, stream,
-                     static_cast<const T*>(q), p.lq, g.H, p.G, p.R, p.qsplit, qpart);
+  launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
   if (g.nb > 0) launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
