@@ -56,6 +56,8 @@ def _configure(L):
     L.oracle_query_scores.argtypes = [c_int] * 6 + [c_int, _vp, c_int, _vp, ctypes.c_double, _f64p]
     L.oracle_select.argtypes = ([c_int] * 6 + [c_int, _vp, c_int, _vp, _u8p] + [c_int] * 4 +
                                 [ctypes.c_double, c_int, c_int, _i32p, _i32p, _f64p, _f64p])
+    L.oracle_select_prob.argtypes = ([c_int] * 5 + [c_int, _vp, _f64p, _u8p] + [c_int] * 4 +
+                                     [ctypes.c_double, c_int, c_int, _i32p, _i32p, _f64p, _f64p])
     L.oracle_sparse_attn.argtypes = ([c_int] * 6 + [c_int, _vp, c_int, _vp, _vp, _u8p, _i32p, _i32p,
                                      c_int, c_int, ctypes.c_double, c_int, _i32p, _i32p, _f64p, _f64p])
     L.oracle_dense_attn.argtypes = ([c_int] * 6 + [c_int, _vp, c_int, _vp, _vp, _u8p, c_int, c_int,
@@ -227,6 +229,36 @@ def select(q, k, B: int, top_k: int, group_size: int, window_chunks: int, awe_mi
                               cnt.ctypes.data_as(_i32p), score.ctypes.data_as(_f64p),
                               alls.ctypes.data_as(_f64p) if alls is not None else ctypes.cast(None, _f64p))
     _check(awe, "select")
+    out = dict(idx=idx, cnt=cnt, score=score, awe=bool(awe))
+    if alls is not None:
+        out["all_scores"] = alls
+    return out
+
+
+def select_prob(q, kc, n: int, Bpc: int, top_k: int, group_size: int, window_chunks: int,
+                awe_min_outside_chunks: int, scale: float, resident=None, heads=None, want_all_scores=False):
+    """Selection by the probability-averaged compression score: each query's softmax over
+    all n*Bpc pooled keys kc ([H, n*Bpc, d], float64), averaged over its group (Eq. 3),
+    then the top-K over Omega (Eq. 2).  Same outputs as ``select``; the scores are the
+    group-mean probabilities."""
+    kc = np.ascontiguousarray(np.asarray(kc, dtype=np.float64))
+    H, N, d = (int(s) for s in kc.shape)
+    if N != n * Bpc:
+        raise ValueError(f"kc holds {N} pooled keys, expected n*Bpc = {n * Bpc}")
+    Lq = int(q.shape[0])
+    R = -(-Lq // group_size)
+    h0, h1 = (0, H) if heads is None else heads
+    etq, kq, pq = _as_input(q)
+    keep, rp = _u8_or_null(resident)
+    idx = np.full((H, R, top_k), -1, dtype=np.int32)
+    cnt = np.zeros((H, R), dtype=np.int32)
+    score = np.full((H, R, top_k), -np.inf)
+    alls = np.zeros((H, R, N)) if want_all_scores else None
+    awe = lib().oracle_select_prob(H, d, n, Bpc, Lq, etq, pq, kc.ctypes.data_as(_f64p), rp, top_k, group_size,
+                                   window_chunks, awe_min_outside_chunks, scale, h0, h1, idx.ctypes.data_as(_i32p),
+                                   cnt.ctypes.data_as(_i32p), score.ctypes.data_as(_f64p),
+                                   alls.ctypes.data_as(_f64p) if alls is not None else ctypes.cast(None, _f64p))
+    _check(awe, "select_prob")
     out = dict(idx=idx, cnt=cnt, score=score, awe=bool(awe))
     if alls is not None:
         out["all_scores"] = alls

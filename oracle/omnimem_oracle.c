@@ -270,6 +270,90 @@ int oracle_select(int H, int d, int S, int n, int B, int Lq, int et_q, const voi
   return awe;
 }
 
+/* ------------------------------------------------------------------ probability scores
+ * The probability-averaged reading of the compression score (Sec. 3.1: selection
+ * ranks blocks by the compression branch's attention scores; App. C: that branch
+ * attends every pooled token of the history; Eq. 3: a group averages its queries'
+ * scores).  For heads [h_begin, h_end), with kc[h] the N = n*Bpc pooled keys:
+ *   u[q][b]    = scale * (q . kc[h][b])                 for every pooled token b
+ *   p[q][b]    = exp(u[q][b] - LSE_q),  LSE_q = ln sum over all b of exp(u[q][b])
+ *   sbar[r][b] = (1/|G_r|) sum over the queries q of group r of p[q][b]
+ *   I[h][r]    = TopK over Omega of sbar[r][.]
+ * The softmax runs over all N pooled tokens (window and non-resident blocks
+ * included); only the top-K is restricted to Omega.  Ranking, output order,
+ * padding and all_scores are as in oracle_select.  Returns the AWE state or -1. */
+int oracle_select_prob(int H, int d, int n, int Bpc, int Lq, int et_q, const void* Q, const double* kc,
+                       const uint8_t* resident, int top_k, int G_q, int E, int T_out, double scale, int h_begin,
+                       int h_end, int32_t* idx, int32_t* cnt, double* sel_score, double* all_scores) {
+  if (Bpc < 1 || H < 1 || d < 1 || n < 0 || Lq < 1 || top_k < 1 || G_q < 1 || E < 0 || T_out < 0) return -1;
+  if (h_begin < 0 || h_end > H || h_begin > h_end || idx == NULL || cnt == NULL) return -1;
+  if (!valid_et(et_q) || Q == NULL || (n > 0 && kc == NULL)) return -1;
+  int R = (Lq + G_q - 1) / G_q;
+  int64_t nb = (int64_t)n * Bpc;
+  uint8_t* omega = (uint8_t*)malloc((size_t)nb + 1);
+  if (omega == NULL) return -1;
+  int awe = oracle_candidates(n, Bpc, top_k, E, T_out, resident, omega);
+  if (awe < 0) {
+    free(omega);
+    return -1;
+  }
+
+#pragma omp parallel for collapse(2) schedule(dynamic)
+  for (int h = h_begin; h < h_end; ++h) {
+    for (int r = 0; r < R; ++r) {
+      double* u = (double*)malloc(sizeof(double) * (size_t)(nb + 1));
+      double* sbar = (double*)calloc((size_t)(nb + 1), sizeof(double));
+      ranked_t* cand = (ranked_t*)malloc(sizeof(ranked_t) * (size_t)(nb + 1));
+      int32_t* chosen = (int32_t*)malloc(sizeof(int32_t) * (size_t)(top_k + 1));
+      int row0 = r * G_q, row1 = row0 + G_q < Lq ? row0 + G_q : Lq;
+      for (int q = row0; q < row1 && nb > 0; ++q) {
+        double mx = -INFINITY;
+        for (int64_t b = 0; b < nb; ++b) {
+          double dot = 0.0;
+          for (int j = 0; j < d; ++j) dot += widen(Q, ((int64_t)q * H + h) * d + j, et_q) * kc[((int64_t)h * nb + b) * d + j];
+          u[b] = scale * dot;
+          mx = u[b] > mx ? u[b] : mx;
+        }
+        double denom = 0.0;
+        for (int64_t b = 0; b < nb; ++b) denom += exp(u[b] - mx);
+        double lse_q = mx + log(denom);
+        for (int64_t b = 0; b < nb; ++b) sbar[b] += exp(u[b] - lse_q);
+      }
+      int64_t m = 0;
+      for (int64_t b = 0; b < nb; ++b) {
+        double sb = sbar[b] / (double)(row1 - row0);
+        if (all_scores != NULL) all_scores[((int64_t)h * R + r) * nb + b] = omega[b] ? sb : NAN;
+        if (omega[b] != 0) {
+          cand[m].s = sb;
+          cand[m].b = (int32_t)b;
+          ++m;
+        }
+      }
+      qsort(cand, (size_t)m, sizeof(ranked_t), rank_cmp);
+      int take = m < top_k ? (int)m : top_k;
+      for (int t = 0; t < take; ++t) chosen[t] = cand[t].b;
+      qsort(chosen, (size_t)take, sizeof(int32_t), id_cmp);
+      int64_t base = ((int64_t)h * R + r) * top_k;
+      for (int t = 0; t < top_k; ++t) {
+        idx[base + t] = t < take ? chosen[t] : -1;
+        if (sel_score != NULL) {
+          double v = -INFINITY;
+          for (int w = 0; w < take && t < take; ++w)
+            if (cand[w].b == chosen[t]) v = cand[w].s;
+          sel_score[base + t] = v;
+        }
+      }
+      cnt[(int64_t)h * R + r] = take;
+      free(u);
+      free(sbar);
+      free(cand);
+      free(chosen);
+    }
+  }
+  free(omega);
+  return awe;
+}
+
 /* ------------------------------------------------------------------ attention
  * Softmax attention of one query over an explicit list of key tokens, by the
  * definition: logits u_j = scale * (q . k_j); O = sum_j softmax(u)_j v_j and

@@ -325,6 +325,75 @@ def pin_bf16_rounding():
     assert np.array_equal(O.round_bf16(x), lib)
 
 
+def pin_prob_scores_where_readings_differ():
+    # A worked case where the probability-averaged score and the mean-logit score
+    # (reading R1) rank differently.  One-hot pooled keys make the logits the query
+    # entries: query 1 strongly prefers block 1, query 2 mildly prefers block 0.
+    # Mean logits (1, -5, 0) pick block 0; mean probabilities pick block 1.
+    q = np.array([[[0.0, 10.0, 0.0]], [[2.0, -20.0, 0.0]]])      # [Lq=2, H=1, d=3]
+    k = np.eye(3).reshape(3, 1, 1, 3)                            # 3 chunks of one 1-token block
+    logit = O.select(q, k, 1, 1, 2, 0, 0, 1.0)
+    assert logit["idx"].tolist() == [[[0]]], logit
+    kc = O.pool_keys(k, 1)
+    prob = O.select_prob(q, kc, 3, 1, 1, 2, 0, 0, 1.0, want_all_scores=True)
+    assert prob["idx"].tolist() == [[[1]]], prob
+    want = (sps.softmax(q[0, 0]) + sps.softmax(q[1, 0])) / 2     # library softmax per query
+    assert np.allclose(prob["all_scores"][0, 0], want, rtol=1e-14, atol=0), (prob["all_scores"], want)
+    assert prob["score"][0, 0, 0] == prob["all_scores"][0, 0, 1]
+
+
+def pin_prob_scores_vs_library():
+    # Library softmax of numpy logits over every pooled key, averaged over each
+    # group's rows (ragged last group), on random inputs; window excluded by AWE.
+    q, k, _ = _case(71, n=5, S=10, H=2, d=6, Lq=11)
+    B, G, scale = 4, 3, 0.6
+    Bpc = O.blocks_per_chunk(10, B)
+    kc = O.pool_keys(k, B)
+    got = O.select_prob(q, kc, 5, Bpc, 3, G, 1, 2, scale, want_all_scores=True)
+    assert got["awe"]
+    omega, _ = O.candidates(5, Bpc, 3, 1, 2)
+    for h in range(2):
+        p = sps.softmax(scale * (q[:, h] @ kc[h].T), axis=1)     # [Lq, N]
+        for r in range(-(-11 // G)):
+            want = p[r * G: min(r * G + G, 11)].mean(axis=0)
+            have = got["all_scores"][h, r]
+            assert np.all(np.isnan(have[~omega])), (h, r)
+            assert np.allclose(have[omega], want[omega], rtol=1e-12, atol=0), (h, r)
+            top = sorted(np.flatnonzero(omega), key=lambda b: (-want[b], b))[:3]
+            assert got["idx"][h, r].tolist() == sorted(top), (h, r)
+
+
+def pin_prob_scores_invariants():
+    # (a) Without exclusion each group's scores are a mean of probability vectors, so
+    #     they sum to 1 over the blocks.
+    # (b) Adding one vector c to every pooled key shifts each query's logits by a
+    #     constant, which its softmax removes: the scores do not change.
+    # (c) Softmax is monotone, so with one query per group, or groups of identical
+    #     rows, the top-K equals the mean-logit selection (reading R1).
+    q, k, _ = _case(72, n=4, S=9, H=3, d=5, Lq=10)
+    B, scale = 3, 0.7
+    Bpc = O.blocks_per_chunk(9, B)
+    kc = O.pool_keys(k, B)
+    a = O.select_prob(q, kc, 4, Bpc, 4, 3, 0, 0, scale, want_all_scores=True)
+    assert np.allclose(a["all_scores"].sum(axis=-1), 1.0, rtol=0, atol=1e-12), a["all_scores"].sum(axis=-1)
+    c = np.random.default_rng(73).standard_normal(5)
+    b = O.select_prob(q, kc + c, 4, Bpc, 4, 3, 0, 0, scale, want_all_scores=True)
+    assert np.allclose(a["all_scores"], b["all_scores"], rtol=1e-11, atol=1e-15)
+    assert np.array_equal(a["idx"], b["idx"])
+    resident = np.ones(4 * Bpc, dtype=bool)
+    resident[[1, 5]] = False
+    for E, T_out in ((0, 0), (1, 2), (2, 0)):
+        one = O.select_prob(q, kc, 4, Bpc, 3, 1, E, T_out, scale, resident=resident)
+        ref = O.select(q, k, B, 3, 1, E, T_out, scale, resident=resident)
+        assert np.array_equal(one["idx"], ref["idx"]) and np.array_equal(one["cnt"], ref["cnt"]), (E, T_out)
+        assert one["awe"] == ref["awe"]
+    G = 4
+    rep = np.repeat(q[::G], G, axis=0)[:10]                      # rows of each group identical
+    same = O.select_prob(rep, kc, 4, Bpc, 3, G, 1, 2, scale, resident=resident)
+    ref = O.select(rep, k, B, 3, G, 1, 2, scale, resident=resident)
+    assert np.array_equal(same["idx"], ref["idx"]) and np.array_equal(same["cnt"], ref["cnt"])
+
+
 def pin_gated_combine():
     # Eq. 1 with sigmoid gates: a saturated gate keeps or drops a branch exactly,
     # a zero logit weighs a branch by 1/2, and sigmoid(x) + sigmoid(-x) = 1.

@@ -47,6 +47,14 @@ MUTANTS = [
     ("softmax_not_normalised", "for (int j = 0; j < d; ++j) out[j] /= denom;", ";"),
     ("bf16_widened_wrong", "uint32_t bits = ((uint32_t)((const uint16_t*)base)[i]) << 16;",
      "uint32_t bits = ((uint32_t)((const uint16_t*)base)[i]) << 15;"),
+    ("prob_lse_missing_max", "double lse_q = mx + log(denom);", "double lse_q = log(denom);"),
+    ("prob_sum_not_mean", "double sb = sbar[b] / (double)(row1 - row0);", "double sb = sbar[b];"),
+    ("prob_averages_logits", "sbar[b] += exp(u[b] - lse_q);", "sbar[b] += u[b];"),
+    ("prob_softmax_over_omega_only", "for (int64_t b = 0; b < nb; ++b) denom += exp(u[b] - mx);",
+     "for (int64_t b = 0; b < nb; ++b) denom += omega[b] ? exp(u[b] - mx) : 0.0;"),
+    ("prob_group_rows_off_by_one", "row1 = row0 + G_q < Lq ? row0 + G_q : Lq;",
+     "row1 = row0 + G_q < Lq ? row0 + G_q + 1 : Lq;"),
+    ("prob_omega_ignored", "if (omega[b] != 0) {", "if (1) {"),
     ("union_counts_duplicates", "if (!mine[b]) { mine[b] = 1; ++count; }", "{ mine[b] = 1; ++count; }"),
 ]
 
