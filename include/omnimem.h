@@ -100,13 +100,24 @@ typedef struct {
  *                         T_out whole chunks lie outside the window, and (Eq. 2's
  *                         guard) at least K blocks do.
  *  scale                  score scale sigma > 0 (1/sqrt(d) in the workloads).
+ *  score_mode             what s[h][r][b] is (Sec. 3.1: the compression-attention
+ *                         score, averaged over the group by Eq. 3):
+ *                         OMNIMEM_SCORE_LOGIT (0, the default of a zeroed struct): the
+ *                           group-mean logit, scale * <qbar[h][r], kbar[h][b]>;
+ *                         OMNIMEM_SCORE_PROB (1): the group mean of each query's
+ *                           softmax probability of block b over every pooled key
+ *                           of the history (the compression branch's attention
+ *                           weights).  omnimem_select_compressed only.
  */
+enum { OMNIMEM_SCORE_LOGIT = 0, OMNIMEM_SCORE_PROB = 1 };
+
 typedef struct {
   int32_t top_k;
   int32_t group_size;
   int32_t window_chunks;
   int32_t awe_min_outside_chunks;
   float scale;
+  int32_t score_mode;
 } omnimem_select_params_t;
 
 /* Blocks per chunk, ceil(S/B); -1 if S < 1 or B < 1.  Host only, pure. */
@@ -142,6 +153,7 @@ size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq, 
  * awe_active: (host, out, may be NULL) the exclusion state used.
  * workspace: device scratch of at least omnimem_select_workspace_bytes(), 256-byte aligned.
  * Accumulation is fp32 on exact inputs; ranking is on fp32 scores.
+ * p->score_mode must be OMNIMEM_SCORE_LOGIT here (OMNIMEM_EINVAL otherwise).
  */
 omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                 const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt, float* score,
@@ -249,6 +261,15 @@ omnimem_status_t omnimem_compress_chunk(const omnimem_kv_cache_t* kv, int32_t ch
  * kv->page_table == NULL every block is a candidate, residency being handled by
  * the caller (omnimem_lru_require before the selection attention).  The workspace
  * is sized by omnimem_select_workspace_bytes(kv, lq, p).
+ *
+ * With p->score_mode == OMNIMEM_SCORE_PROB the scores are
+ *   u[h][i][b]  = scale * <q_i, kbar[h][b]>                 for all n*Bpc pooled keys
+ *   s[h][r][b]  = (1/|G_r|) sum over rows i of group r of exp(u[h][i][b] - LSE[h][i]),
+ *                 LSE[h][i] = ln sum over all b of exp(u[h][i][b])
+ * (the softmax includes the window and non-resident blocks; Omega restricts only
+ * the top-K), and `score` returns these group-mean probabilities.  The products
+ * run on bf16 MFMA with fp32 accumulation, kbar split into two bf16 pieces (and
+ * fp32 queries too), which keeps the logits to about 2^-16 relative of fp32.
  */
 omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const omnimem_cmp_cache_t* cc,
                                            const void* q, int32_t lq, const omnimem_select_params_t* p,

@@ -10,6 +10,8 @@ from .omnimem import (  # noqa: F401
     CompressedCache,
     LruOffload,
     OmniMemError,
+    SCORE_LOGIT,
+    SCORE_PROB,
     PagedKVCache,
     Selection,
     lib,

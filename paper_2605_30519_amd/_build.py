@@ -8,7 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 OBJ_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libomnimem.so")
-SOURCES = ["api.hip", "select.hip", "attention.hip", "union_gather.hip", "fuse.hip", "offload.hip"]
+SOURCES = ["api.hip", "select.hip", "prob.hip", "attention.hip", "union_gather.hip", "fuse.hip", "offload.hip"]
 HEADERS = ["device_common.h", "launch.h"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

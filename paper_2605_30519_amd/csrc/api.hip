@@ -81,7 +81,7 @@ omnimem_status_t resolve_select(const omnimem_kv_cache_t* kv, int32_t lq, const 
   if (st != OMNIMEM_OK) return st;
   if (p == nullptr || lq < 0) return OMNIMEM_EINVAL;
   if (p->top_k < 1 || p->group_size < 1 || p->window_chunks < 0 || p->awe_min_outside_chunks < 0 ||
-      !good_scale(p->scale))
+      !good_scale(p->scale) || (p->score_mode != OMNIMEM_SCORE_LOGIT && p->score_mode != OMNIMEM_SCORE_PROB))
     return OMNIMEM_EINVAL;
   const int awe = omnimem_awe_active(g.n, p->window_chunks, p->awe_min_outside_chunks, p->top_k, g.Bpc);
   if (lq == 0) {
@@ -90,7 +90,7 @@ omnimem_status_t resolve_select(const omnimem_kv_cache_t* kv, int32_t lq, const 
     return OMNIMEM_OK;
   }
   plan = omnimem::plan_select(g, lq, p->top_k, p->group_size, p->window_chunks, p->awe_min_outside_chunks, p->scale,
-                              awe);
+                              awe, p->score_mode);
   return OMNIMEM_OK;
 }
 
@@ -113,6 +113,7 @@ OMNIMEM_API omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const 
   omnimem::SelectPlan plan;
   omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
   if (st != OMNIMEM_OK) return st;
+  if (p->score_mode != OMNIMEM_SCORE_LOGIT) return OMNIMEM_EINVAL;  // probabilities need the pooled history
   if (awe_active) *awe_active = plan.awe;
   if (lq == 0) return OMNIMEM_OK;
   if (q == nullptr || idx == nullptr || cnt == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;

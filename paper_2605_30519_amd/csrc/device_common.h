@@ -35,6 +35,16 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float x) {
   return static_cast<uint16_t>((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
 }
 
+// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
+// -0 is folded onto +0 first so that equal scores compare equal.  Candidate keys
+// are forced >= 1 so that 0 can mark "not a candidate".
+__device__ __forceinline__ uint32_t score_key(float s) {
+  s = s + 0.0f;
+  const uint32_t u = __float_as_uint(s);
+  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return k == 0u ? 1u : k;
+}
+
 // 16-byte vector load widened to fp32: 8 bf16 or 4 fp32 values.
 template <typename T>
 struct Vec16;

@@ -120,16 +120,6 @@ __device__ __forceinline__ void proxy_cols(const float* __restrict__ partial, in
 }
 
 // -------------------------------------------------------------- score keys
-// Order-preserving map of an fp32 score to uint32 (larger score -> larger key).
-// -0 is folded onto +0 first so that equal scores compare equal.  Candidate keys
-// are forced >= 1 so that 0 can mark "not a candidate".
-__device__ __forceinline__ uint32_t score_key(float s) {
-  s = s + 0.0f;
-  const uint32_t u = __float_as_uint(s);
-  const uint32_t k = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-  return k == 0u ? 1u : k;
-}
-
 // Inverse of score_key on candidate keys (returns the score with -0 as +0).
 __device__ __forceinline__ float key_score(uint32_t k) {
   return __uint_as_float((k & 0x80000000u) ? (k & 0x7fffffffu) : ~k);
@@ -975,9 +965,11 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
 
 }  // namespace
 
-SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe) {
+SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe,
+                       int score_mode) {
   (void)T_out;
   SelectPlan p{};
+  p.score_mode = score_mode;
   p.lq = lq;
   p.G = G;
   p.R = (lq + G - 1) / G;
@@ -995,6 +987,23 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
   if (!p.inline_scores) off = align256(off + static_cast<size_t>(g.H) * g.nb * g.D * sizeof(float));
   p.off_keys = off;
   off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
+  p.off_part = off;
+  if (score_mode == 1) {
+    constexpr int kSliceRows = 64;
+    p.prob_multi = G <= kSliceRows / 2;
+    if (p.prob_multi) {
+      p.prob_gps = kSliceRows / G;
+      p.prob_spg = 1;
+      p.prob_slices = (p.R + p.prob_gps - 1) / p.prob_gps;
+      p.prob_nseg = p.R;
+    } else {
+      p.prob_gps = 1;
+      p.prob_spg = (rows + kSliceRows - 1) / kSliceRows;
+      p.prob_slices = p.R * p.prob_spg;
+      p.prob_nseg = p.prob_slices;
+    }
+    off = align256(off + static_cast<size_t>(g.H) * p.prob_nseg * g.nb * sizeof(float));
+  }
   p.total = off;
   return p;
 }
@@ -1031,6 +1040,15 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
   float* qpart = reinterpret_cast<float*>(ws + p.off_qpart);
   uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
   const int nbp = (g.nb + 3) / 4 * 4;
+  if (p.score_mode == 1) {
+    if (g.nb > 0) {
+      float* part = reinterpret_cast<float*>(ws + p.off_part);
+      const hipError_t e = launch_prob_keys(g, p, q, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), part, keys, nbp,
+                                            stream);
+      if (e != hipSuccess) return e;
+    }
+    return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
+  }
   launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
   if (g.nb > 0) launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);

@@ -55,7 +55,12 @@ class omnimem_select_params_t(ctypes.Structure):
         ("window_chunks", ctypes.c_int32),
         ("awe_min_outside_chunks", ctypes.c_int32),
         ("scale", ctypes.c_float),
+        ("score_mode", ctypes.c_int32),
     ]
+
+
+SCORE_LOGIT = 0  # the group-mean logit (the default)
+SCORE_PROB = 1   # the group mean of each query's softmax probability (compressed history only)
 
 
 class omnimem_lru_stats_t(ctypes.Structure):
@@ -261,8 +266,9 @@ def omnimem_status_string(status: int) -> str:
     return lib().omnimem_status_string(status).decode()
 
 
-def select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, scale) -> omnimem_select_params_t:
-    return omnimem_select_params_t(top_k, group_size, window_chunks, awe_min_outside_chunks, scale)
+def select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, scale,
+                  score_mode: int = SCORE_LOGIT) -> omnimem_select_params_t:
+    return omnimem_select_params_t(top_k, group_size, window_chunks, awe_min_outside_chunks, scale, score_mode)
 
 
 def omnimem_select_workspace_bytes(cache: PagedKVCache, lq: int, params: omnimem_select_params_t,
@@ -414,11 +420,15 @@ def omnimem_select_compressed(cache: PagedKVCache, cc: CompressedCache, q: torch
                               window_chunks: int, awe_min_outside_chunks: int, scale: Optional[float] = None, *,
                               num_chunks: Optional[int] = None, want_score: bool = True,
                               workspace: Optional[torch.Tensor] = None, out: Optional[Selection] = None,
-                              all_candidates: bool = False, stream=None) -> Selection:
+                              all_candidates: bool = False, score_mode: int = SCORE_LOGIT,
+                              stream=None) -> Selection:
     """all_candidates=True ignores residency (NULL page table): every block of the
-    history is a candidate, as when an LRU hot cache reloads what is selected."""
+    history is a candidate, as when an LRU hot cache reloads what is selected.
+    score_mode=SCORE_PROB ranks by group-mean softmax probabilities over the pooled
+    keys instead of group-mean logits."""
     lq, H, d = (int(s) for s in q.shape)
-    params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
+    params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale),
+                           score_mode)
     desc = cache.descriptor(num_chunks, with_table=not all_candidates)
     cdesc = cc.descriptor()
     R = -(-lq // group_size)
