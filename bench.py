@@ -451,6 +451,31 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
         three_branch(i, evs3[i])
     torch.cuda.synchronize()
     med3 = lambda a, b: float(np.median([e[a].elapsed_time(e[b]) for e in evs3]))
+
+    # selection by probability-averaged scores (score_mode SCORE_PROB), the workload's
+    # groups and the paper's G = 15 with top-4
+    from paper_2605_30519_amd import SCORE_PROB
+    q0, c0 = layers[0]
+    prob = {}
+    for name, G, Kp in (("workload_groups", w.group_size, K), ("g15_top4", 15, 4)):
+        pp = select_params(Kp, G, w.window_chunks, w.awe_min_outside_chunks, w.scale, SCORE_PROB)
+        wsp = workspace_tensor(omnimem_select_workspace_bytes(c0, w.query_tokens, pp), dev)
+        sp = None
+        for _ in range(20):
+            sp = omnimem_select_compressed(c0, ccs[0], q0, Kp, G, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                                           workspace=wsp, out=sp, want_score=False, score_mode=SCORE_PROB)
+        e[0].record()
+        for _ in range(50):
+            omnimem_select_compressed(c0, ccs[0], q0, Kp, G, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                                      workspace=wsp, out=sp, want_score=False, score_mode=SCORE_PROB)
+        e[1].record()
+        torch.cuda.synchronize()
+        pms = e[0].elapsed_time(e[1]) / 50
+        logit_fl = 2.0 * w.query_tokens * n * w.blocks_per_chunk * w.head_dim * w.heads
+        prob[name] = {"group_size": G, "top_k": Kp, "select_ms": round(pms, 4),
+                      "logit_tflops": round(logit_fl / (pms * 1e-3) / 1e12, 2),
+                      "mfma_tflops": round(4 * logit_fl / (pms * 1e-3) / 1e12, 2)}
+        del wsp
     return {"step": "pool the newest chunk + select from the pooled keys + sparse attention",
             "ms_per_chunk_layer": round(ms, 4),
             "effective_tflops": round(float(np.mean(flops)) / (ms * 1e-3) / 1e12, 2),
@@ -460,7 +485,8 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
             "three_branch": {"step": "the compressed chunk step + CMP + SWA over the window + gated fusion (Eq. 1)",
                              "ms_per_chunk_layer": round(tb_ms, 4), "selection_step_ms": round(med3(0, 1), 4),
                              "cmp_attn_ms": round(med3(1, 2), 4), "swa_attn_ms": round(med3(2, 3), 4),
-                             "gated_combine_ms": round(med3(3, 4), 4)}}
+                             "gated_combine_ms": round(med3(3, 4), 4)},
+            "prob_scores": prob}
 
 
 def small_group_measure(dev, reps=50):

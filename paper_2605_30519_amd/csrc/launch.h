@@ -28,14 +28,15 @@ struct SelectPlan {
   float scale;
   int qsplit;           // row splits per group in the proxy-query reduction
   bool inline_scores;   // scores computed inside the pooling kernel (small R)
-  // probability-averaged scores (score_mode 1): query slices of at most 64 rows,
+  // probability-averaged scores (score_mode 1): query slices of at most 128 rows,
   // either whole groups (multi: gps groups per slice) or parts of one group (spg
-  // slices per group); one partial row of nb sums per (head, segment)
+  // slices per group); one partial row of nb sums per (head, segment), and the
+  // pooled keys split into bf16 pieces, 64-key tiles
   int score_mode;
   bool prob_multi;
   int prob_gps, prob_spg, prob_slices, prob_nseg;
   // workspace carve-up (byte offsets)
-  size_t off_qpart, off_kbar, off_keys, off_part, total;
+  size_t off_qpart, off_kbar, off_keys, off_part, off_ksplit, total;
 };
 
 constexpr int kQRowsPerSplit = 512;
@@ -47,7 +48,8 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
 // Probability-averaged score keys (score_mode 1) from pooled keys kbar
 // [H][kbar_stride][D] fp32: order-preserving keys [H][R][nbp], 0 outside Omega.
 hipError_t launch_prob_keys(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                            int64_t kbar_stride, float* part, uint32_t* keys, int nbp, hipStream_t stream);
+                            int64_t kbar_stride, float* part, void* ksplit, uint32_t* keys, int nbp,
+                            hipStream_t stream);
 
 hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
                          float* score, void* workspace, hipStream_t stream);

@@ -5,15 +5,19 @@
 // with LSE_i the log-sum-exp of row i over all pooled keys, so that sbar is the
 // group mean of the compression branch's attention weights.
 //
-// k_prob_partial: one workgroup per (head, slice of at most 64 query rows).  It walks
-// the pooled keys in tiles of 64 twice: first for each row's LSE (online, exp2
-// domain), then for exp(u - LSE) summed over the rows of each group segment in the
-// slice.  The products are bf16 MFMA (32x32x16) with fp32 accumulation; each fp32
-// pooled key is split into two bf16 pieces (hi + lo, exact to about 2^-17), bf16
-// queries are exact, fp32 queries are split the same way (hi*hi + lo*hi + hi*lo).
-// The first pass forms S^T = K Q^T (a lane owns one query row: the row's max and sum
-// stay in the lane), the second S = Q K^T (a lane owns one pooled key: the sum over
-// a group's rows is a sum over the lane's accumulator rows).
+// k_split_keys: the fp32 pooled keys, split once per call into two bf16 pieces
+// (kbar ~= hi + lo, exact to about 2^-17 relative), stored tile by tile (64 keys,
+// hi then lo) so that a workgroup stages a tile with plain coalesced 16-byte loads.
+// k_prob_partial: one workgroup per (head, slice of at most 128 query rows), the
+// slices of one head contiguous on one XCD so that its L2 holds that head's keys.
+// Each wave owns 64 rows (two 32-row MFMA tiles that share every key fragment) and
+// 32 keys of each tile.  It walks the tiles twice: first for each row's LSE
+// (online, exp2 domain, the hardware exp2: probabilities below 2^-126 count as 0),
+// then for exp(u - LSE) summed over the rows of each group segment of the slice.  The products are bf16 MFMA (32x32x16) with fp32
+// accumulation: hi*q + lo*q for bf16 queries (exact), plus hi*q_lo for fp32 queries
+// split the same way.  The first pass forms S^T = K Q^T (a lane owns one query
+// row: its max and sum stay in the lane), the second S = Q K^T (a lane owns one
+// key: the sum over a group's rows is a sum over the lane's accumulator rows).
 // k_prob_merge: sums a group's slices in order, divides by the group's row count and
 // writes the order-preserving keys that k_topk ranks (0 outside Omega).
 #include <math.h>
@@ -25,8 +29,8 @@ namespace omnimem {
 namespace {
 
 constexpr int kPThreads = 256;
-constexpr int kPRows = 64;    // query rows per slice (two 32-row MFMA tiles)
-constexpr int kPKeys = 64;    // pooled keys per tile (two 32-key MFMA tiles)
+constexpr int kPRows = 128;   // query rows per slice: 64 per wave, two waves deep
+constexpr int kPKeys = 64;    // pooled keys per tile: 32 per wave, two waves wide
 constexpr int kPRedStride = kPKeys + 1;
 constexpr float kLog2eP = 1.4426950408889634f;
 
@@ -44,23 +48,24 @@ struct QueryPieces<float> {
 struct ProbArgs {
   const void* q;
   int lq, H, G, R;
-  const float* kbar;
-  int64_t kbar_stride;  // pooled keys per head in kbar
-  int nb;
+  const uint4* ksplit;  // [H][ntiles][2][64][D] bf16 pieces of the pooled keys
+  int ntiles, nb;
   float scale;
   int multi;            // 1: a slice holds gps whole groups; 0: a slice is part of one group
-  int gps, spg, nseg;
+  int gps, spg, slices, nseg;
   float* part;          // [H][nseg][nb]
 };
 
-__device__ __forceinline__ void lse_merge(float& m, float& l, float m2, float l2) {
+// Merges two (max, sum) states of a log-sum-exp; maxima in raw units, sums of
+// exp2(c2 * (x - max)).
+__device__ __forceinline__ void lse_merge(float& m, float& l, float m2, float l2, float c2) {
   const float mx = fmaxf(m, m2);
   if (mx == -INFINITY) {
     m = mx;
     l = 0.f;
     return;
   }
-  l = l * exp2f(m - mx) + l2 * exp2f(m2 - mx);
+  l = l * exp2f(c2 * (m - mx)) + l2 * exp2f(c2 * (m2 - mx));
   m = mx;
 }
 
@@ -79,19 +84,73 @@ __device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo
   lo = make_uint4(l[0], l[1], l[2], l[3]);
 }
 
+// One workgroup per (tile of 64 keys, head); keys past nb are zero.
+template <int D>
+__global__ __launch_bounds__(kPThreads) void k_split_keys(const float* __restrict__ kbar, int64_t kbar_stride, int nb,
+                                                          int ntiles, uint4* __restrict__ ksplit) {
+  constexpr int CH = D / 8;
+  const int t = blockIdx.x, h = blockIdx.y;
+  uint4* dst = ksplit + (static_cast<int64_t>(h) * ntiles + t) * (2 * kPKeys * CH);
+  for (int e = threadIdx.x; e < kPKeys * CH; e += kPThreads) {
+    const int row = e / CH, c = e % CH, b = t * kPKeys + row;
+    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (b < nb) {
+      const float* src = kbar + (static_cast<int64_t>(h) * kbar_stride + b) * D + 8 * c;
+      const float4 x0 = *reinterpret_cast<const float4*>(src), x1 = *reinterpret_cast<const float4*>(src + 4);
+      x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w;
+      x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
+    }
+    uint4 hi, lo;
+    split8(x, hi, lo);
+    dst[e] = hi;
+    dst[kPKeys * CH + e] = lo;
+  }
+}
+
+// Split-key tiles: 16-byte chunk e of tile t (piece e / (64 CH), key row, chunk c)
+// is fetched by thread e mod 256 and goes to chunk c ^ (row mod CH) of its LDS
+// row, so that the fragment reads of 8 consecutive rows hit 8 different chunk
+// columns.
+template <int D>
+__device__ __forceinline__ void fetch_tile(const ProbArgs& a, int h, int t, u32x4 (&kv)[2 * kPKeys * D / 8 / kPThreads]) {
+  constexpr int TILE_CHUNKS = 2 * kPKeys * D / 8;
+  const u32x4* src = reinterpret_cast<const u32x4*>(a.ksplit) + (static_cast<int64_t>(h) * a.ntiles + t) * TILE_CHUNKS;
+#pragma unroll
+  for (int u = 0; u < TILE_CHUNKS / kPThreads; ++u) kv[u] = src[threadIdx.x + u * kPThreads];
+}
+
+template <int D>
+__device__ __forceinline__ void stage_tile(const u32x4 (&kv)[2 * kPKeys * D / 8 / kPThreads], uint16_t* ktile) {
+  constexpr int CH = D / 8;
+#pragma unroll
+  for (int u = 0; u < 2 * kPKeys * CH / kPThreads; ++u) {
+    const int e = threadIdx.x + u * kPThreads, piece = e / (kPKeys * CH), rem = e % (kPKeys * CH);
+    const int row = rem / CH, c = rem % CH;
+    *reinterpret_cast<u32x4*>(ktile + piece * kPKeys * D + row * D + 8 * (c ^ (row % CH))) = kv[u];
+  }
+}
+
+// The 8 bf16 of key row krow, d = 16 kk + 8 half + 0..7, of one piece (0 hi, 1 lo).
+template <int D>
+__device__ __forceinline__ bf16x8 key_frag(const uint16_t* ktile, int piece, int kk, int krow, int half) {
+  constexpr int CH = D / 8;
+  const int pc = (2 * kk + half) ^ (krow % CH);
+  return *reinterpret_cast<const bf16x8*>(ktile + piece * kPKeys * D + krow * D + 8 * pc);
+}
+
 template <typename T, int D>
-__global__ __launch_bounds__(kPThreads) void k_prob_partial(ProbArgs a) {
-  constexpr int KK = D / 16;            // MFMA steps over d
-  constexpr int CH = D / 8;             // 16-byte bf16 chunks per pooled key
-  constexpr int CPT = CH / 4;           // chunks staged per thread (4 threads per key)
+__global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
+  constexpr int KK = D / 16;                      // MFMA steps over d
+  constexpr int CH = D / 8;                       // 16-byte chunks per key row
+  constexpr int LPT = 2 * kPKeys * CH / kPThreads;  // 16-byte loads per thread per tile
   constexpr int QP = QueryPieces<T>::N;
-  __shared__ __align__(16) uint16_t khi[kPKeys * D];
-  __shared__ __align__(16) uint16_t klo[kPKeys * D];
+  __shared__ __align__(16) uint16_t ktile[2 * kPKeys * D];
   __shared__ float red[kPRows * kPRedStride];
   __shared__ float mrg_m[2][kPRows], mrg_l[2][kPRows];
   __shared__ float lse2[kPRows];
 
-  const int h = blockIdx.y, slice = blockIdx.x;
+  const int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
+  const int h = id / a.slices, slice = id % a.slices;
   int row0, rows, seg0;
   if (a.multi) {
     seg0 = slice * a.gps;
@@ -106,13 +165,15 @@ __global__ __launch_bounds__(kPThreads) void k_prob_partial(ProbArgs a) {
   if (rows <= 0) return;  // workgroup-uniform, before any barrier
 
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave, half = lane / 32;
-  const int rq = wave & 1, kq = wave >> 1;  // this wave's 32 query rows and 32 pooled keys of a tile
-  const int qrow = 32 * rq + lane % 32;     // slice-local query row this lane supplies
-  const int krow = 32 * kq + lane % 32;     // tile-local pooled key this lane supplies
+  const int rh = wave & 1, kq = wave >> 1;  // rows [64 rh, +64) of the slice, keys [32 kq, +32) of a tile
+  const int krow = 32 * kq + lane % 32;     // tile-local key this lane supplies
 
-  // query operand: row qrow, d = 16 kk + 8 half + 0..7 (zero past the slice)
-  bf16x8 qh[KK], ql[KK];
-  {
+  // query operands of the wave's two 32-row tiles: row 64 rh + 32 s + lane%32,
+  // d = 16 kk + 8 half + 0..7 (zero past the slice)
+  bf16x8 qh[2][KK], ql[2][KK];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    const int qrow = 64 * rh + 32 * s + lane % 32;
     const bool live = qrow < rows;
     const int64_t base = (static_cast<int64_t>(row0 + qrow) * a.H + h) * D;
 #pragma unroll
@@ -128,130 +189,124 @@ __global__ __launch_bounds__(kPThreads) void k_prob_partial(ProbArgs a) {
           split8(x, hi, lo);
         }
       }
-      qh[kk] = __builtin_bit_cast(bf16x8, hi);
-      ql[kk] = __builtin_bit_cast(bf16x8, lo);
+      qh[s][kk] = __builtin_bit_cast(bf16x8, hi);
+      ql[s][kk] = __builtin_bit_cast(bf16x8, lo);
     }
   }
 
-  // pooled-key tile: thread tid stages key tid/4, dimensions [(tid%4) D/4, +D/4)
-  float4 kv[2 * CPT];
-  auto fetch = [&](int b0) {
-    const int b = b0 + tid / 4;
-    const float* src = a.kbar + (static_cast<int64_t>(h) * a.kbar_stride + b) * D + (tid % 4) * (D / 4);
-#pragma unroll
-    for (int u = 0; u < 2 * CPT; ++u)
-      kv[u] = b < a.nb ? *reinterpret_cast<const float4*>(src + 4 * u) : make_float4(0.f, 0.f, 0.f, 0.f);
-  };
-  // chunk c of key row r sits at chunk c ^ (r mod CH): the fragment reads of 8
-  // consecutive rows hit 8 different chunk columns
-  auto stage = [&]() {
-    const int r = tid / 4;
-#pragma unroll
-    for (int cc = 0; cc < CPT; ++cc) {
-      const float x[8] = {kv[2 * cc].x,     kv[2 * cc].y,     kv[2 * cc].z,     kv[2 * cc].w,
-                          kv[2 * cc + 1].x, kv[2 * cc + 1].y, kv[2 * cc + 1].z, kv[2 * cc + 1].w};
-      uint4 hi, lo;
-      split8(x, hi, lo);
-      const int c = (tid % 4) * CPT + cc, pc = c ^ (r % CH);
-      *reinterpret_cast<uint4*>(khi + r * D + 8 * pc) = hi;
-      *reinterpret_cast<uint4*>(klo + r * D + 8 * pc) = lo;
-    }
-  };
-  auto frag = [&](const uint16_t* base, int kk) {
-    const int pc = (2 * kk + half) ^ (krow % CH);
-    return *reinterpret_cast<const bf16x8*>(base + krow * D + 8 * pc);
-  };
-
+  u32x4 kv[LPT];
   const float c2 = a.scale * kLog2eP;
-  const int ntiles = (a.nb + kPKeys - 1) / kPKeys;
 
   // ---- pass 1: LSE of every row over all pooled keys (S^T = K Q^T, lane = row)
-  float m_run = -INFINITY, l_run = 0.f;
-  fetch(0);
-  for (int t = 0; t < ntiles; ++t) {
+  float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+  fetch_tile<D>(a, h, 0, kv);
+  for (int t = 0; t < a.ntiles; ++t) {
     __syncthreads();
-    stage();
+    stage_tile<D>(kv, ktile);
     __syncthreads();
-    if (t + 1 < ntiles) fetch((t + 1) * kPKeys);
-    f32x16 acc = {};
+    if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    f32x16 acc[2] = {};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8 kh = frag(khi, kk), kl = frag(klo, kk);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, qh[kk], acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, qh[kk], acc, 0, 0, 0);
-      if constexpr (QP == 2) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, ql[kk], acc, 0, 0, 0);
-    }
-    // acc[i]: pooled key t*64 + 32 kq + 8 (i/4) + 4 half + i%4 against row qrow
-    float x[16], mx = -INFINITY;
+      const bf16x8 kh = key_frag<D>(ktile, 0, kk, krow, half), kl = key_frag<D>(ktile, 1, kk, krow, half);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int b = t * kPKeys + 32 * kq + 8 * (i / 4) + 4 * half + i % 4;
-      x[i] = b < a.nb ? c2 * acc[i] : -INFINITY;
-      mx = fmaxf(mx, x[i]);
+      for (int s = 0; s < 2; ++s) {
+        acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, qh[s][kk], acc[s], 0, 0, 0);
+        acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kl, qh[s][kk], acc[s], 0, 0, 0);
+        if constexpr (QP == 2) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, ql[s][kk], acc[s], 0, 0, 0);
+      }
     }
-    if (mx > -INFINITY) {
-      const float mnew = fmaxf(m_run, mx);
-      float s = 0.f;
+    // acc[s][i]: key t*64 + 32 kq + 8 (i/4) + 4 half + i%4 against row 64 rh + 32 s + lane%32;
+    // the running max is kept in raw (unscaled) units, scale > 0
+    if (t * kPKeys + kPKeys > a.nb) {  // workgroup-uniform: only the last tile is partial
 #pragma unroll
-      for (int i = 0; i < 16; ++i) s += exp2f(x[i] - mnew);
-      l_run = l_run * exp2f(m_run - mnew) + s;
-      m_run = mnew;
+      for (int i = 0; i < 16; ++i) {
+        const int b = t * kPKeys + 32 * kq + 8 * (i / 4) + 4 * half + i % 4;
+        if (b >= a.nb) acc[0][i] = acc[1][i] = -INFINITY;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      float mx = acc[s][0];
+#pragma unroll
+      for (int i = 1; i < 16; ++i) mx = fmaxf(mx, acc[s][i]);
+      if (mx > -INFINITY) {
+        const float mnew = fmaxf(m_run[s], mx), off = -c2 * mnew;
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) sum += __builtin_amdgcn_exp2f(fmaf(acc[s][i], c2, off));
+        l_run[s] = l_run[s] * __builtin_amdgcn_exp2f(c2 * (m_run[s] - mnew)) + sum;
+        m_run[s] = mnew;
+      }
     }
   }
-  lse_merge(m_run, l_run, __shfl_xor(m_run, 32), __shfl_xor(l_run, 32));
-  if (half == 0) {
-    mrg_m[kq][qrow] = m_run;
-    mrg_l[kq][qrow] = l_run;
+#pragma unroll
+  for (int s = 0; s < 2; ++s) {
+    lse_merge(m_run[s], l_run[s], __shfl_xor(m_run[s], 32), __shfl_xor(l_run[s], 32), c2);
+    if (half == 0) {
+      mrg_m[kq][64 * rh + 32 * s + lane % 32] = m_run[s];
+      mrg_l[kq][64 * rh + 32 * s + lane % 32] = l_run[s];
+    }
   }
   __syncthreads();
   if (tid < kPRows) {
     float m = mrg_m[0][tid], l = mrg_l[0][tid];
-    lse_merge(m, l, mrg_m[1][tid], mrg_l[1][tid]);
-    lse2[tid] = tid < rows ? m + log2f(l) : INFINITY;  // rows past the slice weigh 0
+    lse_merge(m, l, mrg_m[1][tid], mrg_l[1][tid], c2);
+    lse2[tid] = tid < rows ? c2 * m + log2f(l) : INFINITY;  // log2 domain; rows past the slice weigh 0
   }
   __syncthreads();
 
   // ---- pass 2: exp(u - LSE) summed over each segment's rows (S = Q K^T, lane = key)
-  float lr[16];
+  float lr[2][16];
 #pragma unroll
-  for (int i = 0; i < 16; ++i) lr[i] = lse2[32 * rq + 8 * (i / 4) + 4 * half + i % 4];
+  for (int s = 0; s < 2; ++s)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) lr[s][i] = lse2[64 * rh + 32 * s + 8 * (i / 4) + 4 * half + i % 4];
   const int ngroups = a.multi ? min(a.gps, a.R - seg0) : 1;
-  fetch(0);
-  for (int t = 0; t < ntiles; ++t) {
+  fetch_tile<D>(a, h, 0, kv);
+  for (int t = 0; t < a.ntiles; ++t) {
     __syncthreads();
-    stage();
+    stage_tile<D>(kv, ktile);
     __syncthreads();
-    if (t + 1 < ntiles) fetch((t + 1) * kPKeys);
-    f32x16 acc = {};
+    if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    f32x16 acc[2] = {};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8 kh = frag(khi, kk), kl = frag(klo, kk);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qh[kk], kh, acc, 0, 0, 0);
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qh[kk], kl, acc, 0, 0, 0);
-      if constexpr (QP == 2) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ql[kk], kh, acc, 0, 0, 0);
+      const bf16x8 kh = key_frag<D>(ktile, 0, kk, krow, half), kl = key_frag<D>(ktile, 1, kk, krow, half);
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qh[s][kk], kh, acc[s], 0, 0, 0);
+        acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qh[s][kk], kl, acc[s], 0, 0, 0);
+        if constexpr (QP == 2) acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ql[s][kk], kh, acc[s], 0, 0, 0);
+      }
     }
-    // acc[i]: row 32 rq + 8 (i/4) + 4 half + i%4 against pooled key t*64 + krow
+    // acc[s][i]: row 64 rh + 32 s + 8 (i/4) + 4 half + i%4 against key t*64 + krow
     const int b0 = t * kPKeys;
     if (!a.multi) {
       float v = 0.f;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) v += exp2f(c2 * acc[i] - lr[i]);
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) v += __builtin_amdgcn_exp2f(fmaf(acc[s][i], c2, -lr[s][i]));
       v += __shfl_xor(v, 32);
-      if (half == 0) red[rq * kPKeys + krow] = v;
+      if (half == 0) red[rh * kPKeys + krow] = v;
       __syncthreads();
       if (tid < kPKeys && b0 + tid < a.nb)
         a.part[(static_cast<int64_t>(h) * a.nseg + seg0) * a.nb + b0 + tid] = red[tid] + red[kPKeys + tid];
     } else {
 #pragma unroll
-      for (int i = 0; i < 16; ++i)
-        red[(32 * rq + 8 * (i / 4) + 4 * half + i % 4) * kPRedStride + krow] = exp2f(c2 * acc[i] - lr[i]);
+      for (int s = 0; s < 2; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          red[(64 * rh + 32 * s + 8 * (i / 4) + 4 * half + i % 4) * kPRedStride + krow] =
+              __builtin_amdgcn_exp2f(fmaf(acc[s][i], c2, -lr[s][i]));
       __syncthreads();
       for (int e = tid; e < ngroups * kPKeys; e += kPThreads) {
         const int j = e / kPKeys, col = e % kPKeys;
         const int r_end = min(j * a.G + a.G, rows);
-        float s = 0.f;
-        for (int r = j * a.G; r < r_end; ++r) s += red[r * kPRedStride + col];
-        if (b0 + col < a.nb) a.part[(static_cast<int64_t>(h) * a.nseg + seg0 + j) * a.nb + b0 + col] = s;
+        float sum = 0.f;
+        for (int r = j * a.G; r < r_end; ++r) sum += red[r * kPRedStride + col];
+        if (b0 + col < a.nb) a.part[(static_cast<int64_t>(h) * a.nseg + seg0 + j) * a.nb + b0 + col] = sum;
       }
     }
   }
@@ -280,23 +335,28 @@ __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restric
 
 template <typename T, int D>
 hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                             int64_t kbar_stride, float* part, uint32_t* keys, int nbp, hipStream_t stream) {
+                             int64_t kbar_stride, float* part, uint4* ksplit, uint32_t* keys, int nbp,
+                             hipStream_t stream) {
+  const int ntiles = (g.nb + kPKeys - 1) / kPKeys;
+  hipLaunchKernelGGL((k_split_keys<D>), dim3(ntiles, g.H), dim3(kPThreads), 0, stream, kbar, kbar_stride, g.nb,
+                     ntiles, ksplit);
   ProbArgs a;
   a.q = q;
   a.lq = p.lq;
   a.H = g.H;
   a.G = p.G;
   a.R = p.R;
-  a.kbar = kbar;
-  a.kbar_stride = kbar_stride;
+  a.ksplit = ksplit;
+  a.ntiles = ntiles;
   a.nb = g.nb;
   a.scale = p.scale;
   a.multi = p.prob_multi ? 1 : 0;
   a.gps = p.prob_gps;
   a.spg = p.prob_spg;
+  a.slices = p.prob_slices;
   a.nseg = p.prob_nseg;
   a.part = part;
-  hipLaunchKernelGGL((k_prob_partial<T, D>), dim3(p.prob_slices, g.H), dim3(kPThreads), 0, stream, a);
+  hipLaunchKernelGGL((k_prob_partial<T, D>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
   const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
   hipLaunchKernelGGL(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R,
                      a.multi, p.prob_spg, g.page_table, g.num_pages, p.first_excluded, keys);
@@ -306,13 +366,15 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
 }  // namespace
 
 hipError_t launch_prob_keys(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                            int64_t kbar_stride, float* part, uint32_t* keys, int nbp, hipStream_t stream) {
+                            int64_t kbar_stride, float* part, void* ksplit, uint32_t* keys, int nbp,
+                            hipStream_t stream) {
+  uint4* ks = static_cast<uint4*>(ksplit);
   if (g.dtype == 0) {
-    if (g.D == 128) return launch_prob_typed<uint16_t, 128>(g, p, q, kbar, kbar_stride, part, keys, nbp, stream);
-    return launch_prob_typed<uint16_t, 64>(g, p, q, kbar, kbar_stride, part, keys, nbp, stream);
+    if (g.D == 128) return launch_prob_typed<uint16_t, 128>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
+    return launch_prob_typed<uint16_t, 64>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
   }
-  if (g.D == 128) return launch_prob_typed<float, 128>(g, p, q, kbar, kbar_stride, part, keys, nbp, stream);
-  return launch_prob_typed<float, 64>(g, p, q, kbar, kbar_stride, part, keys, nbp, stream);
+  if (g.D == 128) return launch_prob_typed<float, 128>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
+  return launch_prob_typed<float, 64>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
 }
 
 }  // namespace omnimem

@@ -989,7 +989,7 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
   off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
   p.off_part = off;
   if (score_mode == 1) {
-    constexpr int kSliceRows = 64;
+    constexpr int kSliceRows = 128;
     p.prob_multi = G <= kSliceRows / 2;
     if (p.prob_multi) {
       p.prob_gps = kSliceRows / G;
@@ -1003,6 +1003,8 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
       p.prob_nseg = p.prob_slices;
     }
     off = align256(off + static_cast<size_t>(g.H) * p.prob_nseg * g.nb * sizeof(float));
+    p.off_ksplit = off;
+    off = align256(off + static_cast<size_t>(g.H) * ((g.nb + 63) / 64) * 2 * 64 * g.D * sizeof(uint16_t));
   }
   p.total = off;
   return p;
@@ -1043,8 +1045,8 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
   if (p.score_mode == 1) {
     if (g.nb > 0) {
       float* part = reinterpret_cast<float*>(ws + p.off_part);
-      const hipError_t e = launch_prob_keys(g, p, q, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), part, keys, nbp,
-                                            stream);
+      const hipError_t e = launch_prob_keys(g, p, q, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), part,
+                                            ws + p.off_ksplit, keys, nbp, stream);
       if (e != hipSuccess) return e;
     }
     return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);

@@ -10,10 +10,11 @@ an oracle near-tie; the scores of the selected blocks must match to 1e-4 relativ
 (the kernel's logits carry about 2^-16 relative error from its two-piece bf16
 split of the pooled keys, fp32 accumulation and the hardware exp2/log2).
 
-Shapes cover both kernel modes: slices that hold whole groups (G <= 32: G = 1, 7,
-15, 32) and slices that are parts of one group (G >= 33: G = 33 ... Lq), several
-64-key tiles with a ragged last tile, d = 64 and 128, B = 64 and 128, bf16 and
-fp32 queries, ragged last groups and non-resident blocks.
+Shapes cover both kernel modes: 128-row slices that hold whole groups (G <= 64:
+G = 1, 7, 15, 32, 33, 40, 64) and slices that are parts of one group (G >= 65:
+one, two, three and 37 parts), several 64-key tiles with a ragged last tile,
+d = 64 and 128, B = 64 and 128, bf16 and fp32 queries, ragged last groups and
+non-resident blocks.
 """
 import numpy as np
 import pytest
@@ -67,15 +68,18 @@ def check_prob(sel, ref, heads=None):
 
 PROB_SMALL = [
     # H, d, S, Lq, B, n, K, G, E, T, dtype
-    (3, 128, 600, 300, 64, 14, 7, 130, 1, 2, torch.bfloat16),   # parts of groups; last group 40 rows
-    (2, 64, 600, 333, 64, 9, 5, 333, 1, 3, torch.bfloat16),     # d = 64, one group in 6 slices
-    (2, 128, 600, 257, 128, 9, 3, 100, 1, 2, torch.bfloat16),   # B = 128, 88-token tail block
-    (2, 128, 600, 300, 64, 14, 4, 15, 1, 3, torch.bfloat16),    # the paper's G = 15: 4 groups per slice
-    (2, 128, 600, 100, 64, 8, 4, 1, 0, 0, torch.bfloat16),      # one row per group: 64 groups per slice
+    (3, 128, 600, 300, 64, 14, 7, 130, 1, 2, torch.bfloat16),   # two parts per group; last group 40 rows
+    (2, 64, 600, 333, 64, 9, 5, 333, 1, 3, torch.bfloat16),     # d = 64, one group in 3 parts
+    (2, 128, 600, 257, 128, 9, 3, 100, 1, 2, torch.bfloat16),   # B = 128, 88-token tail block, one part
+    (2, 128, 600, 300, 64, 14, 4, 15, 1, 3, torch.bfloat16),    # the paper's G = 15: 8 groups per slice
+    (2, 128, 600, 200, 64, 8, 4, 1, 0, 0, torch.bfloat16),      # one row per group: 128 groups per slice
     (2, 128, 600, 97, 64, 8, 4, 32, 0, 0, torch.bfloat16),      # G = 32, last group 1 row
-    (2, 128, 600, 100, 64, 8, 4, 33, 1, 2, torch.bfloat16),     # G = 33: one part per group
+    (2, 128, 600, 100, 64, 8, 4, 33, 1, 2, torch.bfloat16),     # G = 33: 3 groups per slice
+    (2, 128, 600, 300, 64, 8, 4, 64, 1, 2, torch.bfloat16),     # G = 64: the largest whole-group mode
+    (2, 128, 600, 300, 64, 8, 4, 65, 1, 2, torch.bfloat16),     # G = 65: one part per group
     (2, 128, 600, 100, 128, 9, 3, 40, 0, 0, torch.float32),     # fp32 queries
-    (2, 64, 600, 50, 64, 7, 3, 7, 1, 0, torch.float32),         # fp32, d = 64, 9 groups per slice
+    (2, 64, 600, 50, 64, 7, 3, 7, 1, 0, torch.float32),         # fp32, d = 64, 18 groups per slice
+    (2, 128, 600, 300, 64, 9, 3, 150, 1, 2, torch.float32),     # fp32, two parts per group
     (1, 64, 64, 1, 64, 3, 2, 1, 2, 0, torch.float32),           # one query row, one tile
 ]
 
@@ -145,9 +149,9 @@ def test_prob_edge_cases(dev):
 
 @pytest.mark.parametrize("G", [None, 15])
 def test_prob_wan13b_n20(dev, G):
-    """The 1.3B layer at 20 cached chunks: the workload's one group per head (74
-    slices of 64 rows each) and the paper's G = 15 (312 groups); the oracle checks
-    heads 0 and 1."""
+    """The 1.3B layer at 20 cached chunks: the workload's one group per head (37
+    slices of at most 128 rows) and the paper's G = 15 (312 groups, 8 per slice);
+    the oracle checks heads 0 and 1."""
     w = synth.WORKLOADS["wan1.3b_n20"]
     n = w.history_chunks
     group = G or w.group_size
