@@ -56,7 +56,42 @@ def parse():
     p.add_argument("--no-lru", action="store_true", help="skip the LRU hot-cache measurement")
     p.add_argument("--no-small-group", action="store_true", help="skip the paper's small-group setting")
     p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
+    p.add_argument("--prob-only", type=int, default=0, metavar="G",
+                   help="only time selection by probability-averaged scores from the pooled history, "
+                        "query groups of G rows (top-64 for one group per head, else top-4), and exit")
     return p.parse_args()
+
+
+def prob_only(dev, G, reps=50):
+    """Selection by probability-averaged scores alone, on the bench workload's first
+    layer and its pooled history: a profiling target for those kernels."""
+    import torch
+
+    from paper_2605_30519_amd import (SCORE_PROB, CompressedCache, omnimem_compress_chunk, omnimem_select_compressed,
+                                      synth)
+    w = synth.WORKLOADS[WORKLOAD]
+    n = w.history_chunks
+    K = w.top_k if G >= w.query_tokens else 4
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=1000)
+    cc = CompressedCache.allocate(cache, n)
+    for c in range(n):
+        omnimem_compress_chunk(cache, c, cc)
+    sel = None
+    for _ in range(20):
+        sel = omnimem_select_compressed(cache, cc, x.q, K, G, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                                        out=sel, want_score=False, score_mode=SCORE_PROB)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        omnimem_select_compressed(cache, cc, x.q, K, G, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                                  out=sel, want_score=False, score_mode=SCORE_PROB)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    logit_fl = 2.0 * w.query_tokens * n * w.blocks_per_chunk * w.head_dim * w.heads
+    print(json.dumps({"prob_select": {"workload": WORKLOAD, "group_size": G, "top_k": K, "select_ms": round(ms, 4),
+                                      "logit_tflops": round(logit_fl / (ms * 1e-3) / 1e12, 2)}}), flush=True)
 
 
 def attn_flops(idx, cnt, w, n_chunks):
@@ -119,6 +154,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     lib()
+    if args.prob_only:
+        prob_only(dev, args.prob_only)
+        return
     w = synth.WORKLOADS[WORKLOAD]
     n = w.history_chunks
     H, R, K = w.heads, w.groups, w.top_k

@@ -30,8 +30,8 @@ struct SelectPlan {
   bool inline_scores;   // scores computed inside the pooling kernel (small R)
   // probability-averaged scores (score_mode 1): query slices of at most 128 rows,
   // either whole groups (multi: gps groups per slice) or parts of one group (spg
-  // slices per group); one partial row of nb sums per (head, segment), and the
-  // pooled keys split into bf16 pieces, 64-key tiles
+  // slices per group); for parts, one partial row of nb sums per (head, slice);
+  // the pooled keys split into bf16 pieces, 64-key tiles
   int score_mode;
   bool prob_multi;
   int prob_gps, prob_spg, prob_slices, prob_nseg;

@@ -18,8 +18,9 @@
 // split the same way.  The first pass forms S^T = K Q^T (a lane owns one query
 // row: its max and sum stay in the lane), the second S = Q K^T (a lane owns one
 // key: the sum over a group's rows is a sum over the lane's accumulator rows).
-// k_prob_merge: sums a group's slices in order, divides by the group's row count and
-// writes the order-preserving keys that k_topk ranks (0 outside Omega).
+// The group means become the order-preserving keys that k_topk ranks (0 outside
+// Omega): written by k_prob_partial when its slice holds whole groups, else by
+// k_prob_merge, which sums a group's slices in order.
 #include <math.h>
 
 #include "device_common.h"
@@ -53,7 +54,12 @@ struct ProbArgs {
   float scale;
   int multi;            // 1: a slice holds gps whole groups; 0: a slice is part of one group
   int gps, spg, slices, nseg;
-  float* part;          // [H][nseg][nb]
+  float* part;          // [H][nseg][nb] (parts of groups)
+  // whole-group slices write the ranking keys themselves
+  uint32_t* keys;       // [H][R][nbp]
+  int nbp, first_excluded;
+  const int32_t* page_table;
+  int64_t num_pages;
 };
 
 // Merges two (max, sum) states of a log-sum-exp; maxima in raw units, sums of
@@ -306,27 +312,29 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
         const int r_end = min(j * a.G + a.G, rows);
         float sum = 0.f;
         for (int r = j * a.G; r < r_end; ++r) sum += red[r * kPRedStride + col];
-        if (b0 + col < a.nb) a.part[(static_cast<int64_t>(h) * a.nseg + seg0 + j) * a.nb + b0 + col] = sum;
+        const int b = b0 + col;
+        if (b < a.nb) {
+          const int32_t pg = a.page_table != nullptr ? a.page_table[b] : 0;
+          const bool live = b < a.first_excluded && pg >= 0 && (a.page_table == nullptr || pg < a.num_pages);
+          a.keys[(static_cast<int64_t>(h) * a.R + seg0 + j) * a.nbp + b] =
+              live ? score_key(sum / static_cast<float>(r_end - j * a.G)) : 0u;
+        }
       }
     }
   }
 }
 
+// Slices that are parts of one group: the group's parts summed in order.
 __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restrict__ part, int nseg, int nb, int nbp,
-                                                          int lq, int G, int R, int multi, int spg,
+                                                          int lq, int G, int R, int spg,
                                                           const int32_t* __restrict__ page_table, int64_t num_pages,
                                                           int first_excluded, uint32_t* __restrict__ keys) {
   const int b = blockIdx.x * kPThreads + threadIdx.x, r = blockIdx.y, h = blockIdx.z;
   if (b >= nb) return;
   const int rows = min(r * G + G, lq) - r * G;
-  float s;
-  if (multi) {
-    s = part[(static_cast<int64_t>(h) * nseg + r) * nb + b];
-  } else {
-    s = 0.f;
-    const int parts = (rows + kPRows - 1) / kPRows;
-    for (int k = 0; k < parts; ++k) s += part[(static_cast<int64_t>(h) * nseg + r * spg + k) * nb + b];
-  }
+  float s = 0.f;
+  const int parts = (rows + kPRows - 1) / kPRows;
+  for (int k = 0; k < parts; ++k) s += part[(static_cast<int64_t>(h) * nseg + r * spg + k) * nb + b];
   s = s / static_cast<float>(rows);
   const int32_t p = page_table != nullptr ? page_table[b] : 0;
   const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
@@ -356,10 +364,17 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   a.slices = p.prob_slices;
   a.nseg = p.prob_nseg;
   a.part = part;
+  a.keys = keys;
+  a.nbp = nbp;
+  a.first_excluded = p.first_excluded;
+  a.page_table = g.page_table;
+  a.num_pages = g.num_pages;
   hipLaunchKernelGGL((k_prob_partial<T, D>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
-  const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
-  hipLaunchKernelGGL(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R,
-                     a.multi, p.prob_spg, g.page_table, g.num_pages, p.first_excluded, keys);
+  if (!a.multi) {
+    const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
+    hipLaunchKernelGGL(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R,
+                       p.prob_spg, g.page_table, g.num_pages, p.first_excluded, keys);
+  }
   return hipGetLastError();
 }
 

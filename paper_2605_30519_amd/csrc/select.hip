@@ -1002,7 +1002,7 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
       p.prob_slices = p.R * p.prob_spg;
       p.prob_nseg = p.prob_slices;
     }
-    off = align256(off + static_cast<size_t>(g.H) * p.prob_nseg * g.nb * sizeof(float));
+    if (!p.prob_multi) off = align256(off + static_cast<size_t>(g.H) * p.prob_nseg * g.nb * sizeof(float));
     p.off_ksplit = off;
     off = align256(off + static_cast<size_t>(g.H) * ((g.nb + 63) / 64) * 2 * 64 * g.D * sizeof(uint16_t));
   }
