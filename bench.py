@@ -266,6 +266,11 @@ def main():
                    "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe},
     }
 
+    # ---------------------------------------------------------------- select, cache state
+    # the select stage with the 256 MB Infinity Cache (MALL) flushed before each call
+    # by a 1 GiB write, and warm (the same layer back to back)
+    result["stages"]["select_cache_state"] = select_cache_state(layers, sels, ws, w, sbytes)
+
     # ---------------------------------------------------------------- compressed history
     if not args.no_compressed:
         log("compressed-history path (pool the newest chunk + select from pooled keys + sparse attention)")
@@ -525,6 +530,51 @@ def compressed_measure(dev, layers, sels, outs, lses, w, args):
                              "cmp_attn_ms": round(med3(1, 2), 4), "swa_attn_ms": round(med3(2, 3), 4),
                              "gated_combine_ms": round(med3(3, 4), 4)},
             "prob_scores": prob}
+
+
+def select_cache_state(layers, sels, ws, w, sbytes, reps=30):
+    """Select alone, HIP events around each call, layers in rotation: (a) after a
+    1 GiB read that evicts the MALL with clean lines; (b) after a 1 GiB write, which
+    leaves the MALL full of dirty lines that the select's reads must first write
+    back; (c) warm, one layer back to back."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select
+    K = w.top_k
+    scratch = torch.empty(1 << 28, dtype=torch.float32, device=layers[0][0].device)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(3 * reps)]
+    total = torch.zeros((), dtype=torch.float32, device=scratch.device)
+
+    def sel(i, e):
+        q, cache = layers[i % len(layers)]
+        e[0].record()
+        omnimem_select(cache, q, K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale, workspace=ws,
+                       out=sels[i % len(layers)], want_score=False)
+        e[1].record()
+
+    scratch.fill_(1.0)
+    for i in range(reps):
+        total += scratch.sum()
+        sel(i, ev[i])
+    for i in range(reps):
+        scratch.fill_(float(i))
+        sel(i, ev[reps + i])
+    for _ in range(3):
+        sel(0, ev[2 * reps])
+    for i in range(reps):
+        sel(0, ev[2 * reps + i])
+    torch.cuda.synchronize()
+    out = {}
+    for name, part in (("mall_evicted_by_1gib_read", ev[:reps]), ("after_1gib_write_dirty_mall", ev[reps:2 * reps]),
+                       ("warm_same_layer", ev[2 * reps:])):
+        t = np.array([a.elapsed_time(b) for a, b in part])
+        gbs = sbytes / (float(np.median(t)) * 1e-3) / 1e9
+        out[name] = {"select_ms": round(float(np.median(t)), 4),
+                     "p10_p90": [round(float(np.percentile(t, 10)), 4), round(float(np.percentile(t, 90)), 4)],
+                     "achieved_gbs": round(gbs, 1), "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    del scratch
+    return out
 
 
 def small_group_measure(dev, reps=50):
