@@ -40,6 +40,7 @@ struct SelectPlan {
 };
 
 constexpr int kQRowsPerSplit = 512;
+constexpr int kProbSliceRows = 128;  // query rows per workgroup of the probability scores
 constexpr int kInlineGroups = 4;
 
 SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe,

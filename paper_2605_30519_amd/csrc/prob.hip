@@ -30,7 +30,8 @@ namespace omnimem {
 namespace {
 
 constexpr int kPThreads = 256;
-constexpr int kPRows = 128;   // query rows per slice: 64 per wave, two waves deep
+constexpr int kPRows = kProbSliceRows;  // query rows per slice: 64 per wave, two waves deep
+static_assert(kPRows == 128, "the wave layout assumes 128-row slices");
 constexpr int kPKeys = 64;    // pooled keys per tile: 32 per wave, two waves wide
 constexpr int kPRedStride = kPKeys + 1;
 constexpr float kLog2eP = 1.4426950408889634f;

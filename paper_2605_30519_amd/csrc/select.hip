@@ -989,7 +989,7 @@ SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_ou
   off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
   p.off_part = off;
   if (score_mode == 1) {
-    constexpr int kSliceRows = 128;
+    constexpr int kSliceRows = kProbSliceRows;
     p.prob_multi = G <= kSliceRows / 2;
     if (p.prob_multi) {
       p.prob_gps = kSliceRows / G;
