@@ -14,6 +14,13 @@ ms_per_step = ms per chunk-layer, a roofline object for the dominant kernel
 (measured with HIP events on the launch stream), the CPU oracle's throughput on
 a bounded sample of the same workload, per-stage times, and a sweep over history
 length (10/30/60/120 chunks) with the speedup over in-build dense attention.
+
+Further objects in the same line, each skippable by a flag: the select stage by
+cache state; the compressed-history step (pooled keys, CMP attention, the gated
+three-branch forward of Eq. 1, and selection by probability-averaged scores);
+the paper's small-group setting (G_q = 15); the LRU hot cache; the 30-layer
+history ramp; achievable-peak probes; CPU-oracle extrapolations.  --prob-only G
+times only the probability-score selection (a profiling target).
 """
 from __future__ import annotations
 
