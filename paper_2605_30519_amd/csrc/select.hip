@@ -28,24 +28,28 @@ namespace {
 constexpr int kThreads = 256;
 
 // -------------------------------------------------------------- proxy queries
-constexpr int kQThreads = 1024;
+constexpr int kQThreads = 512;
+constexpr int kQColSplits = 2;       // the big variant: each workgroup sums half of d (one 128-byte line per row)
 constexpr int kQSmallThreads = 64;   // groups of at most kQSmallRows rows: one wave per split
 constexpr int kQSmallRows = 64;
 
-// NT threads per split; UNROLL rows per thread in flight (the big variant covers a
-// 512-row split in one round, the one-wave variant small groups).
-template <typename T, int D, int NT>
+// NT threads per (split, column range of D/DS); UNROLL rows per thread in flight
+// (the big variant covers a 512-row split in one round, the one-wave variant small
+// groups).  blockIdx.x = split * DS + column range.
+template <typename T, int D, int NT, int DS>
 __global__ __launch_bounds__(NT) void k_qmean_partial(const T* __restrict__ q, int lq, int H, int G, int R,
                                                       int nsplit, float* __restrict__ partial) {
   using V = Vec16<T>;
   constexpr int VEC = V::N;
-  constexpr int CPR = D / VEC;       // 16-byte chunks per row
-  constexpr int PHASES = NT / CPR;   // rows summed side by side
-  constexpr int UNROLL = NT == kQThreads ? (kQRowsPerSplit + PHASES - 1) / PHASES : (kQSmallRows + PHASES - 1) / PHASES;
+  constexpr int DC = D / DS;          // columns of this workgroup
+  constexpr int CPR = DC / VEC;       // 16-byte chunks per row
+  constexpr int PHASES = NT / CPR;    // rows summed side by side
+  constexpr int SPLIT_ROWS = NT == kQSmallThreads ? kQSmallRows : kQRowsPerSplit;
+  constexpr int UNROLL = (SPLIT_ROWS + PHASES - 1) / PHASES;
   constexpr int kWaves = NT / kWave, PH_PER_WAVE = kWave / CPR;
-  __shared__ float red[kWaves][D];
+  __shared__ float red[kWaves][DC];
 
-  const int s = blockIdx.x, r = blockIdx.y, h = blockIdx.z;
+  const int s = blockIdx.x / DS, cs = blockIdx.x % DS, r = blockIdx.y, h = blockIdx.z;
   const int g0 = r * G, g1 = min(g0 + G, lq);
   const int r0 = g0 + s * kQRowsPerSplit, r1 = min(r0 + kQRowsPerSplit, g1);
   const int c = threadIdx.x % CPR, ph = threadIdx.x / CPR;
@@ -58,7 +62,7 @@ __global__ __launch_bounds__(NT) void k_qmean_partial(const T* __restrict__ q, i
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       const int rr = row + u * PHASES;
-      raw[u] = rr < r1 ? *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(rr) * H + h) * D + c * VEC)
+      raw[u] = rr < r1 ? *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(rr) * H + h) * D + cs * DC + c * VEC)
                        : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
@@ -81,11 +85,11 @@ __global__ __launch_bounds__(NT) void k_qmean_partial(const T* __restrict__ q, i
   }
   __syncthreads();
   static_assert(PH_PER_WAVE >= 1, "a wave spans whole rows");
-  for (int col = threadIdx.x; col < D; col += NT) {
+  for (int col = threadIdx.x; col < DC; col += NT) {
     float sum = 0.f;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) sum += red[w][col];
-    partial[((static_cast<int64_t>(h) * R + r) * nsplit + s) * D + col] = sum;
+    partial[((static_cast<int64_t>(h) * R + r) * nsplit + s) * D + cs * DC + col] = sum;
   }
 }
 
@@ -885,17 +889,17 @@ void launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, in
   }
 }
 
-// Proxy-query partial sums: 1,024 threads per 512-row split, or one wave per
-// group when groups hold at most kQSmallRows rows (one split each).
+// Proxy-query partial sums: two 512-thread workgroups per 512-row split (one per
+// half of d), or one wave per group when groups hold at most kQSmallRows rows (one
+// split each).
 template <typename T, int D>
 void launch_qmean(const SelectPlan& p, const CacheGeom& g, const T* q, float* qpart, hipStream_t stream) {
-  const dim3 grid(p.qsplit, p.R, g.H);
   if (p.G <= kQSmallRows)
-    hipLaunchKernelGGL((k_qmean_partial<T, D, kQSmallThreads>), grid, dim3(kQSmallThreads), 0, stream, q, p.lq, g.H,
-                       p.G, p.R, p.qsplit, qpart);
+    hipLaunchKernelGGL((k_qmean_partial<T, D, kQSmallThreads, 1>), dim3(p.qsplit, p.R, g.H), dim3(kQSmallThreads), 0,
+                       stream, q, p.lq, g.H, p.G, p.R, p.qsplit, qpart);
   else
-    hipLaunchKernelGGL((k_qmean_partial<T, D, kQThreads>), grid, dim3(kQThreads), 0, stream, q, p.lq, g.H, p.G, p.R,
-                       p.qsplit, qpart);
+    hipLaunchKernelGGL((k_qmean_partial<T, D, kQThreads, kQColSplits>), dim3(p.qsplit * kQColSplits, p.R, g.H),
+                       dim3(kQThreads), 0, stream, q, p.lq, g.H, p.G, p.R, p.qsplit, qpart);
 }
 
 hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* keys, int nbp, int32_t* idx,
