@@ -145,21 +145,28 @@ __device__ __forceinline__ bf16x8 key_frag(const uint16_t* ktile, int piece, int
   return *reinterpret_cast<const bf16x8*>(ktile + piece * kPKeys * D + krow * D + 8 * pc);
 }
 
-template <typename T, int D>
+// MULTI: the slice holds whole groups, and a 128 x 64 probability tile is reduced
+// through LDS; the key tile then has one LDS buffer, staged between two barriers.
+// Otherwise the slice is part of one group: two key-tile buffers, tile t + 1
+// staged right after tile t's MFMAs, one barrier per tile.
+template <typename T, int D, bool MULTI>
 __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
   constexpr int KK = D / 16;                      // MFMA steps over d
   constexpr int CH = D / 8;                       // 16-byte chunks per key row
   constexpr int LPT = 2 * kPKeys * CH / kPThreads;  // 16-byte loads per thread per tile
   constexpr int QP = QueryPieces<T>::N;
-  __shared__ __align__(16) uint16_t ktile[2 * kPKeys * D];
-  __shared__ float red[kPRows * kPRedStride];
+  constexpr int NBUF = MULTI ? 1 : 2;
+  constexpr int TILE = 2 * kPKeys * D;            // bf16 elements of one split tile
+  __shared__ __align__(16) uint16_t ktile[NBUF * TILE];
+  // MULTI: the probability tile; else two buffers of the two row halves' key sums
+  __shared__ float red[MULTI ? kPRows * kPRedStride : 2 * 2 * kPKeys];
   __shared__ float mrg_m[2][kPRows], mrg_l[2][kPRows];
   __shared__ float lse2[kPRows];
 
   const int id = xcd_contiguous_id(blockIdx.x, gridDim.x);
   const int h = id / a.slices, slice = id % a.slices;
   int row0, rows, seg0;
-  if (a.multi) {
+  if constexpr (MULTI) {
     seg0 = slice * a.gps;
     row0 = seg0 * a.G;
     rows = min(a.gps * a.G, a.lq - row0);
@@ -207,15 +214,23 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
   // ---- pass 1: LSE of every row over all pooled keys (S^T = K Q^T, lane = row)
   float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
   fetch_tile<D>(a, h, 0, kv);
-  for (int t = 0; t < a.ntiles; ++t) {
-    __syncthreads();
+  if constexpr (NBUF == 2) {
     stage_tile<D>(kv, ktile);
     __syncthreads();
-    if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    if (a.ntiles > 1) fetch_tile<D>(a, h, 1, kv);
+  }
+  for (int t = 0; t < a.ntiles; ++t) {
+    const uint16_t* kt = ktile + (NBUF == 2 ? (t & 1) * TILE : 0);
+    if constexpr (NBUF == 1) {
+      __syncthreads();
+      stage_tile<D>(kv, ktile);
+      __syncthreads();
+      if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    }
     f32x16 acc[2] = {};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8 kh = key_frag<D>(ktile, 0, kk, krow, half), kl = key_frag<D>(ktile, 1, kk, krow, half);
+      const bf16x8 kh = key_frag<D>(kt, 0, kk, krow, half), kl = key_frag<D>(kt, 1, kk, krow, half);
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kh, qh[s][kk], acc[s], 0, 0, 0);
@@ -246,6 +261,11 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
         m_run[s] = mnew;
       }
     }
+    if constexpr (NBUF == 2) {
+      if (t + 1 < a.ntiles) stage_tile<D>(kv, ktile + ((t + 1) & 1) * TILE);
+      __syncthreads();
+      if (t + 2 < a.ntiles) fetch_tile<D>(a, h, t + 2, kv);
+    }
   }
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
@@ -269,17 +289,26 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
   for (int s = 0; s < 2; ++s)
 #pragma unroll
     for (int i = 0; i < 16; ++i) lr[s][i] = lse2[64 * rh + 32 * s + 8 * (i / 4) + 4 * half + i % 4];
-  const int ngroups = a.multi ? min(a.gps, a.R - seg0) : 1;
+  const int ngroups = MULTI ? min(a.gps, a.R - seg0) : 1;
+  float* const part_row = a.part + (static_cast<int64_t>(h) * a.nseg + seg0) * a.nb;
   fetch_tile<D>(a, h, 0, kv);
-  for (int t = 0; t < a.ntiles; ++t) {
-    __syncthreads();
+  if constexpr (NBUF == 2) {
     stage_tile<D>(kv, ktile);
     __syncthreads();
-    if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    if (a.ntiles > 1) fetch_tile<D>(a, h, 1, kv);
+  }
+  for (int t = 0; t < a.ntiles; ++t) {
+    const uint16_t* kt = ktile + (NBUF == 2 ? (t & 1) * TILE : 0);
+    if constexpr (NBUF == 1) {
+      __syncthreads();
+      stage_tile<D>(kv, ktile);
+      __syncthreads();
+      if (t + 1 < a.ntiles) fetch_tile<D>(a, h, t + 1, kv);
+    }
     f32x16 acc[2] = {};
 #pragma unroll
     for (int kk = 0; kk < KK; ++kk) {
-      const bf16x8 kh = key_frag<D>(ktile, 0, kk, krow, half), kl = key_frag<D>(ktile, 1, kk, krow, half);
+      const bf16x8 kh = key_frag<D>(kt, 0, kk, krow, half), kl = key_frag<D>(kt, 1, kk, krow, half);
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         acc[s] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qh[s][kk], kh, acc[s], 0, 0, 0);
@@ -289,17 +318,20 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
     }
     // acc[s][i]: row 64 rh + 32 s + 8 (i/4) + 4 half + i%4 against key t*64 + krow
     const int b0 = t * kPKeys;
-    if (!a.multi) {
+    if constexpr (!MULTI) {
+      // the key sums of tile t go to buffer t & 1; those of tile t - 1, written
+      // before the last barrier, are added and stored now
       float v = 0.f;
 #pragma unroll
       for (int s = 0; s < 2; ++s)
 #pragma unroll
         for (int i = 0; i < 16; ++i) v += __builtin_amdgcn_exp2f(fmaf(acc[s][i], c2, -lr[s][i]));
       v += __shfl_xor(v, 32);
-      if (half == 0) red[rh * kPKeys + krow] = v;
-      __syncthreads();
-      if (tid < kPKeys && b0 + tid < a.nb)
-        a.part[(static_cast<int64_t>(h) * a.nseg + seg0) * a.nb + b0 + tid] = red[tid] + red[kPKeys + tid];
+      if (half == 0) red[(t & 1) * 2 * kPKeys + rh * kPKeys + krow] = v;
+      if (t > 0 && tid < kPKeys && b0 - kPKeys + tid < a.nb) {
+        const float* r = red + ((t - 1) & 1) * 2 * kPKeys;
+        part_row[b0 - kPKeys + tid] = r[tid] + r[kPKeys + tid];
+      }
     } else {
 #pragma unroll
       for (int s = 0; s < 2; ++s)
@@ -321,6 +353,18 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
               live ? score_key(sum / static_cast<float>(r_end - j * a.G)) : 0u;
         }
       }
+    }
+    if constexpr (NBUF == 2) {
+      if (t + 1 < a.ntiles) stage_tile<D>(kv, ktile + ((t + 1) & 1) * TILE);
+      __syncthreads();
+      if (t + 2 < a.ntiles) fetch_tile<D>(a, h, t + 2, kv);
+    }
+  }
+  if constexpr (!MULTI) {  // the last tile's key sums, written before the loop's last barrier
+    const int t = a.ntiles - 1, b = t * kPKeys + tid;
+    if (tid < kPKeys && b < a.nb) {
+      const float* r = red + (t & 1) * 2 * kPKeys;
+      part_row[b] = r[tid] + r[kPKeys + tid];
     }
   }
 }
@@ -370,7 +414,10 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   a.first_excluded = p.first_excluded;
   a.page_table = g.page_table;
   a.num_pages = g.num_pages;
-  hipLaunchKernelGGL((k_prob_partial<T, D>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
+  if (a.multi)
+    hipLaunchKernelGGL((k_prob_partial<T, D, true>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
+  else
+    hipLaunchKernelGGL((k_prob_partial<T, D, false>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
   if (!a.multi) {
     const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
     hipLaunchKernelGGL(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R,
