@@ -11,7 +11,10 @@
 // k_prob_partial: one workgroup per (head, slice of at most 128 query rows), the
 // slices of one head contiguous on one XCD so that its L2 holds that head's keys.
 // Each wave owns 64 rows (two 32-row MFMA tiles that share every key fragment) and
-// 32 keys of each tile.  It walks the tiles twice: first for each row's LSE
+// 32 keys of each tile; a slice that is part of one group double-buffers the key
+// tiles in LDS (one barrier per tile), a slice of whole groups stages each tile
+// between two barriers, its LDS holding the probability tile that it reduces per
+// group.  The workgroup walks the tiles twice: first for each row's LSE
 // (online, exp2 domain, the hardware exp2: probabilities below 2^-126 count as 0),
 // then for exp(u - LSE) summed over the rows of each group segment of the slice.  The products are bf16 MFMA (32x32x16) with fp32
 // accumulation: hi*q + lo*q for bf16 queries (exact), plus hi*q_lo for fp32 queries
