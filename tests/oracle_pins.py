@@ -413,6 +413,19 @@ def pin_gated_combine():
     g = rng.standard_normal((5, 2, 3))
     assert np.allclose(O.gated_combine(a, b, None, g) + O.gated_combine(None, None, c, g),
                        O.gated_combine(a, b, c, g), atol=1e-14)
+    # Finite logits: sigmoid(ln 3) = 3/4 and sigmoid(-ln 3) = 1/4 exactly, since
+    # 1 / (1 + e^{-ln 3}) = 1 / (1 + 1/3).  A slip such as sigmoid(2x) = (1 + tanh x) / 2
+    # keeps every property above but fails these.
+    ones = np.ones((1, 1, 1))
+    three = np.full((1, 1, 3), -800.0)
+    three[..., 0] = math.log(3.0)
+    assert abs(O.gated_combine(ones, None, None, three)[0, 0, 0] - 0.75) < 1e-15
+    three[..., 0] = -math.log(3.0)
+    assert abs(O.gated_combine(ones, None, None, three)[0, 0, 0] - 0.25) < 1e-15
+    # Random logits over the whole range against the library logistic function.
+    g = rng.standard_normal((5, 2, 3)) * 6.0
+    ref = sps.expit(g[..., 0:1]) * a + sps.expit(g[..., 1:2]) * b + sps.expit(g[..., 2:3]) * c
+    assert np.allclose(O.gated_combine(a, b, c, g), ref, rtol=1e-14, atol=1e-15)
 
 
 def pin_attention_special_cases():

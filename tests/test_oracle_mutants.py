@@ -81,3 +81,37 @@ def test_pins_reject_mutant(name, old, new, source, tmp_path):
             except (AssertionError, ValueError, ZeroDivisionError, FloatingPointError):
                 caught.append(pin.__name__)
     assert caught, f"mutant {name} passed every pin"
+
+
+# Mistakes planted in the oracle's Python-level functions: the function's source is
+# edited, compiled in the oracle module's namespace and swapped in for the pins' run.
+PY_MUTANTS = [
+    ("gate_sigmoid_of_twice_the_logit", "gated_combine",
+     "z = np.exp(-np.abs(gl[..., c]))", "z = np.exp(-2.0 * np.abs(gl[..., c]))"),
+    ("gate_branches_reversed", "gated_combine", "z = np.exp(-np.abs(gl[..., c]))",
+     "z = np.exp(-np.abs(gl[..., 2 - c]))"),
+    ("gate_sign_flipped", "gated_combine", "np.where(gl[..., c] >= 0, 1.0 / (1.0 + z), z / (1.0 + z))",
+     "np.where(gl[..., c] >= 0, z / (1.0 + z), 1.0 / (1.0 + z))"),
+    ("bf16_rounds_to_7_bits", "round_bf16", "np.round(m * 256.0) / 256.0", "np.round(m * 128.0) / 128.0"),
+    ("cmp_cache_values_from_keys", "cmp_cache", "kc, vc = pool_keys(k, B), pool_keys(v, B)",
+     "kc, vc = pool_keys(k, B), pool_keys(k, B)"),
+]
+
+
+@pytest.mark.parametrize("name,func,old,new", PY_MUTANTS, ids=[m[0] for m in PY_MUTANTS])
+def test_pins_reject_python_mutant(name, func, old, new, monkeypatch):
+    import inspect
+    import textwrap
+
+    src = textwrap.dedent(inspect.getsource(getattr(oracle, func)))
+    assert src.count(old) >= 1, f"mutation site for {name} not found in oracle.{func}"
+    ns = dict(vars(oracle))
+    exec(compile(src.replace(old, new, 1), f"<mutant {name}>", "exec"), ns)
+    monkeypatch.setattr(oracle, func, ns[func])
+    caught = []
+    for pin in ALL_PINS:
+        try:
+            pin()
+        except (AssertionError, ValueError, ZeroDivisionError, FloatingPointError):
+            caught.append(pin.__name__)
+    assert caught, f"mutant {name} passed every pin"
