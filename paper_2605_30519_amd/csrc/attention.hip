@@ -1052,28 +1052,17 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   const int64_t nwg = static_cast<int64_t>(g.H) * L.R * a.tiles_per_group;
   if (nwg <= 0) return hipSuccess;
   if (nwg > 0x7fffffff) return hipErrorInvalidConfiguration;
-  if (r64) {
-    hipLaunchKernelGGL(k_attn_bf16_r64<128>, dim3(static_cast<unsigned>(nwg)), dim3(kR64Waves * kWave), 0, stream, a);
-  } else if (g.dtype == 0) {
-    const dim3 grid(static_cast<unsigned>(nwg));
-    if (!small) {
-      if (g.D == 128)
-        hipLaunchKernelGGL((k_attn_bf16<128, true, kWaves>), grid, dim3(kWaves * kWave), 0, stream, a);
-      else
-        hipLaunchKernelGGL((k_attn_bf16<64, true, kWaves>), grid, dim3(kWaves * kWave), 0, stream, a);
-    } else {
-      if (g.D == 128)
-        hipLaunchKernelGGL((k_attn_bf16<128, false, kSmallWaves>), grid, dim3(kSmallWaves * kWave), 0, stream, a);
-      else
-        hipLaunchKernelGGL((k_attn_bf16<64, false, kSmallWaves>), grid, dim3(kSmallWaves * kWave), 0, stream, a);
-    }
-  } else {
+  const dim3 grid(static_cast<unsigned>(nwg));
+  // bf16 with d = 128 and more than 32 rows per group always takes the 64-row kernel
+  if (r64) return launch_kernel(k_attn_bf16_r64<128>, grid, dim3(kR64Waves * kWave), 0, stream, a);
+  if (g.dtype == 0) {
+    if (!small) return launch_kernel(k_attn_bf16<64, true, kWaves>, grid, dim3(kWaves * kWave), 0, stream, a);
     if (g.D == 128)
-      hipLaunchKernelGGL(k_attn_f32<128>, dim3(static_cast<unsigned>(nwg)), dim3(kWave), 0, stream, a);
-    else
-      hipLaunchKernelGGL(k_attn_f32<64>, dim3(static_cast<unsigned>(nwg)), dim3(kWave), 0, stream, a);
+      return launch_kernel(k_attn_bf16<128, false, kSmallWaves>, grid, dim3(kSmallWaves * kWave), 0, stream, a);
+    return launch_kernel(k_attn_bf16<64, false, kSmallWaves>, grid, dim3(kSmallWaves * kWave), 0, stream, a);
   }
-  return hipGetLastError();
+  if (g.D == 128) return launch_kernel(k_attn_f32<128>, grid, dim3(kWave), 0, stream, a);
+  return launch_kernel(k_attn_f32<64>, grid, dim3(kWave), 0, stream, a);
 }
 
 }  // namespace omnimem

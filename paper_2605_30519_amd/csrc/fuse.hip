@@ -75,14 +75,12 @@ hipError_t launch_gated_combine(int dtype, int64_t rows, int D, const void* o_cm
   if (blocks > 0x7fffffff) return hipErrorInvalidConfiguration;
   const dim3 grid(static_cast<unsigned>(blocks));
   if (dtype == 0)
-    hipLaunchKernelGGL(k_gated_combine<uint16_t>, grid, dim3(kFuseThreads), 0, stream,
-                       static_cast<const uint16_t*>(o_cmp), static_cast<const uint16_t*>(o_slc),
-                       static_cast<const uint16_t*>(o_swa), gate, rows, cpr, static_cast<uint16_t*>(out));
-  else
-    hipLaunchKernelGGL(k_gated_combine<float>, grid, dim3(kFuseThreads), 0, stream,
+    return launch_kernel(k_gated_combine<uint16_t>, grid, dim3(kFuseThreads), 0, stream,
+                         static_cast<const uint16_t*>(o_cmp), static_cast<const uint16_t*>(o_slc),
+                         static_cast<const uint16_t*>(o_swa), gate, rows, cpr, static_cast<uint16_t*>(out));
+  return launch_kernel(k_gated_combine<float>, grid, dim3(kFuseThreads), 0, stream,
                        static_cast<const float*>(o_cmp), static_cast<const float*>(o_slc),
                        static_cast<const float*>(o_swa), gate, rows, cpr, static_cast<float*>(out));
-  return hipGetLastError();
 }
 
 }  // namespace omnimem

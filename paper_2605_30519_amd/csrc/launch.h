@@ -5,7 +5,40 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <type_traits>
+#include <utility>
+
 namespace omnimem {
+
+// Launches one kernel and returns that launch's own status.  The runtime's
+// per-thread "last error" is neither read nor cleared, so an error left there by
+// the caller's own HIP work is not reported as the library's, and is not lost.
+template <typename... KArgs, typename... Args>
+inline hipError_t launch_kernel(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t shmem, hipStream_t stream,
+                                Args&&... args) {
+  static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+  std::tuple<std::decay_t<KArgs>...> vals(static_cast<std::decay_t<KArgs>>(std::forward<Args>(args))...);
+  void* ptrs[sizeof...(KArgs) > 0 ? sizeof...(KArgs) : 1] = {};
+  std::apply([&ptrs](auto&... v) {
+    size_t i = 0;
+    ((ptrs[i++] = static_cast<void*>(&v)), ...);
+  }, vals);
+  return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs, shmem, stream);
+}
+
+// The status of a sequence of launches: the first failure is kept and the launches
+// after it are not issued.
+struct LaunchStatus {
+  hipError_t err = hipSuccess;
+  template <typename Kernel, typename... Args>
+  void operator()(Kernel kernel, dim3 grid, dim3 block, size_t shmem, hipStream_t stream, Args&&... args) {
+    if (err == hipSuccess) err = launch_kernel(kernel, grid, block, shmem, stream, std::forward<Args>(args)...);
+  }
+  void add(hipError_t e) {
+    if (err == hipSuccess) err = e;
+  }
+};
 
 // Geometry of one paged layer cache, resolved and validated on the host.
 struct CacheGeom {

@@ -394,8 +394,8 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
                              int64_t kbar_stride, float* part, uint4* ksplit, uint32_t* keys, int nbp,
                              hipStream_t stream) {
   const int ntiles = (g.nb + kPKeys - 1) / kPKeys;
-  hipLaunchKernelGGL((k_split_keys<D>), dim3(ntiles, g.H), dim3(kPThreads), 0, stream, kbar, kbar_stride, g.nb,
-                     ntiles, ksplit);
+  LaunchStatus st;
+  st(k_split_keys<D>, dim3(ntiles, g.H), dim3(kPThreads), 0, stream, kbar, kbar_stride, g.nb, ntiles, ksplit);
   ProbArgs a;
   a.q = q;
   a.lq = p.lq;
@@ -418,15 +418,15 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   a.page_table = g.page_table;
   a.num_pages = g.num_pages;
   if (a.multi)
-    hipLaunchKernelGGL((k_prob_partial<T, D, true>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
+    st(k_prob_partial<T, D, true>, dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
   else
-    hipLaunchKernelGGL((k_prob_partial<T, D, false>), dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
+    st(k_prob_partial<T, D, false>, dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
   if (!a.multi) {
     const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
-    hipLaunchKernelGGL(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R,
-                       p.prob_spg, g.page_table, g.num_pages, p.first_excluded, keys);
+    st(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R, p.prob_spg,
+       g.page_table, g.num_pages, p.first_excluded, keys);
   }
-  return hipGetLastError();
+  return st.err;
 }
 
 }  // namespace

@@ -866,39 +866,37 @@ __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict_
 inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
 template <int D>
-void launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride, const float* qpart,
-                  int nbp, uint32_t* keys, hipStream_t stream) {
+hipError_t launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride,
+                        const float* qpart, int nbp, uint32_t* keys, hipStream_t stream) {
   if (p.R <= kInlineGroups) {
     const int waves = (g.nb + kScoreRowsPerWave - 1) / kScoreRowsPerWave;
     const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
     if (p.R == 1)
-      hipLaunchKernelGGL((k_score_rows<D, 1>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit,
-                         p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
-    else
-      hipLaunchKernelGGL((k_score_rows<D, kInlineGroups>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart,
+      return launch_kernel(k_score_rows<D, 1>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit,
+                           p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+    return launch_kernel(k_score_rows<D, kInlineGroups>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart,
                          p.qsplit, p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale,
                          keys);
-  } else if (p.R >= kScoreTiledMinGroups) {
-    const dim3 grid((g.nb + 63) / 64, (p.R + 63) / 64, g.H);
-    hipLaunchKernelGGL((k_score_tiled<D>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq,
-                       p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
-  } else {
-    const dim3 grid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
-    hipLaunchKernelGGL((k_score<D>), grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq, p.G,
-                       g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
   }
+  if (p.R >= kScoreTiledMinGroups) {
+    const dim3 grid((g.nb + 63) / 64, (p.R + 63) / 64, g.H);
+    return launch_kernel(k_score_tiled<D>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq,
+                         p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+  }
+  const dim3 grid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
+  return launch_kernel(k_score<D>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq, p.G,
+                       g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
 }
 
 // Proxy-query partial sums: two 512-thread workgroups per 512-row split (one per
 // half of d), or one wave per group when groups hold at most kQSmallRows rows (one
 // split each).
 template <typename T, int D>
-void launch_qmean(const SelectPlan& p, const CacheGeom& g, const T* q, float* qpart, hipStream_t stream) {
+hipError_t launch_qmean(const SelectPlan& p, const CacheGeom& g, const T* q, float* qpart, hipStream_t stream) {
   if (p.G <= kQSmallRows)
-    hipLaunchKernelGGL((k_qmean_partial<T, D, kQSmallThreads, 1>), dim3(p.qsplit, p.R, g.H), dim3(kQSmallThreads), 0,
-                       stream, q, p.lq, g.H, p.G, p.R, p.qsplit, qpart);
-  else
-    hipLaunchKernelGGL((k_qmean_partial<T, D, kQThreads, kQColSplits>), dim3(p.qsplit * kQColSplits, p.R, g.H),
+    return launch_kernel(k_qmean_partial<T, D, kQSmallThreads, 1>, dim3(p.qsplit, p.R, g.H), dim3(kQSmallThreads), 0,
+                         stream, q, p.lq, g.H, p.G, p.R, p.qsplit, qpart);
+  return launch_kernel(k_qmean_partial<T, D, kQThreads, kQColSplits>, dim3(p.qsplit * kQColSplits, p.R, g.H),
                        dim3(kQThreads), 0, stream, q, p.lq, g.H, p.G, p.R, p.qsplit, qpart);
 }
 
@@ -909,14 +907,12 @@ hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* 
   // that; with many rows (small query groups) 256-thread workgroups pack more rows
   // per CU
   if (p.R * g.H >= kTopkManyRows && g.nb <= 256 * 4 * kTopkVecPerLane)
-    hipLaunchKernelGGL(k_topk<256>, tgrid, dim3(256), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  else if (g.nb <= 512 * 4 * kTopkVecPerLane)
-    hipLaunchKernelGGL(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  else if (g.nb <= kTopkRegMax)
-    hipLaunchKernelGGL(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  else
-    hipLaunchKernelGGL(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
-  return hipGetLastError();
+    return launch_kernel(k_topk<256>, tgrid, dim3(256), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  if (g.nb <= 512 * 4 * kTopkVecPerLane)
+    return launch_kernel(k_topk<512>, tgrid, dim3(512), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  if (g.nb <= kTopkRegMax)
+    return launch_kernel(k_topk<1024>, tgrid, dim3(1024), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
+  return launch_kernel(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
 }
 
 template <typename T, int D>
@@ -928,7 +924,8 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
   uint32_t* keys = reinterpret_cast<uint32_t*>(ws + p.off_keys);
   const int nbp = (g.nb + 3) / 4 * 4;
 
-  launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
+  LaunchStatus st;
+  st.add(launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream));
   if (g.nb > 0) {
     PoolArgs a;
     a.k_pages = g.k_pages;
@@ -951,7 +948,7 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     a.blocks_per_wave = kPoolBlocksPerWave;
     const int waves = (g.nb + a.blocks_per_wave - 1) / a.blocks_per_wave;
     const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
-    auto pool = [&](auto kernel) { hipLaunchKernelGGL(kernel, grid, dim3(kThreads), 0, stream, a); };
+    auto pool = [&](auto kernel) { st(kernel, grid, dim3(kThreads), 0, stream, a); };
     if (g.B == 64) {
       if (!p.inline_scores) pool(k_pool_score<T, D, 64, 0>);
       else if (p.R == 1) pool(k_pool_score<T, D, 64, 1>);
@@ -961,9 +958,10 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
       else if (p.R == 1) pool(k_pool_score<T, D, 128, 1>);
       else pool(k_pool_score<T, D, 128, kInlineGroups>);
     }
-    if (!p.inline_scores)
-      launch_score<D>(g, p, kbar, static_cast<int64_t>(g.nb), qpart, nbp, keys, stream);
+    if (!p.inline_scores && st.err == hipSuccess)
+      st.add(launch_score<D>(g, p, kbar, static_cast<int64_t>(g.nb), qpart, nbp, keys, stream));
   }
+  if (st.err != hipSuccess) return st.err;
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
 
@@ -1031,11 +1029,8 @@ hipError_t launch_compress_typed(const CacheGeom& g, const CmpCache& cc, int chu
   a.c_page_table = cc.page_table;
   a.cap_blocks = cc.cap_blocks;
   const dim3 grid((g.Bpc + kThreads / kWave - 1) / (kThreads / kWave), g.H);
-  if (g.B == 64)
-    hipLaunchKernelGGL((k_compress_chunk<T, D, 64>), grid, dim3(kThreads), 0, stream, a);
-  else
-    hipLaunchKernelGGL((k_compress_chunk<T, D, 128>), grid, dim3(kThreads), 0, stream, a);
-  return hipGetLastError();
+  if (g.B == 64) return launch_kernel(k_compress_chunk<T, D, 64>, grid, dim3(kThreads), 0, stream, a);
+  return launch_kernel(k_compress_chunk<T, D, 128>, grid, dim3(kThreads), 0, stream, a);
 }
 
 template <typename T, int D>
@@ -1055,8 +1050,10 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
     }
     return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
   }
-  launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
-  if (g.nb > 0) launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
+  hipError_t e = launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
+  if (e == hipSuccess && g.nb > 0)
+    e = launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
+  if (e != hipSuccess) return e;
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
 }
 

@@ -96,21 +96,21 @@ hipError_t launch_union_gather(const CacheGeom& g, const UnionPlan& up, const At
   void* kbuf = ws + up.off_kbuf;
   void* vbuf = ws + up.off_vbuf;
   const int nb = g.nb;
+  LaunchStatus st;
   if (nb == 0) {
-    hipLaunchKernelGGL(k_fill_i32, dim3(1), dim3(64), 0, stream, union_blocks, 1, 0);
+    st(k_fill_i32, dim3(1), dim3(64), 0, stream, union_blocks, 1, 0);
   } else {
-    hipLaunchKernelGGL(k_fill_i32, dim3((nb + 255) / 256), dim3(256), 0, stream, flags, nb, 0);
+    st(k_fill_i32, dim3((nb + 255) / 256), dim3(256), 0, stream, flags, nb, 0);
     const int rows = g.H * a.R;
     const int64_t entries = static_cast<int64_t>(rows) * a.top_k;
-    hipLaunchKernelGGL(k_union_mark, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, stream, a.idx,
-                       a.cnt, rows, a.top_k, nb, g.page_table, g.num_pages, flags);
-    hipLaunchKernelGGL(k_union_scan, dim3(1), dim3(kScanThreads), 0, stream, flags, nb, table, union_blocks);
-    hipLaunchKernelGGL(k_union_gather, dim3(nb, g.H), dim3(256), 0, stream, static_cast<const uint4*>(g.k_pages),
-                       static_cast<const uint4*>(g.v_pages), g.page_table, table, g.H, up.slab_bytes / 16,
-                       static_cast<uint4*>(kbuf), static_cast<uint4*>(vbuf));
+    st(k_union_mark, dim3(static_cast<unsigned>((entries + 255) / 256)), dim3(256), 0, stream, a.idx, a.cnt, rows,
+       a.top_k, nb, g.page_table, g.num_pages, flags);
+    st(k_union_scan, dim3(1), dim3(kScanThreads), 0, stream, flags, nb, table, union_blocks);
+    st(k_union_gather, dim3(nb, g.H), dim3(256), 0, stream, static_cast<const uint4*>(g.k_pages),
+       static_cast<const uint4*>(g.v_pages), g.page_table, table, g.H, up.slab_bytes / 16, static_cast<uint4*>(kbuf),
+       static_cast<uint4*>(vbuf));
   }
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (st.err != hipSuccess) return st.err;
   CacheGeom gu = g;
   gu.k_pages = kbuf;
   gu.v_pages = vbuf;

@@ -221,6 +221,11 @@ class PagedKVCache:
                 raise ValueError("cache tensors must be contiguous")
         if self.page_table.dtype != torch.int32:
             raise TypeError("page_table must be int32")
+        if self.k_pages.dim() != 4 or self.v_pages.shape != self.k_pages.shape:
+            raise ValueError("k_pages and v_pages must share one [num_pages, H, B, d] shape")
+        if self.page_table.dim() != 2 or int(self.page_table.shape[1]) != self.blocks_per_chunk:
+            raise ValueError(f"page_table must be [n, {self.blocks_per_chunk}] (blocks per chunk)")
+        _on_gpu(self.k_pages, v_pages=self.v_pages, page_table=self.page_table)
         n = self.num_chunks if num_chunks is None else int(num_chunks)
         if n > self.num_chunks:
             raise ValueError("num_chunks exceeds the page table")
@@ -249,6 +254,76 @@ def _check(status: int, what: str):
 
 def _default_scale(cache: PagedKVCache, scale):
     return 1.0 / math.sqrt(cache.head_dim) if scale is None else float(scale)
+
+
+# Argument checks.  The C ABI receives raw pointers, so shapes, dtypes, devices and
+# contiguity of tensors can only be checked here; every check runs before anything
+# is launched.  Shape and dtype are checked before the device, so that the checks
+# themselves can be exercised on a machine without a GPU.
+
+def _need(cond: bool, msg: str):
+    if not cond:
+        raise ValueError(msg)
+
+
+def _on_gpu(like: torch.Tensor, like_name: str = "the cache", **tensors):
+    """Every given tensor (None = absent) lives on the GPU that holds `like`."""
+    _need(like.is_cuda, f"{like_name} must live on a GPU")
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        _need(t.is_cuda, f"{name} must be a GPU tensor")
+        _need(t.device == like.device, f"{name} must be on {like.device}, not {t.device}")
+
+
+def _check_tensor(name: str, t, shape, dtype):
+    _need(isinstance(t, torch.Tensor), f"{name} must be a tensor")
+    _need(tuple(t.shape) == tuple(shape), f"{name} must have shape {tuple(shape)}, not {tuple(t.shape)}")
+    _need(t.dtype == dtype, f"{name} must be {dtype}, not {t.dtype}")
+    _need(t.is_contiguous(), f"{name} must be contiguous")
+
+
+def _check_q(cache: "PagedKVCache", q) -> int:
+    """q: [lq, H, d] in the cache's dtype, contiguous.  Returns lq."""
+    _need(isinstance(q, torch.Tensor) and q.dim() == 3, "q must be a [lq, H, d] tensor")
+    lq = int(q.shape[0])
+    _check_tensor("q", q, (lq, cache.num_heads, cache.head_dim), cache.dtype)
+    return lq
+
+
+def _check_outputs(q: torch.Tensor, out, lse):
+    lq, H, d = (int(s) for s in q.shape)
+    if out is not None:
+        _check_tensor("out", out, (lq, H, d), q.dtype)
+    if lse is not None:
+        _check_tensor("lse", lse, (H, lq), torch.float32)
+
+
+def _check_lists(q: torch.Tensor, idx, cnt, group_size: int) -> int:
+    """idx [H, R, K] and cnt [H, R] int32 for R = ceil(lq / group_size).  Returns K."""
+    _need(int(group_size) >= 1, "group_size must be >= 1")
+    lq, H = int(q.shape[0]), int(q.shape[1])
+    R = -(-lq // int(group_size))
+    _need(isinstance(idx, torch.Tensor) and idx.dim() == 3, "idx must be an [H, R, K] tensor")
+    K = int(idx.shape[-1])
+    _need(K >= 1, "idx must hold at least one entry per row")
+    _check_tensor("idx", idx, (H, R, K), torch.int32)
+    _check_tensor("cnt", cnt, (H, R), torch.int32)
+    return K
+
+
+def _check_workspace(ws, need: int, like: torch.Tensor):
+    _need(isinstance(ws, torch.Tensor) and ws.dim() == 1, "workspace must be a 1-D uint8 tensor")
+    _check_tensor("workspace", ws, (int(ws.shape[0]),), torch.uint8)
+    _need(ws.numel() >= need, f"workspace holds {ws.numel()} bytes, {need} needed")
+    _on_gpu(like, workspace=ws)
+
+
+def _check_selection_out(sel: "Selection", H: int, R: int, K: int):
+    _check_tensor("out.idx", sel.idx, (H, R, K), torch.int32)
+    _check_tensor("out.cnt", sel.cnt, (H, R), torch.int32)
+    if sel.score is not None:
+        _check_tensor("out.score", sel.score, (H, R, K), torch.float32)
 
 
 # --------------------------------------------------------------- host helpers
@@ -301,18 +376,25 @@ def omnimem_select(cache: PagedKVCache, q: torch.Tensor, top_k: int, group_size:
                    awe_min_outside_chunks: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
                    want_score: bool = True, workspace: Optional[torch.Tensor] = None,
                    out: Optional[Selection] = None, stream=None) -> Selection:
-    lq, H, d = (int(s) for s in q.shape)
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    _need(int(top_k) >= 1 and int(group_size) >= 1, "top_k and group_size must be >= 1")
     params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
-    desc = cache.descriptor(num_chunks)
     R = -(-lq // group_size)
+    if out is not None:
+        _check_selection_out(out, H, R, int(top_k))
+    desc = cache.descriptor(num_chunks)
     dev = q.device
     if out is None:
         out = Selection(torch.empty((H, R, top_k), dtype=torch.int32, device=dev),
                         torch.empty((H, R), dtype=torch.int32, device=dev),
                         torch.empty((H, R, top_k), dtype=torch.float32, device=dev) if want_score else None, 0)
+    _check_selection_out(out, H, R, int(top_k))
+    _on_gpu(cache.k_pages, q=q, idx=out.idx, cnt=out.cnt, score=out.score)
     need = int(lib().omnimem_select_workspace_bytes(ctypes.byref(desc), lq, ctypes.byref(params)))
     if workspace is None:
         workspace = workspace_tensor(need, dev)
+    _check_workspace(workspace, need, q)
     awe = ctypes.c_int32(0)
     st = lib().omnimem_select(ctypes.byref(desc), _ptr(q), lq, ctypes.byref(params), _ptr(out.idx), _ptr(out.cnt),
                               _ptr(out.score), ctypes.byref(awe), _ptr(workspace), workspace.numel(), _stream(stream))
@@ -325,13 +407,17 @@ def omnimem_sparse_attn(cache: PagedKVCache, q: torch.Tensor, idx: torch.Tensor,
                         group_size: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
                         out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
                         stream=None):
-    lq, H, d = (int(s) for s in q.shape)
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    top_k = _check_lists(q, idx, cnt, group_size)
+    _check_outputs(q, out, lse)
     desc = cache.descriptor(num_chunks)
+    _on_gpu(cache.k_pages, q=q, idx=idx, cnt=cnt, out=out, lse=lse)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
         lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
-    st = lib().omnimem_sparse_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), int(idx.shape[-1]),
+    st = lib().omnimem_sparse_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), top_k,
                                    group_size, _default_scale(cache, scale), _ptr(out), _ptr(lse), _stream(stream))
     _check(st, "omnimem_sparse_attn")
     return out, lse
@@ -341,8 +427,11 @@ def omnimem_dense_attn(cache: PagedKVCache, q: torch.Tensor, chunk_begin: int, c
                        scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
                        out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
                        stream=None):
-    lq, H, d = (int(s) for s in q.shape)
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    _check_outputs(q, out, lse)
     desc = cache.descriptor(num_chunks)
+    _on_gpu(cache.k_pages, q=q, out=out, lse=lse)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
@@ -357,16 +446,22 @@ def omnimem_union_gather_attn(cache: PagedKVCache, q: torch.Tensor, idx: torch.T
                               group_size: int, scale: Optional[float] = None, *, num_chunks: Optional[int] = None,
                               workspace: Optional[torch.Tensor] = None, out: Optional[torch.Tensor] = None,
                               lse: Optional[torch.Tensor] = None, stream=None):
-    lq, H, d = (int(s) for s in q.shape)
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    top_k = _check_lists(q, idx, cnt, group_size)
+    _check_outputs(q, out, lse)
     desc = cache.descriptor(num_chunks)
+    _on_gpu(cache.k_pages, q=q, idx=idx, cnt=cnt, out=out, lse=lse)
     if out is None:
         out = torch.empty_like(q)
     if lse is None:
         lse = torch.empty((H, lq), dtype=torch.float32, device=q.device)
     union_blocks = torch.zeros(1, dtype=torch.int32, device=q.device)
+    need = int(lib().omnimem_union_workspace_bytes(ctypes.byref(desc)))
     if workspace is None:
-        workspace = workspace_tensor(int(lib().omnimem_union_workspace_bytes(ctypes.byref(desc))), q.device)
-    st = lib().omnimem_union_gather_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), int(idx.shape[-1]),
+        workspace = workspace_tensor(need, q.device)
+    _check_workspace(workspace, need, q)
+    st = lib().omnimem_union_gather_attn(ctypes.byref(desc), _ptr(q), lq, _ptr(idx), _ptr(cnt), top_k,
                                          group_size, _default_scale(cache, scale), _ptr(out), _ptr(lse),
                                          _ptr(union_blocks), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "omnimem_union_gather_attn")
@@ -401,6 +496,24 @@ class CompressedCache:
                    torch.zeros(pages, dtype=torch.int32, device=dev),
                    cache.block_size, cache.chunk_tokens, int(capacity_chunks))
 
+    def check_against(self, cache: PagedKVCache):
+        """The pooled tensors must match the full cache's heads, dim, dtype and GPU."""
+        H, d = cache.num_heads, cache.head_dim
+        tokens = max(self.capacity_chunks * cache.blocks_per_chunk, 1)
+        pages = max(1, -(-tokens // CMP_PAGE_TOKENS))
+        _need(self.block_size == cache.block_size and self.chunk_tokens == cache.chunk_tokens,
+              "compressed cache geometry differs from the full cache")
+        _need(self.k_mean.dim() == 3, "k_mean must be [H, capacity*Bpc, d]")
+        _check_tensor("k_mean", self.k_mean, (H, int(self.k_mean.shape[1]), d), torch.float32)
+        _need(int(self.k_mean.shape[1]) >= tokens, "k_mean holds fewer pooled tokens than the capacity")
+        for name, t in (("cmp k_pages", self.k_pages), ("cmp v_pages", self.v_pages)):
+            _need(t.dim() == 4, f"{name} must be [pages, H, {CMP_PAGE_TOKENS}, d]")
+            _check_tensor(name, t, (int(t.shape[0]), H, CMP_PAGE_TOKENS, d), cache.dtype)
+            _need(int(t.shape[0]) >= pages, f"{name} holds fewer pages than the capacity needs")
+        _check_tensor("cmp page_table", self.page_table, (int(self.page_table.shape[0]),), torch.int32)
+        _on_gpu(cache.k_pages, k_mean=self.k_mean, cmp_k_pages=self.k_pages, cmp_v_pages=self.v_pages,
+                cmp_page_table=self.page_table)
+
     def descriptor(self) -> omnimem_cmp_cache_t:
         return omnimem_cmp_cache_t(
             _DTYPES[self.k_pages.dtype], int(self.k_pages.shape[1]), int(self.k_pages.shape[3]), self.block_size,
@@ -410,6 +523,7 @@ class CompressedCache:
 
 def omnimem_compress_chunk(cache: PagedKVCache, chunk: int, cc: CompressedCache, *,
                            num_chunks: Optional[int] = None, stream=None) -> None:
+    cc.check_against(cache)
     desc = cache.descriptor(num_chunks)
     cdesc = cc.descriptor()
     _check(lib().omnimem_compress_chunk(ctypes.byref(desc), int(chunk), ctypes.byref(cdesc), _stream(stream)),
@@ -426,20 +540,28 @@ def omnimem_select_compressed(cache: PagedKVCache, cc: CompressedCache, q: torch
     history is a candidate, as when an LRU hot cache reloads what is selected.
     score_mode=SCORE_PROB ranks by group-mean softmax probabilities over the pooled
     keys instead of group-mean logits."""
-    lq, H, d = (int(s) for s in q.shape)
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    _need(int(top_k) >= 1 and int(group_size) >= 1, "top_k and group_size must be >= 1")
+    cc.check_against(cache)
     params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale),
                            score_mode)
+    R = -(-lq // group_size)
+    if out is not None:
+        _check_selection_out(out, H, R, int(top_k))
     desc = cache.descriptor(num_chunks, with_table=not all_candidates)
     cdesc = cc.descriptor()
-    R = -(-lq // group_size)
     dev = q.device
     if out is None:
         out = Selection(torch.empty((H, R, top_k), dtype=torch.int32, device=dev),
                         torch.empty((H, R), dtype=torch.int32, device=dev),
                         torch.empty((H, R, top_k), dtype=torch.float32, device=dev) if want_score else None, 0)
+    _check_selection_out(out, H, R, int(top_k))
+    _on_gpu(cache.k_pages, q=q, idx=out.idx, cnt=out.cnt, score=out.score)
     need = int(lib().omnimem_select_workspace_bytes(ctypes.byref(desc), lq, ctypes.byref(params)))
     if workspace is None:
         workspace = workspace_tensor(need, dev)
+    _check_workspace(workspace, need, q)
     awe = ctypes.c_int32(0)
     st = lib().omnimem_select_compressed(ctypes.byref(desc), ctypes.byref(cdesc), _ptr(q), lq, ctypes.byref(params),
                                          _ptr(out.idx), _ptr(out.cnt), _ptr(out.score), ctypes.byref(awe),
@@ -452,7 +574,12 @@ def omnimem_select_compressed(cache: PagedKVCache, cc: CompressedCache, q: torch
 def omnimem_cmp_attn(cc: CompressedCache, n_chunks: int, q: torch.Tensor, scale: Optional[float] = None, *,
                      out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None, want_lse: bool = True,
                      stream=None):
-    lq, H, d = (int(s) for s in q.shape)
+    H, d = int(cc.k_pages.shape[1]), int(cc.k_pages.shape[3])
+    _need(isinstance(q, torch.Tensor) and q.dim() == 3, "q must be a [lq, H, d] tensor")
+    lq = int(q.shape[0])
+    _check_tensor("q", q, (lq, H, d), cc.k_pages.dtype)
+    _check_outputs(q, out, lse)
+    _on_gpu(cc.k_pages, "the compressed cache", q=q, out=out, lse=lse, v_pages=cc.v_pages, page_table=cc.page_table)
     if out is None:
         out = torch.empty_like(q)
     if lse is None and want_lse:
@@ -477,6 +604,9 @@ def omnimem_gated_combine(o_cmp: Optional[torch.Tensor], o_slc: Optional[torch.T
             raise ValueError("branch outputs must share shape, dtype and be contiguous")
     if gate_logits.dtype != torch.float32 or tuple(gate_logits.shape) != (lq, H, 3) or not gate_logits.is_contiguous():
         raise ValueError("gate_logits must be a contiguous float32 [lq, H, 3] tensor")
+    if out is not None:
+        _check_tensor("out", out, (lq, H, d), ref.dtype)
+    _on_gpu(ref, "the branch outputs", o_cmp=o_cmp, o_slc=o_slc, o_swa=o_swa, gate_logits=gate_logits, out=out)
     if out is None:
         out = torch.empty_like(ref)
     st = lib().omnimem_gated_combine(_DTYPES[ref.dtype], lq, H, d, _ptr(o_cmp), _ptr(o_slc), _ptr(o_swa),
