@@ -24,7 +24,9 @@
  *    allocates and owns every buffer, including workspaces; the library allocates
  *    no memory (except omnimem_lru_create's host bookkeeping object, released by
  *    omnimem_lru_destroy) and keeps no mutable global state, so calls on
- *    different streams may run concurrently on disjoint outputs.
+ *    different streams may run concurrently on disjoint outputs.  The one
+ *    exception is omnimem_select_noalloc, whose static per-GPU scratch is shared
+ *    by all of its calls.
  *  - All work is enqueued on `stream` (a hipStream_t; NULL = the null stream) and
  *    is asynchronous: no entry point synchronises with the host.
  *  - Arguments are validated on the host before anything is enqueued; on failure
@@ -55,7 +57,8 @@ typedef enum {
   OMNIMEM_EINVAL = -1,      /* a null, misaligned or out-of-range argument */
   OMNIMEM_EUNSUPPORTED = -2,/* a shape or dtype this build has no kernel for */
   OMNIMEM_EWORKSPACE = -3,  /* the workspace is smaller than the size query returns */
-  OMNIMEM_EHIP = -4         /* the HIP runtime reported an error at launch */
+  OMNIMEM_EHIP = -4,        /* the HIP runtime reported an error at launch */
+  OMNIMEM_ESCRATCH = -5     /* the problem needs more than omnimem_select_noalloc's static scratch */
 } omnimem_status_t;
 
 /*
@@ -158,6 +161,26 @@ size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq, 
 omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                 const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt, float* score,
                                 int32_t* awe_active, void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * omnimem_select without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc).  Same contract, outputs and bits as omnimem_select; the
+ * scratch is a static device array of OMNIMEM_NOALLOC_SCRATCH_BYTES inside the
+ * library, one per GPU, held until the process ends.  The call allocates nothing
+ * and calls no allocating routine; the caller still passes q and the outputs.
+ *  - Runs on the current device (hipSetDevice); `stream` must belong to it.
+ *  - Returns OMNIMEM_ESCRATCH, launching nothing, when
+ *    omnimem_select_workspace_bytes(kv, lq, p) exceeds the static size.
+ *  - Every call on one GPU shares that GPU's array: calls that can overlap on one
+ *    GPU (other streams, other host threads) race and must be serialised by the
+ *    caller.  The array keeps the last call's contents; nothing read depends on them.
+ */
+#define OMNIMEM_NOALLOC_SCRATCH_BYTES (8u << 20)
+
+omnimem_status_t omnimem_select_noalloc(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                        const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt, float* score,
+                                        int32_t* awe_active, void* stream);
 
 /*
  * Per-head scattered block-sparse attention (Sec. 3.3 Eq. 5; Alg. 1 Step 2).

@@ -24,6 +24,7 @@ from .omnimem import (  # noqa: F401
     omnimem_gated_combine,
     omnimem_select,
     omnimem_select_compressed,
+    omnimem_select_noalloc,
     omnimem_select_workspace_bytes,
     omnimem_sparse_attn,
     omnimem_status_string,

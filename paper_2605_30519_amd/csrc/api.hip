@@ -4,10 +4,18 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "../../include/omnimem.h"
 #include "launch.h"
 
 #define OMNIMEM_API extern "C" __attribute__((visibility("default")))
+
+// Device scratch of omnimem_select_noalloc, for callers that cannot allocate.  One
+// copy per GPU, alive until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory: only the address resolved per device by
+// hipGetSymbolAddress may be passed to kernels.
+static __device__ __align__(256) unsigned char scratch[OMNIMEM_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -105,22 +113,78 @@ OMNIMEM_API size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, 
   return lq == 0 ? 256 : plan.total;
 }
 
+namespace {
+
+// The checks omnimem_select and omnimem_select_noalloc share (all but the workspace).
+omnimem_status_t check_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                              const omnimem_select_params_t* p, const int32_t* idx, const int32_t* cnt,
+                              CacheGeom& g, omnimem::SelectPlan& plan) {
+  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
+  if (st != OMNIMEM_OK) return st;
+  if (p->score_mode != OMNIMEM_SCORE_LOGIT) return OMNIMEM_EINVAL;  // probabilities need the pooled history
+  if (lq == 0) return OMNIMEM_OK;
+  if (q == nullptr || idx == nullptr || cnt == nullptr || !aligned16(q)) return OMNIMEM_EINVAL;
+  return OMNIMEM_OK;
+}
+
+// Device address of `scratch` on each device, resolved once per device with that
+// device current.
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void* g_scratch_addr[kMaxDevices];
+
+omnimem_status_t scratch_of_current_device(void** addr) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) return OMNIMEM_EHIP;
+  if (dev >= kMaxDevices) return OMNIMEM_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (g_scratch_addr[dev] == nullptr) {
+    void* a = nullptr;
+    if (hipGetSymbolAddress(&a, HIP_SYMBOL(scratch)) != hipSuccess || a == nullptr) return OMNIMEM_EHIP;
+    g_scratch_addr[dev] = a;
+  }
+  *addr = g_scratch_addr[dev];
+  return OMNIMEM_OK;
+}
+
+}  // namespace
+
 OMNIMEM_API omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                             const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt,
                                             float* score, int32_t* awe_active, void* workspace,
                                             size_t workspace_bytes, void* stream) {
   CacheGeom g;
   omnimem::SelectPlan plan;
-  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
+  omnimem_status_t st = check_select(kv, q, lq, p, idx, cnt, g, plan);
   if (st != OMNIMEM_OK) return st;
-  if (p->score_mode != OMNIMEM_SCORE_LOGIT) return OMNIMEM_EINVAL;  // probabilities need the pooled history
+  if (lq > 0) {
+    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
+    if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
+  }
   if (awe_active) *awe_active = plan.awe;
   if (lq == 0) return OMNIMEM_OK;
-  if (q == nullptr || idx == nullptr || cnt == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
-  if (!aligned16(q) || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
-  if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
   return hip_status(
       omnimem::launch_select(g, plan, q, idx, cnt, score, workspace, static_cast<hipStream_t>(stream)));
+}
+
+OMNIMEM_API omnimem_status_t omnimem_select_noalloc(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
+                                                    const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt,
+                                                    float* score, int32_t* awe_active, void* stream) {
+  CacheGeom g;
+  omnimem::SelectPlan plan;
+  omnimem_status_t st = check_select(kv, q, lq, p, idx, cnt, g, plan);
+  if (st != OMNIMEM_OK) return st;
+  if (lq > 0 && plan.total > OMNIMEM_NOALLOC_SCRATCH_BYTES) return OMNIMEM_ESCRATCH;
+  void* ws = nullptr;
+  if (lq > 0) {
+    st = scratch_of_current_device(&ws);
+    if (st != OMNIMEM_OK) return st;
+  }
+  if (awe_active) *awe_active = plan.awe;
+  if (lq == 0) return OMNIMEM_OK;
+  // the kernels write every scratch word they later read, so the previous call's
+  // contents need no clearing
+  return hip_status(omnimem::launch_select(g, plan, q, idx, cnt, score, ws, static_cast<hipStream_t>(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_sparse_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
@@ -349,6 +413,8 @@ OMNIMEM_API const char* omnimem_status_string(int32_t status) {
       return "workspace too small";
     case OMNIMEM_EHIP:
       return "HIP launch error";
+    case OMNIMEM_ESCRATCH:
+      return "selection needs more scratch than omnimem_select_noalloc's static buffer";
     default:
       return "unknown status";
   }

@@ -93,6 +93,7 @@ EXPORTED = [
     "omnimem_awe_active",
     "omnimem_select_workspace_bytes",
     "omnimem_select",
+    "omnimem_select_noalloc",
     "omnimem_sparse_attn",
     "omnimem_dense_attn",
     "omnimem_union_workspace_bytes",
@@ -122,6 +123,8 @@ def _configure(L):
     L.omnimem_select_workspace_bytes.restype = sz
     L.omnimem_select.argtypes = [kvp, vp, i32, pp, vp, vp, vp, ctypes.POINTER(i32), vp, sz, vp]
     L.omnimem_select.restype = i32
+    L.omnimem_select_noalloc.argtypes = [kvp, vp, i32, pp, vp, vp, vp, ctypes.POINTER(i32), vp]
+    L.omnimem_select_noalloc.restype = i32
     L.omnimem_sparse_attn.argtypes = [kvp, vp, i32, vp, vp, i32, i32, f32, vp, vp, vp]
     L.omnimem_sparse_attn.restype = i32
     L.omnimem_dense_attn.argtypes = [kvp, vp, i32, i32, i32, f32, vp, vp, vp]
@@ -399,6 +402,32 @@ def omnimem_select(cache: PagedKVCache, q: torch.Tensor, top_k: int, group_size:
     st = lib().omnimem_select(ctypes.byref(desc), _ptr(q), lq, ctypes.byref(params), _ptr(out.idx), _ptr(out.cnt),
                               _ptr(out.score), ctypes.byref(awe), _ptr(workspace), workspace.numel(), _stream(stream))
     _check(st, "omnimem_select")
+    out.awe_active = int(awe.value)
+    return out
+
+
+NOALLOC_SCRATCH_BYTES = 8 << 20   # OMNIMEM_NOALLOC_SCRATCH_BYTES
+
+
+def omnimem_select_noalloc(cache: PagedKVCache, q: torch.Tensor, top_k: int, group_size: int, window_chunks: int,
+                           awe_min_outside_chunks: int, scale: Optional[float] = None, *, out: Selection,
+                           num_chunks: Optional[int] = None, stream=None) -> Selection:
+    """omnimem_select with the library's static per-GPU scratch instead of a
+    workspace: nothing is allocated, so `out` (idx, cnt and optionally score) must be
+    given.  Runs on the current device; calls that overlap on one GPU race."""
+    lq = _check_q(cache, q)
+    H = cache.num_heads
+    _need(int(top_k) >= 1 and int(group_size) >= 1, "top_k and group_size must be >= 1")
+    _need(out is not None, "out must be given: this call allocates nothing")
+    R = -(-lq // group_size)
+    _check_selection_out(out, H, R, int(top_k))
+    params = select_params(top_k, group_size, window_chunks, awe_min_outside_chunks, _default_scale(cache, scale))
+    desc = cache.descriptor(num_chunks)
+    _on_gpu(cache.k_pages, q=q, idx=out.idx, cnt=out.cnt, score=out.score)
+    awe = ctypes.c_int32(0)
+    st = lib().omnimem_select_noalloc(ctypes.byref(desc), _ptr(q), lq, ctypes.byref(params), _ptr(out.idx),
+                                      _ptr(out.cnt), _ptr(out.score), ctypes.byref(awe), _stream(stream))
+    _check(st, "omnimem_select_noalloc")
     out.awe_active = int(awe.value)
     return out
 

@@ -47,6 +47,7 @@ def test_host_helpers():
     assert L.omnimem_awe_active(-1, 1, 3, 4, 4) == -1
     assert L.omnimem_status_string(0) == b"ok"
     assert L.omnimem_status_string(-3) == b"workspace too small"
+    assert b"static" in L.omnimem_status_string(-5)
     assert L.omnimem_status_string(7) == b"unknown status"
 
 
@@ -157,3 +158,27 @@ def test_attention_validation():
     assert uws >= 12 * 2 * 64 * 64 * 2 * 2
     assert ug(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, FAKE, FAKE, uws - 1, None) == EWS
     assert ug(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, 0, FAKE, uws, None) == EINVAL
+
+
+def test_select_noalloc_validation():
+    """The allocation-free selection shares omnimem_select's checks and refuses a
+    problem larger than its static scratch before touching the device."""
+    L = om.lib()
+    c = cache()
+
+    def call(kv=c, p=params(), lq=256, q=FAKE, idx=FAKE, cnt=FAKE):
+        return L.omnimem_select_noalloc(ctypes.byref(kv), q, lq, ctypes.byref(p), idx, cnt, None, None, None)
+
+    assert call(p=params(top_k=0)) == EINVAL
+    assert call(p=params(score_mode=1)) == EINVAL
+    assert call(q=0) == EINVAL and call(idx=0) == EINVAL and call(cnt=0) == EINVAL
+    assert call(q=FAKE + 2) == EINVAL
+    assert call(kv=cache(head_dim=96)) == EUNSUP
+    # the paper's small groups (G = 15) on a 20-chunk 1.3B layer need about 33 MB
+    big = cache(num_heads=12, head_dim=128, block_size=64, chunk_tokens=4680, num_chunks=20, num_pages=1480)
+    need = L.omnimem_select_workspace_bytes(ctypes.byref(big), 4680, ctypes.byref(params(top_k=4, group_size=15)))
+    assert need > om.NOALLOC_SCRATCH_BYTES
+    assert call(kv=big, lq=4680, p=params(top_k=4, group_size=15)) == -5
+    awe = ctypes.c_int32(-5)
+    assert L.omnimem_select_noalloc(ctypes.byref(c), None, 0, ctypes.byref(params()), None, None, None,
+                                    ctypes.byref(awe), None) == 0 and awe.value == 0
