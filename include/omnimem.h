@@ -79,6 +79,12 @@ typedef enum {
  * page_table: [n][Bpc] int32 page ids.  A negative id marks a block that is not
  *     resident on the GPU: it is never selected and never attended (the pointer
  *     table's 0 entry of App. C).  Ids >= num_pages are treated the same way.
+ * page_table_head_stride: 0 = one table shared by every head.  Otherwise every
+ *     head has a table of its own (App. C's pointer table is indexed by head and
+ *     chunk): head h reads the [n][Bpc] table at page_table + h * stride, and the
+ *     (page, h) slab holds its block, so a page may hold blocks of different
+ *     chunks for different heads.  stride >= n*Bpc.  omnimem_union_gather_attn
+ *     accepts shared tables only (OMNIMEM_EUNSUPPORTED otherwise).
  */
 typedef struct {
   int32_t dtype;        /* omnimem_dtype_t */
@@ -91,6 +97,7 @@ typedef struct {
   const void* k_pages;
   const void* v_pages;
   const int32_t* page_table;
+  int64_t page_table_head_stride; /* 0 = shared by every head; else >= n*Bpc (per-head tables) */
 } omnimem_kv_cache_t;
 
 /*
@@ -328,53 +335,94 @@ omnimem_status_t omnimem_gated_combine(int32_t dtype, int32_t lq, int32_t num_he
                                        const float* gate_logits, void* out, void* stream);
 
 /*
+ * Alg. 1 Step 1's chunk decode, on the device: for every head h and history
+ * chunk c < n,
+ *   needed[h][c] = 1 if some group r < groups lists, among its first cnt[h][r]
+ *                  entries of idx[h][r][0 : top_k], a block b in [0, N_b) with
+ *                  b div Bpc = c; else 0.
+ * idx [H][groups][top_k] and cnt [H][groups] int32 as omnimem_select writes them;
+ * needed [H][n] uint8 (out).  H, n and Bpc come from kv; its pages and page
+ * table are not read (the table may be NULL).  The result is the request of
+ * omnimem_lru_require once copied to the host.
+ */
+omnimem_status_t omnimem_selected_chunks(const omnimem_kv_cache_t* kv, const int32_t* idx, const int32_t* cnt,
+                                         int32_t groups, int32_t top_k, uint8_t* needed, void* stream);
+
+/*
  * GPU hot cache of full-resolution history chunks with LRU eviction (App. B,
  * "Inference and Offloading": the GPU keeps a few chunks, the rest sit in pinned
- * host memory and are reloaded over PCIe when selected; App. F studies its size;
- * Alg. 1's WaitUntilReload).  Host-side runtime state for one layer.
+ * host memory and are reloaded over PCIe when selected; App. F studies the cache's
+ * size; Alg. 1 waits for a selected chunk's reload before reading it).  Host-side
+ * runtime state for one layer.
  *
- * The caller allocates and owns every buffer:
- *   kv->k_pages, kv->v_pages  the GPU page pool: slot t holds a chunk in pages
- *                             [t*Bpc, (t+1)*Bpc); kv->num_pages >= slots*Bpc;
- *   kv->page_table            [kv->num_chunks][Bpc] on the device, written by this
- *                             runtime only: a chunk's row holds its slot's pages while
- *                             it is resident and -1 (not resident) otherwise;
- *   k_host, v_host            pinned host pools (hipHostMalloc) holding every chunk:
- *                             chunk c in pages [c*Bpc, (c+1)*Bpc), the page layout of
- *                             kv ([page][H][B][d]); host_chunks chunks.
- * The residency unit is a chunk of all heads (a page holds every head's copy of a
- * block).  The object keeps host bookkeeping only (no device or pinned memory of its
- * own); it is not thread-safe.  Selection over the compressed history
- * (omnimem_select_compressed with kv->page_table == NULL) needs no chunk resident.
+ * Residency is per (head, chunk), like Alg. 1's pointer table: every head has
+ * `slots` chunk slots and its own least-recently-used order.  The caller
+ * allocates and owns every buffer:
+ *   kv->k_pages, v_pages   the GPU pool, kv->num_pages >= slots*Bpc: slot s of
+ *                          head h is the head-h slabs of pages [s*Bpc, (s+1)*Bpc);
+ *   kv->page_table         per-head tables (kv->page_table_head_stride >= n*Bpc,
+ *                          n = kv->num_chunks >= 1), written by this runtime only:
+ *                          head h's row of chunk c holds the slot's pages while the
+ *                          pair is resident and -1 (not resident) otherwise;
+ *   k_host, v_host         pinned host pools (hipHostMalloc) of host_chunks >= n
+ *                          chunks: chunk c in pages [c*Bpc, (c+1)*Bpc), the page
+ *                          layout of kv ([page][H][B][d]).
+ * The object keeps host bookkeeping and two HIP events (no device or pinned memory
+ * of its own); it is not thread-safe.  Selection over the compressed history
+ * (omnimem_select_compressed with kv->page_table == NULL) needs nothing resident.
  */
 typedef struct omnimem_lru omnimem_lru_t;
 
 typedef struct {
-  int64_t hits, misses, evictions; /* chunks found resident / reloaded / evicted */
+  int64_t hits, misses, evictions; /* (head, chunk) pairs found resident / reloaded / evicted */
   int64_t bytes_reloaded;          /* host-to-device bytes (K and V) */
 } omnimem_lru_stats_t;
 
 /* Creates the state (*out, released by omnimem_lru_destroy) and enqueues on
-   `stream` the write of -1 to every page-table row.  slots >= 1 (G_LRU). */
+   `stream` the write of -1 to every row of every head's table.  slots >= 1. */
 omnimem_status_t omnimem_lru_create(const omnimem_kv_cache_t* kv, int32_t slots, const void* k_host,
                                     const void* v_host, int32_t host_chunks, void* stream, omnimem_lru_t** out);
 void omnimem_lru_destroy(omnimem_lru_t* lru);
 
-/* Makes every chunk in chunks[0:count] (host array; repeats allowed) resident
-   before whatever follows on `stream`: resident chunks count as hits and become
-   most recently used; each other chunk evicts the least recently used chunk not in
-   the request (its row becomes -1), is copied host-to-device into the freed slot
-   (hipMemcpyAsync on `stream`) and gets its row.  The distinct chunks of a request
-   must fit in the slots (else OMNIMEM_EINVAL, nothing changed).  *reloaded (host,
-   may be NULL) receives the number of chunks copied. */
-omnimem_status_t omnimem_lru_require(omnimem_lru_t* lru, const int32_t* chunks, int32_t count, int32_t* reloaded,
-                                     void* stream);
+/*
+ * Makes resident every (head, chunk) pair with needed[h*n + c] != 0 (host array
+ * [H][n], n <= kv->num_chunks; omnimem_selected_chunks computes it).  Per head, in
+ * ascending chunk order: resident pairs are hits and become most recently used;
+ * every other pair takes the head's lowest free slot, else the slot of its least
+ * recently used chunk that the request does not name, and becomes most recently
+ * used; the evicted pair's row becomes -1.
+ * Reloads and row writes are enqueued on copy_stream, after all work already
+ * enqueued on compute_stream (which may still read the slots being reused); the
+ * two may be the same stream.  Nothing on another stream may read the rows of the
+ * evicted chunks meanwhile.  omnimem_lru_wait orders later work after the reloads.
+ * A head that names more chunks than it has slots: OMNIMEM_EINVAL, nothing changed.
+ * *reloaded (host, may be NULL): the number of pairs reloaded.
+ * OMNIMEM_EHIP leaves the runtime unusable (every later call returns it).
+ */
+omnimem_status_t omnimem_lru_require(omnimem_lru_t* lru, const uint8_t* needed, int32_t n, void* compute_stream,
+                                     void* copy_stream, int32_t* reloaded);
+
+/* Makes `stream` wait until the reloads of the last omnimem_lru_require have
+   landed (Alg. 1's WaitUntilReload); no-op if nothing was ever reloaded. */
+omnimem_status_t omnimem_lru_wait(omnimem_lru_t* lru, void* stream);
 
 /* Counters since creation (host). */
 omnimem_status_t omnimem_lru_stats(const omnimem_lru_t* lru, omnimem_lru_stats_t* out);
 
-/* The slot holding `chunk`, or -1 when it is not resident (host). */
-int32_t omnimem_lru_slot_of(const omnimem_lru_t* lru, int32_t chunk);
+/* The slot holding chunk `chunk` of head `head`, or -1 when not resident (host). */
+int32_t omnimem_lru_slot_of(const omnimem_lru_t* lru, int32_t head, int32_t chunk);
+
+/*
+ * Binds the calling thread to the NUMA node of GPU `device`'s PCI function (App. B
+ * binds generation to the node that owns the GPU's PCIe root): its CPU affinity
+ * becomes that node's CPUs among those it may already use, and its memory policy
+ * prefers the node, so pinned host pools it allocates afterwards sit next to the
+ * GPU.  Threads it starts later inherit both.  *node (host, may be NULL): the node
+ * bound, or -1 when the system reports none or the node shares no CPU with the
+ * thread's affinity (nothing is changed then).  OMNIMEM_EINVAL on an unknown
+ * device or a failed system call.
+ */
+omnimem_status_t omnimem_numa_bind(int32_t device, int32_t* node);
 
 #ifdef __cplusplus
 }

@@ -377,6 +377,50 @@ def gated_combine(o_cmp, o_slc, o_swa, gate_logits):
     return out
 
 
+def lru_simulate(requests, slots: int):
+    """The hot cache's replacement policy (App. B: least recently used chunks stay on
+    the GPU; App. F varies the number of slots), for one head.  `requests` is a
+    sequence of collections of chunk ids.  Per request, its distinct chunks are taken
+    in ascending id: a resident chunk is a hit and becomes the most recently used;
+    then each other chunk takes the lowest free slot, or else the slot of the least
+    recently used resident chunk that the request does not name, and becomes the most
+    recently used.  A request naming more than `slots` chunks is an error.
+    Returns dict(slot_of={chunk: slot} after the last request, hits, misses,
+    evictions, per_request=[(hits, misses), ...])."""
+    if slots < 1:
+        raise ValueError("slots must be >= 1")
+    order = []            # resident chunks, least recently used first
+    slot_of = {}
+    hits = misses = evictions = 0
+    per_request = []
+    for req in requests:
+        want = sorted(set(int(c) for c in req))
+        if len(want) > slots:
+            raise ValueError(f"a request names {len(want)} chunks, more than {slots} slots")
+        h0, m0 = hits, misses
+        for c in want:
+            if c in slot_of:
+                order.remove(c)
+                order.append(c)
+                hits += 1
+        for c in want:
+            if c in slot_of:
+                continue
+            free = sorted(set(range(slots)) - set(slot_of.values()))
+            if free:
+                s = free[0]
+            else:
+                victim = next(v for v in order if v not in want)
+                s = slot_of.pop(victim)
+                order.remove(victim)
+                evictions += 1
+            slot_of[c] = s
+            order.append(c)
+            misses += 1
+        per_request.append((hits - h0, misses - m0))
+    return dict(slot_of=slot_of, hits=hits, misses=misses, evictions=evictions, per_request=per_request)
+
+
 def union(idx, cnt, n_blocks: int):
     """Eq. 4 unions: returns (per-head |U_h| [H], cross-head |U|)."""
     idx_a, idx_p = _i32(idx)

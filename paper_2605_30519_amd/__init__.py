@@ -31,5 +31,6 @@ from .omnimem import (  # noqa: F401
     omnimem_union_gather_attn,
     omnimem_union_workspace_bytes,
     select_params,
-    selected_chunks,
+    omnimem_numa_bind,
+    omnimem_selected_chunks,
 )

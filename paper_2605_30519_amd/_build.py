@@ -9,7 +9,12 @@ CSRC = os.path.join(PKG, "csrc")
 OBJ_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libomnimem.so")
 SOURCES = ["api.hip", "select.hip", "prob.hip", "attention.hip", "union_gather.hip", "fuse.hip", "offload.hip"]
-HEADERS = ["device_common.h", "launch.h"]
+# host-only C++ (no HIP): argument checks, work plans, the LRU bookkeeping and the
+# NUMA binding, built by the host compiler; tests also build them under sanitizers
+HOST_SOURCES = ["validate.cpp", "plan.cpp", "lru_core.cpp", "numa.cpp"]
+HEADERS = ["device_common.h", "launch.h", "plan.h", "validate.h", "lru_core.h", "numa.h"]
+CXX = os.environ.get("CXX", "g++")
+HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-fvisibility=hidden", "-Wall"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
@@ -39,6 +44,10 @@ def build(verbose: bool = False) -> str:
     for src in SOURCES:
         obj = os.path.join(OBJ_DIR, src.replace(".hip", ".o"))
         cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+        procs.append((src, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
+    for src in HOST_SOURCES:
+        obj = os.path.join(OBJ_DIR, src.replace(".cpp", ".host.o"))
+        cmd = [CXX, *HOST_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
         procs.append((src, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
     objs = []
     errors = []

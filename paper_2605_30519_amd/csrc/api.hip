@@ -1,13 +1,13 @@
-// api.hip -- the extern "C" entry points of libomnimem.so: host-side validation,
-// workspace planning and kernel launch.  Nothing here allocates memory or
+// api.hip -- the extern "C" entry points of libomnimem.so: the host-side checks
+// of validate.cpp, then the kernel launches.  Nothing here allocates memory or
 // synchronises with the device.
-#include <math.h>
 #include <stdint.h>
 
 #include <mutex>
 
 #include "../../include/omnimem.h"
 #include "launch.h"
+#include "validate.h"
 
 #define OMNIMEM_API extern "C" __attribute__((visibility("default")))
 
@@ -19,113 +19,14 @@ static __device__ __align__(256) unsigned char scratch[OMNIMEM_NOALLOC_SCRATCH_B
 
 namespace {
 
+using omnimem::AttnLaunch;
 using omnimem::CacheGeom;
-
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-// Resolves and validates a cache descriptor.  Returns OMNIMEM_OK or an error.
-// table_optional: a NULL page table is accepted (selection from pooled keys only).
-omnimem_status_t resolve_cache(const omnimem_kv_cache_t* kv, CacheGeom& g, bool table_optional = false) {
-  if (kv == nullptr) return OMNIMEM_EINVAL;
-  if (kv->dtype != OMNIMEM_BF16 && kv->dtype != OMNIMEM_F32) return OMNIMEM_EUNSUPPORTED;
-  if (kv->num_heads < 1 || kv->chunk_tokens < 1 || kv->num_chunks < 0 || kv->num_pages < 0) return OMNIMEM_EINVAL;
-  if (kv->head_dim != 64 && kv->head_dim != 128) return OMNIMEM_EUNSUPPORTED;
-  if (kv->block_size != 64 && kv->block_size != 128) return OMNIMEM_EUNSUPPORTED;
-  g.dtype = kv->dtype == OMNIMEM_BF16 ? 0 : 1;
-  g.H = kv->num_heads;
-  g.D = kv->head_dim;
-  g.B = kv->block_size;
-  g.S = kv->chunk_tokens;
-  g.n = kv->num_chunks;
-  g.Bpc = (g.S + g.B - 1) / g.B;
-  const int64_t nb = static_cast<int64_t>(g.n) * g.Bpc;
-  if (nb > (int64_t{1} << 30)) return OMNIMEM_EINVAL;
-  g.nb = static_cast<int>(nb);
-  g.num_pages = kv->num_pages;
-  // page pool size in elements must fit comfortably in int64 addressing
-  if (g.num_pages > (int64_t{1} << 40) / (static_cast<int64_t>(g.H) * g.B * g.D)) return OMNIMEM_EINVAL;
-  g.k_pages = kv->k_pages;
-  g.v_pages = kv->v_pages;
-  g.page_table = kv->page_table;
-  if (g.nb > 0) {
-    if (g.page_table == nullptr && !table_optional) return OMNIMEM_EINVAL;
-    if (g.num_pages > 0 && (g.k_pages == nullptr || g.v_pages == nullptr)) return OMNIMEM_EINVAL;
-    if (!aligned16(g.k_pages) || !aligned16(g.v_pages) || (reinterpret_cast<uintptr_t>(g.page_table) & 3u))
-      return OMNIMEM_EINVAL;
-  }
-  return OMNIMEM_OK;
-}
+using omnimem::CmpCache;
+using omnimem::SelectPlan;
 
 omnimem_status_t hip_status(hipError_t e) { return e == hipSuccess ? OMNIMEM_OK : OMNIMEM_EHIP; }
 
-bool good_scale(float s) { return isfinite(s) && s > 0.f; }
-
-omnimem_status_t check_attn_common(const CacheGeom& g, const void* q, int32_t lq, const void* out) {
-  (void)g;
-  if (lq < 0) return OMNIMEM_EINVAL;
-  if (lq == 0) return OMNIMEM_OK;
-  if (q == nullptr || out == nullptr || !aligned16(q) || !aligned16(out)) return OMNIMEM_EINVAL;
-  return OMNIMEM_OK;
-}
-
-}  // namespace
-
-OMNIMEM_API int32_t omnimem_blocks_per_chunk(int32_t chunk_tokens, int32_t block_size) {
-  if (chunk_tokens < 1 || block_size < 1) return -1;
-  return (chunk_tokens + block_size - 1) / block_size;
-}
-
-OMNIMEM_API int32_t omnimem_awe_active(int32_t n, int32_t E, int32_t T_out, int32_t K, int32_t Bpc) {
-  if (n < 0 || E < 0 || T_out < 0 || K < 1 || Bpc < 1) return -1;
-  const int64_t outside = n > E ? static_cast<int64_t>(n) - E : 0;
-  return (outside >= T_out && outside * Bpc >= K) ? 1 : 0;
-}
-
-namespace {
-
-omnimem_status_t resolve_select(const omnimem_kv_cache_t* kv, int32_t lq, const omnimem_select_params_t* p,
-                                CacheGeom& g, omnimem::SelectPlan& plan, bool table_optional = false) {
-  omnimem_status_t st = resolve_cache(kv, g, table_optional);
-  if (st != OMNIMEM_OK) return st;
-  if (p == nullptr || lq < 0) return OMNIMEM_EINVAL;
-  if (p->top_k < 1 || p->group_size < 1 || p->window_chunks < 0 || p->awe_min_outside_chunks < 0 ||
-      !good_scale(p->scale) || (p->score_mode != OMNIMEM_SCORE_LOGIT && p->score_mode != OMNIMEM_SCORE_PROB))
-    return OMNIMEM_EINVAL;
-  const int awe = omnimem_awe_active(g.n, p->window_chunks, p->awe_min_outside_chunks, p->top_k, g.Bpc);
-  if (lq == 0) {
-    plan = omnimem::SelectPlan{};
-    plan.awe = awe;
-    return OMNIMEM_OK;
-  }
-  plan = omnimem::plan_select(g, lq, p->top_k, p->group_size, p->window_chunks, p->awe_min_outside_chunks, p->scale,
-                              awe, p->score_mode);
-  return OMNIMEM_OK;
-}
-
-}  // namespace
-
-OMNIMEM_API size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq,
-                                                  const omnimem_select_params_t* p) {
-  CacheGeom g;
-  omnimem::SelectPlan plan;
-  // the size does not depend on the page table (NULL for omnimem_select_compressed)
-  if (resolve_select(kv, lq, p, g, plan, /*table_optional=*/true) != OMNIMEM_OK) return 0;
-  return lq == 0 ? 256 : plan.total;
-}
-
-namespace {
-
-// The checks omnimem_select and omnimem_select_noalloc share (all but the workspace).
-omnimem_status_t check_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
-                              const omnimem_select_params_t* p, const int32_t* idx, const int32_t* cnt,
-                              CacheGeom& g, omnimem::SelectPlan& plan) {
-  omnimem_status_t st = resolve_select(kv, lq, p, g, plan);
-  if (st != OMNIMEM_OK) return st;
-  if (p->score_mode != OMNIMEM_SCORE_LOGIT) return OMNIMEM_EINVAL;  // probabilities need the pooled history
-  if (lq == 0) return OMNIMEM_OK;
-  if (q == nullptr || idx == nullptr || cnt == nullptr || !aligned16(q)) return OMNIMEM_EINVAL;
-  return OMNIMEM_OK;
-}
+hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
 
 // Device address of `scratch` on each device, resolved once per device with that
 // device current.
@@ -149,30 +50,39 @@ omnimem_status_t scratch_of_current_device(void** addr) {
 
 }  // namespace
 
+OMNIMEM_API int32_t omnimem_blocks_per_chunk(int32_t chunk_tokens, int32_t block_size) {
+  return omnimem::blocks_per_chunk(chunk_tokens, block_size);
+}
+
+OMNIMEM_API int32_t omnimem_awe_active(int32_t n, int32_t E, int32_t T_out, int32_t K, int32_t Bpc) {
+  return omnimem::awe_active(n, E, T_out, K, Bpc);
+}
+
+OMNIMEM_API size_t omnimem_select_workspace_bytes(const omnimem_kv_cache_t* kv, int32_t lq,
+                                                  const omnimem_select_params_t* p) {
+  return omnimem::select_workspace_bytes(kv, lq, p);
+}
+
 OMNIMEM_API omnimem_status_t omnimem_select(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                             const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt,
                                             float* score, int32_t* awe_active, void* workspace,
                                             size_t workspace_bytes, void* stream) {
   CacheGeom g;
-  omnimem::SelectPlan plan;
-  omnimem_status_t st = check_select(kv, q, lq, p, idx, cnt, g, plan);
+  SelectPlan plan;
+  omnimem_status_t st = omnimem::check_select(kv, q, lq, p, idx, cnt, g, plan);
+  if (st == OMNIMEM_OK) st = omnimem::check_workspace(plan, lq, workspace, workspace_bytes);
   if (st != OMNIMEM_OK) return st;
-  if (lq > 0) {
-    if (workspace == nullptr || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
-    if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
-  }
   if (awe_active) *awe_active = plan.awe;
   if (lq == 0) return OMNIMEM_OK;
-  return hip_status(
-      omnimem::launch_select(g, plan, q, idx, cnt, score, workspace, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_select(g, plan, q, idx, cnt, score, workspace, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_select_noalloc(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                                     const omnimem_select_params_t* p, int32_t* idx, int32_t* cnt,
                                                     float* score, int32_t* awe_active, void* stream) {
   CacheGeom g;
-  omnimem::SelectPlan plan;
-  omnimem_status_t st = check_select(kv, q, lq, p, idx, cnt, g, plan);
+  SelectPlan plan;
+  omnimem_status_t st = omnimem::check_select(kv, q, lq, p, idx, cnt, g, plan);
   if (st != OMNIMEM_OK) return st;
   if (lq > 0 && plan.total > OMNIMEM_NOALLOC_SCRATCH_BYTES) return OMNIMEM_ESCRATCH;
   void* ws = nullptr;
@@ -184,7 +94,7 @@ OMNIMEM_API omnimem_status_t omnimem_select_noalloc(const omnimem_kv_cache_t* kv
   if (lq == 0) return OMNIMEM_OK;
   // the kernels write every scratch word they later read, so the previous call's
   // contents need no clearing
-  return hip_status(omnimem::launch_select(g, plan, q, idx, cnt, score, ws, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_select(g, plan, q, idx, cnt, score, ws, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_sparse_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
@@ -192,91 +102,30 @@ OMNIMEM_API omnimem_status_t omnimem_sparse_attn(const omnimem_kv_cache_t* kv, c
                                                  int32_t group_size, float scale, void* out, float* lse,
                                                  void* stream) {
   CacheGeom g;
-  omnimem_status_t st = resolve_cache(kv, g);
-  if (st != OMNIMEM_OK) return st;
-  if (top_k < 1 || group_size < 1 || !good_scale(scale)) return OMNIMEM_EINVAL;
-  st = check_attn_common(g, q, lq, out);
+  AttnLaunch a;
+  const omnimem_status_t st = omnimem::check_sparse_attn(kv, q, lq, idx, cnt, top_k, group_size, scale, out, lse, g,
+                                                         a);
   if (st != OMNIMEM_OK || lq == 0) return st;
-  if (idx == nullptr || cnt == nullptr) return OMNIMEM_EINVAL;
-  omnimem::AttnLaunch a{};
-  a.q = q;
-  a.out = out;
-  a.lse = lse;
-  a.lq = lq;
-  a.group_size = group_size;
-  a.R = (lq + group_size - 1) / group_size;
-  a.idx = idx;
-  a.cnt = cnt;
-  a.top_k = top_k;
-  a.scale = scale;
-  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_attention(g, a, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_dense_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
                                                 int32_t chunk_begin, int32_t chunk_end, float scale, void* out,
                                                 float* lse, void* stream) {
   CacheGeom g;
-  omnimem_status_t st = resolve_cache(kv, g);
-  if (st != OMNIMEM_OK) return st;
-  if (chunk_begin < 0 || chunk_end < chunk_begin || chunk_end > g.n || !good_scale(scale)) return OMNIMEM_EINVAL;
-  st = check_attn_common(g, q, lq, out);
+  AttnLaunch a;
+  const omnimem_status_t st = omnimem::check_dense_attn(kv, q, lq, chunk_begin, chunk_end, scale, out, lse, g, a);
   if (st != OMNIMEM_OK || lq == 0) return st;
-  omnimem::AttnLaunch a{};
-  a.q = q;
-  a.out = out;
-  a.lse = lse;
-  a.lq = lq;
-  a.group_size = lq;
-  a.R = 1;
-  a.idx = nullptr;
-  a.cnt = nullptr;
-  a.top_k = 1;
-  a.dense_first_block = chunk_begin * g.Bpc;
-  a.dense_num_blocks = (chunk_end - chunk_begin) * g.Bpc;
-  a.scale = scale;
-  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_attention(g, a, as_stream(stream)));
 }
-
-namespace {
-
-// Validates a compressed cache against the full cache's geometry.
-omnimem_status_t resolve_cmp(const omnimem_cmp_cache_t* cc, const CacheGeom& g, omnimem::CmpCache& c) {
-  if (cc == nullptr) return OMNIMEM_EINVAL;
-  if ((cc->dtype == OMNIMEM_BF16 ? 0 : cc->dtype == OMNIMEM_F32 ? 1 : -1) != g.dtype) return OMNIMEM_EINVAL;
-  if (cc->num_heads != g.H || cc->head_dim != g.D || cc->block_size != g.B || cc->chunk_tokens != g.S)
-    return OMNIMEM_EINVAL;
-  if (cc->capacity_chunks < 0 || cc->num_pages < 0) return OMNIMEM_EINVAL;
-  const int64_t cap = static_cast<int64_t>(cc->capacity_chunks) * g.Bpc;
-  if (cap > (int64_t{1} << 30)) return OMNIMEM_EINVAL;
-  const int64_t pages = (cap + omnimem::kCmpPageTokens - 1) / omnimem::kCmpPageTokens;
-  if (cc->num_pages < pages) return OMNIMEM_EINVAL;
-  if (cap > 0 && (cc->k_mean == nullptr || cc->k_pages == nullptr || cc->v_pages == nullptr ||
-                  cc->page_table == nullptr))
-    return OMNIMEM_EINVAL;
-  if (!aligned16(cc->k_mean) || !aligned16(cc->k_pages) || !aligned16(cc->v_pages) ||
-      (reinterpret_cast<uintptr_t>(cc->page_table) & 3u))
-    return OMNIMEM_EINVAL;
-  c.k_mean = cc->k_mean;
-  c.k_pages = cc->k_pages;
-  c.v_pages = cc->v_pages;
-  c.page_table = cc->page_table;
-  c.num_pages = cc->num_pages;
-  c.cap_blocks = static_cast<int>(cap);
-  return OMNIMEM_OK;
-}
-
-}  // namespace
 
 OMNIMEM_API omnimem_status_t omnimem_compress_chunk(const omnimem_kv_cache_t* kv, int32_t chunk,
                                                     const omnimem_cmp_cache_t* cc, void* stream) {
   CacheGeom g;
-  omnimem_status_t st = resolve_cache(kv, g);
+  CmpCache c;
+  const omnimem_status_t st = omnimem::check_compress_chunk(kv, chunk, cc, g, c);
   if (st != OMNIMEM_OK) return st;
-  omnimem::CmpCache c;
-  st = resolve_cmp(cc, g, c);
-  if (st != OMNIMEM_OK) return st;
-  if (chunk < 0 || chunk >= g.n || chunk >= cc->capacity_chunks) return OMNIMEM_EINVAL;
-  return hip_status(omnimem::launch_compress_chunk(g, c, chunk, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_compress_chunk(g, c, chunk, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t* kv, const omnimem_cmp_cache_t* cc,
@@ -284,91 +133,38 @@ OMNIMEM_API omnimem_status_t omnimem_select_compressed(const omnimem_kv_cache_t*
                                                        int32_t* idx, int32_t* cnt, float* score, int32_t* awe_active,
                                                        void* workspace, size_t workspace_bytes, void* stream) {
   CacheGeom g;
-  omnimem::SelectPlan plan;
-  omnimem_status_t st = resolve_select(kv, lq, p, g, plan, /*table_optional=*/true);
+  SelectPlan plan;
+  CmpCache c;
+  const omnimem_status_t st = omnimem::check_select_compressed(kv, cc, q, lq, p, idx, cnt, workspace,
+                                                               workspace_bytes, g, plan, c);
   if (st != OMNIMEM_OK) return st;
-  omnimem::CmpCache c;
-  st = resolve_cmp(cc, g, c);
-  if (st != OMNIMEM_OK) return st;
-  if (g.n > cc->capacity_chunks) return OMNIMEM_EINVAL;
   if (awe_active) *awe_active = plan.awe;
   if (lq == 0) return OMNIMEM_OK;
-  if (q == nullptr || idx == nullptr || cnt == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
-  if (!aligned16(q) || (reinterpret_cast<uintptr_t>(workspace) & 255u)) return OMNIMEM_EINVAL;
-  if (workspace_bytes < plan.total) return OMNIMEM_EWORKSPACE;
-  return hip_status(omnimem::launch_select_compressed(g, c, plan, q, idx, cnt, score, workspace,
-                                                      static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_select_compressed(g, c, plan, q, idx, cnt, score, workspace, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_cmp_attn(const omnimem_cmp_cache_t* cc, int32_t n_chunks, const void* q,
                                               int32_t lq, float scale, void* out, float* lse, void* stream) {
-  if (cc == nullptr) return OMNIMEM_EINVAL;
-  // the pooled sequence as a one-chunk paged cache of n_chunks * Bpc tokens
-  omnimem_kv_cache_t seq{};
-  seq.dtype = cc->dtype;
-  seq.num_heads = cc->num_heads;
-  seq.head_dim = cc->head_dim;
-  seq.block_size = cc->block_size;
-  seq.chunk_tokens = cc->chunk_tokens;
-  seq.num_chunks = 0;
-  seq.num_pages = 0;
-  CacheGeom full;
-  omnimem_status_t st = resolve_cache(&seq, full);
-  if (st != OMNIMEM_OK) return st;
-  omnimem::CmpCache c;
-  st = resolve_cmp(cc, full, c);
-  if (st != OMNIMEM_OK) return st;
-  if (n_chunks < 0 || n_chunks > cc->capacity_chunks || !good_scale(scale)) return OMNIMEM_EINVAL;
-  const int64_t tokens = static_cast<int64_t>(n_chunks) * full.Bpc;
-  CacheGeom g = full;
-  g.B = omnimem::kCmpPageTokens;
-  g.S = tokens > 0 ? static_cast<int>(tokens) : 1;
-  g.n = tokens > 0 ? 1 : 0;
-  g.Bpc = (g.S + g.B - 1) / g.B;
-  g.nb = g.n * g.Bpc;
-  g.num_pages = c.num_pages;
-  g.k_pages = c.k_pages;
-  g.v_pages = c.v_pages;
-  g.page_table = c.page_table;
-  st = check_attn_common(g, q, lq, out);
+  CacheGeom g;
+  AttnLaunch a;
+  const omnimem_status_t st = omnimem::check_cmp_attn(cc, n_chunks, q, lq, scale, out, lse, g, a);
   if (st != OMNIMEM_OK || lq == 0) return st;
-  omnimem::AttnLaunch a{};
-  a.q = q;
-  a.out = out;
-  a.lse = lse;
-  a.lq = lq;
-  a.group_size = lq;
-  a.R = 1;
-  a.idx = nullptr;
-  a.cnt = nullptr;
-  a.top_k = 1;
-  a.dense_first_block = 0;
-  a.dense_num_blocks = g.nb;
-  a.scale = scale;
-  return hip_status(omnimem::launch_attention(g, a, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_attention(g, a, as_stream(stream)));
 }
 
 OMNIMEM_API omnimem_status_t omnimem_gated_combine(int32_t dtype, int32_t lq, int32_t num_heads, int32_t head_dim,
                                                    const void* o_cmp, const void* o_slc, const void* o_swa,
                                                    const float* gate_logits, void* out, void* stream) {
-  if (dtype != OMNIMEM_BF16 && dtype != OMNIMEM_F32) return OMNIMEM_EUNSUPPORTED;
-  if (head_dim != 64 && head_dim != 128) return OMNIMEM_EUNSUPPORTED;
-  if (lq < 0 || num_heads < 1) return OMNIMEM_EINVAL;
-  if (lq == 0) return OMNIMEM_OK;
-  if (out == nullptr || gate_logits == nullptr || (o_cmp == nullptr && o_slc == nullptr && o_swa == nullptr))
-    return OMNIMEM_EINVAL;
-  if (!aligned16(out) || !aligned16(o_cmp) || !aligned16(o_slc) || !aligned16(o_swa) ||
-      (reinterpret_cast<uintptr_t>(gate_logits) & 3u))
-    return OMNIMEM_EINVAL;
-  const int64_t rows = static_cast<int64_t>(lq) * num_heads;
+  int64_t rows = 0;
+  const omnimem_status_t st = omnimem::check_gated_combine(dtype, lq, num_heads, head_dim, o_cmp, o_slc, o_swa,
+                                                           gate_logits, out, rows);
+  if (st != OMNIMEM_OK || lq == 0) return st;
   return hip_status(omnimem::launch_gated_combine(dtype == OMNIMEM_BF16 ? 0 : 1, rows, head_dim, o_cmp, o_slc, o_swa,
-                                                  gate_logits, out, static_cast<hipStream_t>(stream)));
+                                                  gate_logits, out, as_stream(stream)));
 }
 
 OMNIMEM_API size_t omnimem_union_workspace_bytes(const omnimem_kv_cache_t* kv) {
-  CacheGeom g;
-  if (resolve_cache(kv, g) != OMNIMEM_OK) return 0;
-  return omnimem::plan_union(g).total;
+  return omnimem::union_workspace_bytes(kv);
 }
 
 OMNIMEM_API omnimem_status_t omnimem_union_gather_attn(const omnimem_kv_cache_t* kv, const void* q, int32_t lq,
@@ -377,45 +173,12 @@ OMNIMEM_API omnimem_status_t omnimem_union_gather_attn(const omnimem_kv_cache_t*
                                                        int32_t* union_blocks, void* workspace,
                                                        size_t workspace_bytes, void* stream) {
   CacheGeom g;
-  omnimem_status_t st = resolve_cache(kv, g);
-  if (st != OMNIMEM_OK) return st;
-  if (top_k < 1 || group_size < 1 || !good_scale(scale)) return OMNIMEM_EINVAL;
-  st = check_attn_common(g, q, lq, out);
+  omnimem::UnionPlan up;
+  AttnLaunch a;
+  const omnimem_status_t st = omnimem::check_union_gather(kv, q, lq, idx, cnt, top_k, group_size, scale, out, lse,
+                                                          union_blocks, workspace, workspace_bytes, g, up, a);
   if (st != OMNIMEM_OK || lq == 0) return st;
-  if (idx == nullptr || cnt == nullptr || union_blocks == nullptr || workspace == nullptr) return OMNIMEM_EINVAL;
-  if (reinterpret_cast<uintptr_t>(workspace) & 255u) return OMNIMEM_EINVAL;
-  const omnimem::UnionPlan up = omnimem::plan_union(g);
-  if (workspace_bytes < up.total) return OMNIMEM_EWORKSPACE;
-  omnimem::AttnLaunch a{};
-  a.q = q;
-  a.out = out;
-  a.lse = lse;
-  a.lq = lq;
-  a.group_size = group_size;
-  a.R = (lq + group_size - 1) / group_size;
-  a.idx = idx;
-  a.cnt = cnt;
-  a.top_k = top_k;
-  a.scale = scale;
-  return hip_status(
-      omnimem::launch_union_gather(g, up, a, union_blocks, workspace, static_cast<hipStream_t>(stream)));
+  return hip_status(omnimem::launch_union_gather(g, up, a, union_blocks, workspace, as_stream(stream)));
 }
 
-OMNIMEM_API const char* omnimem_status_string(int32_t status) {
-  switch (status) {
-    case OMNIMEM_OK:
-      return "ok";
-    case OMNIMEM_EINVAL:
-      return "invalid argument";
-    case OMNIMEM_EUNSUPPORTED:
-      return "unsupported shape or dtype";
-    case OMNIMEM_EWORKSPACE:
-      return "workspace too small";
-    case OMNIMEM_EHIP:
-      return "HIP launch error";
-    case OMNIMEM_ESCRATCH:
-      return "selection needs more scratch than omnimem_select_noalloc's static buffer";
-    default:
-      return "unknown status";
-  }
-}
+OMNIMEM_API const char* omnimem_status_string(int32_t status) { return omnimem::status_string(status); }

@@ -36,6 +36,7 @@ struct AttnArgs {
   const void* k_pages;
   const void* v_pages;
   const int32_t* page_table;
+  int64_t pt_stride;  // 0: one table for every head; else head h's table at h * pt_stride
   int64_t num_pages;
   int H, S, B, Bpc, nb;
   int lq, G, R;
@@ -54,20 +55,22 @@ struct AttnArgs {
 template <int TK>
 struct TileWalk {
   const AttnArgs& a;
+  const int32_t* table;  // the head's page table
   const int32_t* list;
   int count;
   int t = 0, sub = 0;
   int64_t page = 0;
   int nvalid = 0;
 
-  __device__ TileWalk(const AttnArgs& args, const int32_t* l, int c) : a(args), list(l), count(c) {}
+  __device__ TileWalk(const AttnArgs& args, const int32_t* pt, const int32_t* l, int c)
+      : a(args), table(pt), list(l), count(c) {}
 
   // position on the next non-empty tile at or after (t, sub); false at the end
   __device__ bool seek() {
     while (t < count) {
       const int id = list ? list[t] : a.dense_first + t;
       if (id >= 0 && id < a.nb) {
-        const int32_t p = a.page_table[id];
+        const int32_t p = table[id];
         if (p >= 0 && p < a.num_pages) {
           const int o = id % a.Bpc;
           const int in_block = (o == a.Bpc - 1 ? a.S - o * a.B : a.B) - sub * TK;
@@ -107,6 +110,11 @@ __device__ __forceinline__ void resolve_tile(const AttnArgs& a, int rows_per_wg,
   row_end = min(row0 + rows_per_wg, g_end);
 }
 
+// The page table head h reads.
+__device__ __forceinline__ const int32_t* head_table(const AttnArgs& a, int h) {
+  return a.page_table + static_cast<int64_t>(h) * a.pt_stride;
+}
+
 __device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const int32_t*& list, int& count) {
   if (a.idx) {
     list = a.idx + static_cast<int64_t>(hr) * a.top_k;
@@ -124,13 +132,14 @@ __device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const in
 // entry per thread, compacted with a block-wide prefix sum; returns the tile count.
 // Contains barriers: every thread of the workgroup must call it.
 template <int NT>
-__device__ int decode_tiles(const AttnArgs& a, const int32_t* list, int count, int first, int2* table, int* scan_tmp) {
+__device__ int decode_tiles(const AttnArgs& a, const int32_t* pt, const int32_t* list, int count, int first,
+                            int2* table, int* scan_tmp) {
   const int e = first + static_cast<int>(threadIdx.x);
   int ntiles = 0, page = 0, nvb = 0;
   if (e < count) {
     const int id = list ? list[e] : a.dense_first + e;
     if (id >= 0 && id < a.nb) {
-      const int32_t p = a.page_table[id];
+      const int32_t p = pt[id];
       if (p >= 0 && p < a.num_pages) {
         const int o = id % a.Bpc;
         nvb = o == a.Bpc - 1 ? a.S - o * a.B : a.B;
@@ -284,7 +293,7 @@ __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
   // tile table: decode list entries NT at a time; `ti` indexes the current table
   int next_entry = 0, ntab = 0, ti = 0;
   while (ntab == 0 && next_entry < count) {
-    ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+    ntab = decode_tiles<NT>(a, head_table(a, h), list, count, next_entry, table, scan_tmp);
     next_entry += NT;
   }
   bool have = ntab > 0;
@@ -304,7 +313,7 @@ __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
       ntab = 0;
       ti = 0;
       while (ntab == 0 && next_entry < count) {
-        ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+        ntab = decode_tiles<NT>(a, head_table(a, h), list, count, next_entry, table, scan_tmp);
         next_entry += NT;
       }
     }
@@ -588,7 +597,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       ntab = 0;
       ti = 0;
       while (ntab == 0 && next_entry < count) {
-        ntab = decode_tiles<NT>(a, list, count, next_entry, table, scan_tmp);
+        ntab = decode_tiles<NT>(a, head_table(a, h), list, count, next_entry, table, scan_tmp);
         next_entry += NT;
       }
       if (ntab == 0) return make_int2(0, 0);  // past the end: an empty tile
@@ -978,7 +987,7 @@ __global__ __launch_bounds__(kWave) void k_attn_f32(AttnArgs a) {
     o[j] = 0.f;
   }
   float m = -INFINITY, l = 0.f;
-  TileWalk<kF32Keys> walk(a, list, count);
+  TileWalk<kF32Keys> walk(a, head_table(a, h), list, count);
   while (walk.seek()) {
     const float* ks = kp + walk.slab_offset(h, D);
     const float* vs = vp + walk.slab_offset(h, D);
@@ -1026,6 +1035,7 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   a.k_pages = g.k_pages;
   a.v_pages = g.v_pages;
   a.page_table = g.page_table;
+  a.pt_stride = g.pt_stride;
   a.num_pages = g.num_pages;
   a.H = g.H;
   a.S = g.S;

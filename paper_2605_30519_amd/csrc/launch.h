@@ -9,6 +9,8 @@
 #include <type_traits>
 #include <utility>
 
+#include "plan.h"
+
 namespace omnimem {
 
 // Launches one kernel and returns that launch's own status.  The runtime's
@@ -40,45 +42,6 @@ struct LaunchStatus {
   }
 };
 
-// Geometry of one paged layer cache, resolved and validated on the host.
-struct CacheGeom {
-  int dtype;          // 0 = bf16, 1 = f32
-  int H, D, B, S;     // heads, head dim, tokens per block, tokens per chunk
-  int n;              // cached history chunks
-  int Bpc;            // blocks per chunk = ceil(S/B)
-  int nb;             // history blocks = n * Bpc
-  int64_t num_pages;
-  const void* k_pages;
-  const void* v_pages;
-  const int32_t* page_table;
-};
-
-// ---------------------------------------------------------------- selection
-struct SelectPlan {
-  int lq, G, R, K;
-  int awe;              // exclusion active
-  int first_excluded;   // blocks >= this id are outside Omega (nb when exclusion is off)
-  float scale;
-  int qsplit;           // row splits per group in the proxy-query reduction
-  bool inline_scores;   // scores computed inside the pooling kernel (small R)
-  // probability-averaged scores (score_mode 1): query slices of at most 128 rows,
-  // either whole groups (multi: gps groups per slice) or parts of one group (spg
-  // slices per group); for parts, one partial row of nb sums per (head, slice);
-  // the pooled keys split into bf16 pieces, 64-key tiles
-  int score_mode;
-  bool prob_multi;
-  int prob_gps, prob_spg, prob_slices, prob_nseg;
-  // workspace carve-up (byte offsets)
-  size_t off_qpart, off_kbar, off_keys, off_part, off_ksplit, total;
-};
-
-constexpr int kQRowsPerSplit = 512;
-constexpr int kProbSliceRows = 128;  // query rows per workgroup of the probability scores
-constexpr int kInlineGroups = 4;
-
-SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe,
-                       int score_mode = 0);
-
 // Probability-averaged score keys (score_mode 1) from pooled keys kbar
 // [H][kbar_stride][D] fp32: order-preserving keys [H][R][nbp], 0 outside Omega.
 hipError_t launch_prob_keys(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
@@ -89,17 +52,6 @@ hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q,
                          float* score, void* workspace, hipStream_t stream);
 
 // ---------------------------------------------------------------- compressed history
-// One pooled key/value per history block, in block order (token t = block t).
-struct CmpCache {
-  float* k_mean;         // [H][cap_blocks][D] fp32 pooled keys
-  void* k_pages;         // [num_pages][H][64][D] pooled keys in the cache dtype
-  void* v_pages;         // same, pooled values
-  int32_t* page_table;   // [num_pages], entry p = p
-  int64_t num_pages;
-  int cap_blocks;        // capacity in pooled tokens
-};
-constexpr int kCmpPageTokens = 64;
-
 hipError_t launch_compress_chunk(const CacheGeom& g, const CmpCache& cc, int chunk, hipStream_t stream);
 
 // Selection with the pooled keys read from cc.k_mean (plan from plan_select).
@@ -107,20 +59,6 @@ hipError_t launch_select_compressed(const CacheGeom& g, const CmpCache& cc, cons
                                     int32_t* idx, int32_t* cnt, float* score, void* workspace, hipStream_t stream);
 
 // ---------------------------------------------------------------- attention
-struct AttnLaunch {
-  const void* q;
-  void* out;
-  float* lse;
-  int lq;
-  int group_size, R;
-  // sparse mode: per-(h, r) lists; dense mode: idx == nullptr, contiguous block range
-  const int32_t* idx;
-  const int32_t* cnt;
-  int top_k;
-  int dense_first_block, dense_num_blocks;
-  float scale;
-};
-
 hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& a, hipStream_t stream);
 
 // ---------------------------------------------------------------- gated fusion (Eq. 1)
@@ -130,13 +68,6 @@ hipError_t launch_gated_combine(int dtype, int64_t rows, int D, const void* o_cm
                                 const void* o_swa, const float* gate, void* out, hipStream_t stream);
 
 // ---------------------------------------------------------------- union gather
-struct UnionPlan {
-  size_t off_flags, off_pos, off_table, off_kbuf, off_vbuf, total;
-  int64_t slab_bytes;  // one (page, head) slab
-};
-
-UnionPlan plan_union(const CacheGeom& g);
-
 hipError_t launch_union_gather(const CacheGeom& g, const UnionPlan& up, const AttnLaunch& a, int32_t* union_blocks,
                                void* workspace, hipStream_t stream);
 

@@ -63,6 +63,7 @@ struct ProbArgs {
   uint32_t* keys;       // [H][R][nbp]
   int nbp, first_excluded;
   const int32_t* page_table;
+  int64_t pt_stride;
   int64_t num_pages;
 };
 
@@ -350,7 +351,7 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
         for (int r = j * a.G; r < r_end; ++r) sum += red[r * kPRedStride + col];
         const int b = b0 + col;
         if (b < a.nb) {
-          const int32_t pg = a.page_table != nullptr ? a.page_table[b] : 0;
+          const int32_t pg = a.page_table != nullptr ? a.page_table[static_cast<int64_t>(h) * a.pt_stride + b] : 0;
           const bool live = b < a.first_excluded && pg >= 0 && (a.page_table == nullptr || pg < a.num_pages);
           a.keys[(static_cast<int64_t>(h) * a.R + seg0 + j) * a.nbp + b] =
               live ? score_key(sum / static_cast<float>(r_end - j * a.G)) : 0u;
@@ -375,7 +376,8 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
 // Slices that are parts of one group: the group's parts summed in order.
 __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restrict__ part, int nseg, int nb, int nbp,
                                                           int lq, int G, int R, int spg,
-                                                          const int32_t* __restrict__ page_table, int64_t num_pages,
+                                                          const int32_t* __restrict__ page_table, int64_t pt_stride,
+                                                          int64_t num_pages,
                                                           int first_excluded, uint32_t* __restrict__ keys) {
   const int b = blockIdx.x * kPThreads + threadIdx.x, r = blockIdx.y, h = blockIdx.z;
   if (b >= nb) return;
@@ -384,7 +386,7 @@ __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restric
   const int parts = (rows + kPRows - 1) / kPRows;
   for (int k = 0; k < parts; ++k) s += part[(static_cast<int64_t>(h) * nseg + r * spg + k) * nb + b];
   s = s / static_cast<float>(rows);
-  const int32_t p = page_table != nullptr ? page_table[b] : 0;
+  const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
   const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
   keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(s) : 0u;
 }
@@ -416,6 +418,7 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   a.nbp = nbp;
   a.first_excluded = p.first_excluded;
   a.page_table = g.page_table;
+  a.pt_stride = g.pt_stride;
   a.num_pages = g.num_pages;
   if (a.multi)
     st(k_prob_partial<T, D, true>, dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
@@ -424,7 +427,7 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   if (!a.multi) {
     const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
     st(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R, p.prob_spg,
-       g.page_table, g.num_pages, p.first_excluded, keys);
+       g.page_table, g.pt_stride, g.num_pages, p.first_excluded, keys);
   }
   return st.err;
 }

@@ -177,6 +177,7 @@ __device__ __forceinline__ void sum_slab(const uint4 (&raw)[SlabShape<T, D, B>::
 struct PoolArgs {
   const void* k_pages;
   const int32_t* page_table;
+  int64_t pt_stride;  // per-head tables: head h's row of block b at h * pt_stride + b
   int64_t num_pages;
   int H, S, Bpc, nb, first_excluded;
   const float* qpart;  // [H][R][nsplit][D] partial row sums of Q
@@ -203,8 +204,9 @@ __global__ __launch_bounds__(kThreads) void k_pool_score(PoolArgs a) {
   const T* pages = static_cast<const T*>(a.k_pages);
 
   int32_t page_ids[kMaxBlocksPerWave];  // the wave's page ids, loaded together before any slab
+  const int32_t* table = a.page_table + static_cast<int64_t>(h) * a.pt_stride;
 #pragma unroll
-  for (int i = 0; i < kMaxBlocksPerWave; ++i) page_ids[i] = first + i < last ? a.page_table[first + i] : -1;
+  for (int i = 0; i < kMaxBlocksPerWave; ++i) page_ids[i] = first + i < last ? table[first + i] : -1;
   auto live = [&](int i) {
     const int64_t page = page_ids[i];
     return first + i < last && first + i < a.first_excluded && page >= 0 && page < a.num_pages;
@@ -277,8 +279,9 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kbar, int64_t kbar_stride,
                                                     const float* __restrict__ qpart,
                                                     int nsplit, int lq, int G, const int32_t* __restrict__ page_table,
-                                                    int64_t num_pages, int nb, int nbp, int first_excluded, int R,
-                                                    float scale, uint32_t* __restrict__ keys) {
+                                                    int64_t pt_stride, int64_t num_pages, int nb, int nbp,
+                                                    int first_excluded, int R, float scale,
+                                                    uint32_t* __restrict__ keys) {
   constexpr int TB = 64, TR = 16;
   __shared__ float ks[TB][D + 1];
   __shared__ float qs[TR][D + 1];
@@ -301,7 +304,7 @@ __global__ __launch_bounds__(kThreads) void k_score(const float* __restrict__ kb
     float dot = 0.f;
     for (int j = 0; j < D; ++j) dot += qs[rr][j] * ks[bb][j];
     // no page table: every block is a candidate (residency is managed elsewhere)
-    const int32_t p = page_table != nullptr ? page_table[b] : 0;
+    const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
     const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
     keys[(static_cast<int64_t>(h) * R + r) * nbp + b] = live ? score_key(scale * dot) : 0u;
   }
@@ -317,9 +320,9 @@ constexpr int kScoreRowsPerWave = 8;
 template <int D, int NR>
 __global__ __launch_bounds__(kThreads) void k_score_rows(const float* __restrict__ kbar, int64_t kbar_stride,
                                                          const float* __restrict__ qpart, int nsplit, int lq, int G,
-                                                         const int32_t* __restrict__ page_table, int64_t num_pages,
-                                                         int nb, int nbp, int first_excluded, int R, float scale,
-                                                         uint32_t* __restrict__ keys) {
+                                                         const int32_t* __restrict__ page_table, int64_t pt_stride,
+                                                         int64_t num_pages, int nb, int nbp, int first_excluded, int R,
+                                                         float scale, uint32_t* __restrict__ keys) {
   constexpr int PL = D / kWave;  // dimensions per lane: 2 (d = 128) or 1 (d = 64)
   const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, h = blockIdx.y;
   const int first = (blockIdx.x * (kThreads / kWave) + wave) * kScoreRowsPerWave;
@@ -345,7 +348,7 @@ __global__ __launch_bounds__(kThreads) void k_score_rows(const float* __restrict
   for (int i = 0; i < kScoreRowsPerWave; ++i) {
     const int b = first + i;
     if (b >= nb) break;
-    const int32_t p = page_table != nullptr ? page_table[b] : 0;
+    const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
     const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
 #pragma unroll
     for (int r = 0; r < NR; ++r) {
@@ -372,9 +375,9 @@ constexpr int kScoreTiledMinGroups = 32;
 template <int D>
 __global__ __launch_bounds__(kThreads) void k_score_tiled(const float* __restrict__ kbar, int64_t kbar_stride,
                                                           const float* __restrict__ qpart, int nsplit, int lq, int G,
-                                                          const int32_t* __restrict__ page_table, int64_t num_pages,
-                                                          int nb, int nbp, int first_excluded, int R, float scale,
-                                                          uint32_t* __restrict__ keys) {
+                                                          const int32_t* __restrict__ page_table, int64_t pt_stride,
+                                                          int64_t num_pages, int nb, int nbp, int first_excluded,
+                                                          int R, float scale, uint32_t* __restrict__ keys) {
   constexpr int TB = 64, TR = 64, KC = 32, STRIDE = 96;
   __shared__ __align__(16) float ks[KC][STRIDE];  // [dimension][block]
   __shared__ __align__(16) float qs[KC][STRIDE];  // [dimension][group]
@@ -442,7 +445,7 @@ __global__ __launch_bounds__(kThreads) void k_score_tiled(const float* __restric
   // accumulator element i of lane l: group wr + 8 (i / 4) + 4 (l / 32) + i % 4, block wb + l % 32
   const int b = b0 + wb + lane % 32;
   if (b >= nb) return;
-  const int32_t p = page_table != nullptr ? page_table[b] : 0;
+  const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
   const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
 #pragma unroll
   for (int i = 0; i < 16; ++i) {
@@ -459,6 +462,7 @@ struct CompressArgs {
   const void* k_pages;
   const void* v_pages;
   const int32_t* page_table;
+  int64_t pt_stride;
   int64_t num_pages;
   int H, S, Bpc, chunk;
   float* k_mean;
@@ -495,7 +499,7 @@ __global__ __launch_bounds__(kThreads) void k_compress_chunk(CompressArgs a) {
   if (o >= a.Bpc) return;
   const int b = a.chunk * a.Bpc + o;
   const int c = lane % Sh::CPR;
-  const int64_t page = a.page_table[b];
+  const int64_t page = a.page_table[static_cast<int64_t>(h) * a.pt_stride + b];
   const bool live = page >= 0 && page < a.num_pages;
   const int nvalid = o == a.Bpc - 1 ? a.S - o * B : B;
   float ks[VEC], vs[VEC];
@@ -863,8 +867,6 @@ __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict_
   if (lane == 0) cnt[row] = total < K ? total : K;
 }
 
-inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
-
 template <int D>
 hipError_t launch_score(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride,
                         const float* qpart, int nbp, uint32_t* keys, hipStream_t stream) {
@@ -873,19 +875,19 @@ hipError_t launch_score(const CacheGeom& g, const SelectPlan& p, const float* kb
     const dim3 grid((waves + kThreads / kWave - 1) / (kThreads / kWave), g.H);
     if (p.R == 1)
       return launch_kernel(k_score_rows<D, 1>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit,
-                           p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+                           p.lq, p.G, g.page_table, g.pt_stride, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
     return launch_kernel(k_score_rows<D, kInlineGroups>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart,
-                         p.qsplit, p.lq, p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale,
+                         p.qsplit, p.lq, p.G, g.page_table, g.pt_stride, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale,
                          keys);
   }
   if (p.R >= kScoreTiledMinGroups) {
     const dim3 grid((g.nb + 63) / 64, (p.R + 63) / 64, g.H);
     return launch_kernel(k_score_tiled<D>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq,
-                         p.G, g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+                         p.G, g.page_table, g.pt_stride, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
   }
   const dim3 grid((g.nb + 63) / 64, (p.R + 15) / 16, g.H);
   return launch_kernel(k_score<D>, grid, dim3(kThreads), 0, stream, kbar, kbar_stride, qpart, p.qsplit, p.lq, p.G,
-                       g.page_table, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
+                       g.page_table, g.pt_stride, g.num_pages, g.nb, nbp, p.first_excluded, p.R, p.scale, keys);
 }
 
 // Proxy-query partial sums: two 512-thread workgroups per 512-row split (one per
@@ -930,6 +932,7 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
     PoolArgs a;
     a.k_pages = g.k_pages;
     a.page_table = g.page_table;
+    a.pt_stride = g.pt_stride;
     a.num_pages = g.num_pages;
     a.H = g.H;
     a.S = g.S;
@@ -967,57 +970,13 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
 
 }  // namespace
 
-SelectPlan plan_select(const CacheGeom& g, int lq, int K, int G, int E, int T_out, float scale, int awe,
-                       int score_mode) {
-  (void)T_out;
-  SelectPlan p{};
-  p.score_mode = score_mode;
-  p.lq = lq;
-  p.G = G;
-  p.R = (lq + G - 1) / G;
-  p.K = K;
-  p.awe = awe;
-  p.first_excluded = awe ? (g.n - E) * g.Bpc : g.nb;
-  p.scale = scale;
-  const int rows = G < lq ? G : lq;
-  p.qsplit = (rows + kQRowsPerSplit - 1) / kQRowsPerSplit;
-  p.inline_scores = p.R <= kInlineGroups;
-  size_t off = 0;
-  p.off_qpart = off;
-  off = align256(off + static_cast<size_t>(g.H) * p.R * p.qsplit * g.D * sizeof(float));
-  p.off_kbar = off;
-  if (!p.inline_scores) off = align256(off + static_cast<size_t>(g.H) * g.nb * g.D * sizeof(float));
-  p.off_keys = off;
-  off = align256(off + static_cast<size_t>(g.H) * p.R * ((g.nb + 3) / 4 * 4 + (g.nb == 0)) * sizeof(uint32_t));
-  p.off_part = off;
-  if (score_mode == 1) {
-    constexpr int kSliceRows = kProbSliceRows;
-    p.prob_multi = G <= kSliceRows / 2;
-    if (p.prob_multi) {
-      p.prob_gps = kSliceRows / G;
-      p.prob_spg = 1;
-      p.prob_slices = (p.R + p.prob_gps - 1) / p.prob_gps;
-      p.prob_nseg = p.R;
-    } else {
-      p.prob_gps = 1;
-      p.prob_spg = (rows + kSliceRows - 1) / kSliceRows;
-      p.prob_slices = p.R * p.prob_spg;
-      p.prob_nseg = p.prob_slices;
-    }
-    if (!p.prob_multi) off = align256(off + static_cast<size_t>(g.H) * p.prob_nseg * g.nb * sizeof(float));
-    p.off_ksplit = off;
-    off = align256(off + static_cast<size_t>(g.H) * ((g.nb + 63) / 64) * 2 * 64 * g.D * sizeof(uint16_t));
-  }
-  p.total = off;
-  return p;
-}
-
 template <typename T, int D>
 hipError_t launch_compress_typed(const CacheGeom& g, const CmpCache& cc, int chunk, hipStream_t stream) {
   CompressArgs a;
   a.k_pages = g.k_pages;
   a.v_pages = g.v_pages;
   a.page_table = g.page_table;
+  a.pt_stride = g.pt_stride;
   a.num_pages = g.num_pages;
   a.H = g.H;
   a.S = g.S;

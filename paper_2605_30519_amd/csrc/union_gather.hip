@@ -65,28 +65,7 @@ __global__ __launch_bounds__(256) void k_union_gather(const uint4* __restrict__ 
   }
 }
 
-inline size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
-
 }  // namespace
-
-UnionPlan plan_union(const CacheGeom& g) {
-  UnionPlan u{};
-  const size_t eb = g.dtype == 0 ? 2 : 4;
-  u.slab_bytes = static_cast<int64_t>(g.B) * g.D * eb;
-  const size_t nb = g.nb > 0 ? g.nb : 1;
-  size_t off = 0;
-  u.off_flags = off;
-  off = align256(off + nb * sizeof(int32_t));
-  u.off_pos = off;  // unused (kept for layout stability)
-  u.off_table = off;
-  off = align256(off + nb * sizeof(int32_t));
-  u.off_kbuf = off;
-  off = align256(off + nb * g.H * static_cast<size_t>(u.slab_bytes));
-  u.off_vbuf = off;
-  off = align256(off + nb * g.H * static_cast<size_t>(u.slab_bytes));
-  u.total = off;
-  return u;
-}
 
 hipError_t launch_union_gather(const CacheGeom& g, const UnionPlan& up, const AttnLaunch& a, int32_t* union_blocks,
                                void* workspace, hipStream_t stream) {
@@ -115,6 +94,7 @@ hipError_t launch_union_gather(const CacheGeom& g, const UnionPlan& up, const At
   gu.k_pages = kbuf;
   gu.v_pages = vbuf;
   gu.page_table = table;
+  gu.pt_stride = 0;
   gu.num_pages = nb;
   return launch_attention(gu, a, stream);
 }

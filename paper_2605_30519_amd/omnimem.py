@@ -45,6 +45,7 @@ class omnimem_kv_cache_t(ctypes.Structure):
         ("k_pages", ctypes.c_void_p),
         ("v_pages", ctypes.c_void_p),
         ("page_table", ctypes.c_void_p),
+        ("page_table_head_stride", ctypes.c_int64),
     ]
 
 
@@ -103,15 +104,38 @@ EXPORTED = [
     "omnimem_select_compressed",
     "omnimem_cmp_attn",
     "omnimem_gated_combine",
+    "omnimem_selected_chunks",
     "omnimem_lru_create",
     "omnimem_lru_destroy",
     "omnimem_lru_require",
+    "omnimem_lru_wait",
     "omnimem_lru_stats",
     "omnimem_lru_slot_of",
+    "omnimem_numa_bind",
 ]
 
 
-def _configure(L):
+class _Present:
+    """Attribute sink for a symbol a partial build does not export (sanitizer tests)."""
+
+
+def _configure(L, required: bool = True):
+    """Declares every exported function's signature on the loaded library L.  With
+    required=False, functions L does not export are skipped (a host-only test build)."""
+    if not required:
+        class _Partial:
+            def __init__(self, lib):
+                self._lib = lib
+
+            def __getattr__(self, name):
+                try:
+                    return getattr(self._lib, name)
+                except AttributeError:
+                    f = _Present()
+                    object.__setattr__(self, name, f)
+                    return f
+        _configure(_Partial(L))
+        return L
     i32, i64, vp, f32, sz = ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_size_t
     kvp = ctypes.POINTER(omnimem_kv_cache_t)
     pp = ctypes.POINTER(omnimem_select_params_t)
@@ -148,12 +172,18 @@ def _configure(L):
     L.omnimem_lru_create.restype = i32
     L.omnimem_lru_destroy.argtypes = [vp]
     L.omnimem_lru_destroy.restype = None
-    L.omnimem_lru_require.argtypes = [vp, ctypes.POINTER(i32), i32, ctypes.POINTER(i32), vp]
+    L.omnimem_lru_require.argtypes = [vp, vp, i32, vp, vp, ctypes.POINTER(i32)]
     L.omnimem_lru_require.restype = i32
+    L.omnimem_lru_wait.argtypes = [vp, vp]
+    L.omnimem_lru_wait.restype = i32
     L.omnimem_lru_stats.argtypes = [vp, ctypes.POINTER(omnimem_lru_stats_t)]
     L.omnimem_lru_stats.restype = i32
-    L.omnimem_lru_slot_of.argtypes = [vp, i32]
+    L.omnimem_lru_slot_of.argtypes = [vp, i32, i32]
     L.omnimem_lru_slot_of.restype = i32
+    L.omnimem_selected_chunks.argtypes = [kvp, vp, vp, i32, i32, vp, vp]
+    L.omnimem_selected_chunks.restype = i32
+    L.omnimem_numa_bind.argtypes = [i32, ctypes.POINTER(i32)]
+    L.omnimem_numa_bind.restype = i32
     return L
 
 
@@ -179,8 +209,9 @@ def library_path() -> str:
 class PagedKVCache:
     """One layer's paged KV cache (device tensors owned by the caller).
 
-    k_pages, v_pages: [num_pages, H, B, d] (bf16 or fp32); page_table: [n, Bpc] int32,
-    negative = block not resident."""
+    k_pages, v_pages: [num_pages, H, B, d] (bf16 or fp32); page_table: [n, Bpc] int32
+    shared by every head, or [H, n, Bpc] with one table per head (the (page, h) slab
+    then holds head h's block); negative = block not resident."""
     k_pages: torch.Tensor
     v_pages: torch.Tensor
     page_table: torch.Tensor
@@ -200,7 +231,11 @@ class PagedKVCache:
 
     @property
     def num_chunks(self) -> int:
-        return int(self.page_table.shape[0])
+        return int(self.page_table.shape[-2])
+
+    @property
+    def per_head_tables(self) -> bool:
+        return self.page_table.dim() == 3
 
     @property
     def blocks_per_chunk(self) -> int:
@@ -226,8 +261,11 @@ class PagedKVCache:
             raise TypeError("page_table must be int32")
         if self.k_pages.dim() != 4 or self.v_pages.shape != self.k_pages.shape:
             raise ValueError("k_pages and v_pages must share one [num_pages, H, B, d] shape")
-        if self.page_table.dim() != 2 or int(self.page_table.shape[1]) != self.blocks_per_chunk:
-            raise ValueError(f"page_table must be [n, {self.blocks_per_chunk}] (blocks per chunk)")
+        if not (self.page_table.dim() == 2 or (self.page_table.dim() == 3 and
+                                               int(self.page_table.shape[0]) == self.num_heads)) \
+                or int(self.page_table.shape[-1]) != self.blocks_per_chunk:
+            raise ValueError(f"page_table must be [n, {self.blocks_per_chunk}] or "
+                             f"[{self.num_heads}, n, {self.blocks_per_chunk}] (blocks per chunk)")
         _on_gpu(self.k_pages, v_pages=self.v_pages, page_table=self.page_table)
         n = self.num_chunks if num_chunks is None else int(num_chunks)
         if n > self.num_chunks:
@@ -235,7 +273,8 @@ class PagedKVCache:
         return omnimem_kv_cache_t(
             _DTYPES[self.k_pages.dtype], self.num_heads, self.head_dim, self.block_size, self.chunk_tokens, n,
             int(self.k_pages.shape[0]), self.k_pages.data_ptr(), self.v_pages.data_ptr(),
-            self.page_table.data_ptr() if with_table else None)
+            self.page_table.data_ptr() if with_table else None,
+            self.num_chunks * self.blocks_per_chunk if self.per_head_tables else 0)
 
 
 def _stream(stream):
@@ -646,14 +685,45 @@ def omnimem_gated_combine(o_cmp: Optional[torch.Tensor], o_slc: Optional[torch.T
 
 # ------------------------------------------------------------ LRU hot cache
 
+def omnimem_selected_chunks(cache: PagedKVCache, sel_idx: torch.Tensor, sel_cnt: torch.Tensor, *,
+                            num_chunks: Optional[int] = None, out: Optional[torch.Tensor] = None,
+                            stream=None) -> torch.Tensor:
+    """Alg. 1 Step 1's chunk decode on the device: [H, n] uint8, 1 where some group of
+    head h selected a block of chunk c."""
+    _need(isinstance(sel_idx, torch.Tensor) and sel_idx.dim() == 3, "idx must be an [H, R, K] tensor")
+    H, R, K = (int(s) for s in sel_idx.shape)
+    _need(H == cache.num_heads, f"idx must have {cache.num_heads} heads")
+    _check_tensor("idx", sel_idx, (H, R, K), torch.int32)
+    _check_tensor("cnt", sel_cnt, (H, R), torch.int32)
+    n = cache.num_chunks if num_chunks is None else int(num_chunks)
+    if out is not None:
+        _check_tensor("out", out, (H, n), torch.uint8)
+    desc = cache.descriptor(num_chunks)
+    _on_gpu(cache.k_pages, idx=sel_idx, cnt=sel_cnt, out=out)
+    if out is None:
+        out = torch.empty((H, n), dtype=torch.uint8, device=sel_idx.device)
+    _check(lib().omnimem_selected_chunks(ctypes.byref(desc), _ptr(sel_idx), _ptr(sel_cnt), R, K, _ptr(out),
+                                         _stream(stream)), "omnimem_selected_chunks")
+    return out
+
+
+def omnimem_numa_bind(device: int = 0) -> int:
+    """Binds the calling thread to the NUMA node of GPU `device` (affinity and memory
+    policy); returns the node, or -1 when there is none to bind."""
+    node = ctypes.c_int32(-1)
+    _check(lib().omnimem_numa_bind(int(device), ctypes.byref(node)), "omnimem_numa_bind")
+    return int(node.value)
+
+
 class LruOffload:
-    """GPU hot cache of full-resolution history chunks with LRU eviction (the
-    library's host runtime).  `gpu` is the GPU pool as a PagedKVCache: k_pages /
-    v_pages of slots*Bpc pages, page_table [n, Bpc] (written by the runtime only).
-    k_host / v_host: pinned CPU tensors [host_chunks*Bpc, H, B, d], chunk c in pages
-    [c*Bpc, (c+1)*Bpc)."""
+    """GPU hot cache of full-resolution history chunks with a per-(head, chunk) LRU
+    (the library's host runtime).  `gpu` is the GPU pool as a PagedKVCache with
+    per-head tables: k_pages / v_pages of at least slots*Bpc pages, page_table
+    [H, n, Bpc] (written by the runtime only).  k_host / v_host: pinned CPU tensors
+    [host_chunks*Bpc, H, B, d], chunk c in pages [c*Bpc, (c+1)*Bpc)."""
 
     def __init__(self, gpu: PagedKVCache, slots: int, k_host: torch.Tensor, v_host: torch.Tensor, stream=None):
+        _need(gpu.per_head_tables, "the GPU pool needs per-head page tables [H, n, Bpc]")
         for t in (k_host, v_host):
             if t.device.type != "cpu" or not t.is_pinned() or not t.is_contiguous() or t.dtype != gpu.dtype:
                 raise ValueError("host pools must be contiguous pinned CPU tensors of the cache dtype")
@@ -668,20 +738,36 @@ class LruOffload:
                                         self.host_chunks, _stream(stream), ctypes.byref(h)), "omnimem_lru_create")
         self._h = h
 
-    def require(self, chunks, stream=None) -> int:
-        arr = (ctypes.c_int32 * max(len(chunks), 1))(*[int(c) for c in chunks])
+    def require(self, needed, compute_stream=None, copy_stream=None) -> int:
+        """needed: [H, n] host uint8 array or tensor (1 = make resident).  Reloads run on
+        copy_stream (default: the compute stream) after the work already enqueued on
+        compute_stream (default: the current stream)."""
+        if isinstance(needed, torch.Tensor):
+            needed = needed.detach()
+            _need(needed.device.type == "cpu", "needed must be a host tensor (copy it from the GPU first)")
+            arr = needed.to(torch.uint8).contiguous().numpy()
+        else:
+            import numpy as np
+            arr = np.ascontiguousarray(np.asarray(needed, dtype=np.uint8))
+        _need(arr.ndim == 2 and arr.shape[0] == self.gpu.num_heads, f"needed must be [{self.gpu.num_heads}, n]")
+        cs = _stream(compute_stream)
+        xs = cs if copy_stream is None else _stream(copy_stream)
         got = ctypes.c_int32(0)
-        _check(lib().omnimem_lru_require(self._h, arr, len(chunks), ctypes.byref(got), _stream(stream)),
-               "omnimem_lru_require")
+        _check(lib().omnimem_lru_require(self._h, arr.ctypes.data_as(ctypes.c_void_p), int(arr.shape[1]), cs, xs,
+                                         ctypes.byref(got)), "omnimem_lru_require")
         return int(got.value)
+
+    def wait(self, stream=None):
+        """Orders `stream` (default: the current stream) after the last reloads."""
+        _check(lib().omnimem_lru_wait(self._h, _stream(stream)), "omnimem_lru_wait")
 
     def stats(self) -> dict:
         st = omnimem_lru_stats_t()
         _check(lib().omnimem_lru_stats(self._h, ctypes.byref(st)), "omnimem_lru_stats")
         return {"hits": st.hits, "misses": st.misses, "evictions": st.evictions, "bytes_reloaded": st.bytes_reloaded}
 
-    def slot_of(self, chunk: int) -> int:
-        return int(lib().omnimem_lru_slot_of(self._h, int(chunk)))
+    def slot_of(self, head: int, chunk: int) -> int:
+        return int(lib().omnimem_lru_slot_of(self._h, int(head), int(chunk)))
 
     def close(self):
         if getattr(self, "_h", None) is not None and self._h.value:
@@ -693,10 +779,3 @@ class LruOffload:
             self.close()
         except Exception:
             pass
-
-
-def selected_chunks(sel: Selection, blocks_per_chunk: int) -> list:
-    """The distinct history chunks a selection reads (host list; synchronises)."""
-    idx = sel.idx.reshape(-1)
-    ids = idx[idx >= 0]
-    return sorted(set((ids // blocks_per_chunk).tolist()))

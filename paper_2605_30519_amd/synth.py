@@ -195,9 +195,47 @@ def page_layer(k: torch.Tensor, v: torch.Tensor, block_size: int, seed: int = 0,
     return PagedKVCache(k_pages, v_pages, table, S)
 
 
+def page_layer_per_head(k: torch.Tensor, v: torch.Tensor, block_size: int, seed: int = 0, pad_value: float = 0.0,
+                        nonresident: Optional[dict] = None, extra_pages: int = 0) -> PagedKVCache:
+    """Like page_layer, with one page table per head ([H, n, Bpc]): head h's block b
+    goes to the (page, h) slab of its own seeded permutation, so one page holds
+    blocks of different chunks for different heads.  nonresident: {head: block ids}
+    marked -1 in that head's table only."""
+    n, S, H, d = (int(s) for s in k.shape)
+    B = block_size
+    Bpc = -(-S // B)
+    nblocks = n * Bpc
+    num_pages = nblocks + extra_pages
+    dev = k.device
+    k_pages = torch.full((num_pages, H, B, d), pad_value, dtype=k.dtype, device=dev)
+    v_pages = torch.full((num_pages, H, B, d), pad_value, dtype=v.dtype, device=dev)
+    tables = []
+    pad = Bpc * B - S
+    for h in range(H):
+        perm = torch.randperm(max(num_pages, 1), generator=_gen(seed * 1009 + h, "cpu"))[:nblocks].to(torch.int32)
+        if nblocks:
+            pidx = perm.to(device=dev, dtype=torch.long)
+            for src, dst in ((k, k_pages), (v, v_pages)):
+                x = src[:, :, h]
+                if pad:
+                    x = torch.cat([x, torch.full((n, pad, d), pad_value, dtype=x.dtype, device=dev)], dim=1)
+                dst[pidx, h] = x.reshape(nblocks, B, d)
+        t = perm.clone()
+        for b in (nonresident or {}).get(h, ()):
+            t[int(b)] = -1
+        tables.append(t.reshape(n, Bpc))
+    return PagedKVCache(k_pages, v_pages, torch.stack(tables).to(dev).contiguous(), S)
+
+
 def resident_mask(cache: PagedKVCache, n_chunks: Optional[int] = None) -> torch.Tensor:
-    """[n*Bpc] bool, True where the page table holds a page (host tensor)."""
+    """[n*Bpc] bool (shared table) or [H, n*Bpc] (per-head tables), True where the
+    page table holds a page (host tensor)."""
     t = cache.page_table.cpu()
+    if t.dim() == 3:
+        if n_chunks is not None:
+            t = t[:, :n_chunks]
+        t = t.reshape(t.shape[0], -1)
+        return (t >= 0) & (t < cache.k_pages.shape[0])
     if n_chunks is not None:
         t = t[:n_chunks]
     return (t.reshape(-1) >= 0) & (t.reshape(-1) < cache.k_pages.shape[0])

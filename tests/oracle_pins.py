@@ -517,4 +517,39 @@ def pin_widening_of_stored_types():
     assert np.array_equal(o1, o3) and np.array_equal(l1, l3)
 
 
+def pin_lru_policy():
+    # The textbook page-replacement example (Silberschatz, Galvin and Gagne,
+    # "Operating System Concepts", the LRU example on 3 frames): this reference string
+    # gives 12 faults under LRU (15 under FIFO, 9 under the optimal policy).
+    ref = [7, 0, 1, 2, 0, 3, 0, 4, 2, 3, 0, 3, 2, 1, 2, 0, 1, 7, 0, 1]
+    r = O.lru_simulate([[c] for c in ref], 3)
+    assert (r["misses"], r["hits"], r["evictions"]) == (12, 8, 9), r
+    # with one chunk per request, LRU keeps exactly the last `slots` distinct chunks
+    # requested (scanning the history backwards)
+    rng = np.random.default_rng(81)
+    for slots in (1, 2, 4):
+        seq = rng.integers(0, 7, 40).tolist()
+        for t in range(1, len(seq) + 1):
+            r = O.lru_simulate([[c] for c in seq[:t]], slots)
+            last = []
+            for c in reversed(seq[:t]):
+                if c not in last:
+                    last.append(c)
+                if len(last) == slots:
+                    break
+            assert set(r["slot_of"]) == set(last), (slots, t)
+    # enough slots: only the first use of each chunk misses; slots fill from 0
+    r = O.lru_simulate([[4, 1], [1, 9], [4], [2, 9]], 5)
+    assert (r["misses"], r["hits"], r["evictions"]) == (4, 3, 0)
+    assert r["slot_of"] == {1: 0, 4: 1, 9: 2, 2: 3}
+    # a request's chunks are all resident afterwards, and the evicted chunk is the
+    # least recently used one the request does not name: after [0,1], [2,3], [1],
+    # the order is 0, 2, 3, 1; [0, 5] keeps 0 (a hit) and evicts 2
+    r = O.lru_simulate([[0, 1], [2, 3], [1], [0, 5]], 4)
+    assert set(r["slot_of"]) == {0, 1, 3, 5} and r["slot_of"][5] == 2 and r["per_request"][-1] == (1, 1)
+    # hits refresh recency: after [0], [1], [0], a new chunk evicts 1 (not 0)
+    r = O.lru_simulate([[0], [1], [0], [2]], 2)
+    assert set(r["slot_of"]) == {0, 2} and r["slot_of"][2] == 1
+
+
 ALL_PINS = [obj for name, obj in sorted(globals().items()) if name.startswith("pin_") and callable(obj)]

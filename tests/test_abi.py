@@ -14,6 +14,12 @@ HEADER = os.path.join(ROOT, "include", "omnimem.h")
 FAKE = 0x10000  # aligned, never dereferenced: every call below fails validation first
 
 
+def abi():
+    """The library the validation cases run against: libomnimem.so here; the
+    sanitizer test swaps in a host-only build of the same checks."""
+    return om.lib()
+
+
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
@@ -77,8 +83,7 @@ def params(**kw):
 
 EINVAL, EUNSUP, EWS = -1, -2, -3
 
-
-@pytest.mark.parametrize("kw,want", [
+CACHE_CASES = [
     (dict(dtype=7), EUNSUP),
     (dict(head_dim=96), EUNSUP),
     (dict(block_size=32), EUNSUP),
@@ -89,9 +94,15 @@ EINVAL, EUNSUP, EWS = -1, -2, -3
     (dict(page_table=0), EINVAL),
     (dict(k_pages=0), EINVAL),
     (dict(k_pages=FAKE + 8), EINVAL),
-])
+    (dict(page_table_head_stride=-1), EINVAL),
+    (dict(page_table_head_stride=11), EINVAL),     # per-head tables hold all n*Bpc = 12 blocks
+    (dict(page_table=FAKE + 2), EINVAL),
+]
+
+
+@pytest.mark.parametrize("kw,want", CACHE_CASES)
 def test_cache_validation(kw, want):
-    L = om.lib()
+    L = abi()
     c = cache(**kw)
     st = L.omnimem_sparse_attn(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, None)
     assert st == want
@@ -100,7 +111,7 @@ def test_cache_validation(kw, want):
 
 
 def test_select_validation():
-    L = om.lib()
+    L = abi()
     c = cache()
     ws = L.omnimem_select_workspace_bytes(ctypes.byref(c), 256, ctypes.byref(params()))
     assert ws > 0 and ws % 256 == 0
@@ -136,7 +147,7 @@ def test_select_validation():
 
 
 def test_attention_validation():
-    L = om.lib()
+    L = abi()
     c = cache()
     sp = L.omnimem_sparse_attn
     assert sp(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 0, 256, 0.125, FAKE, None, None) == EINVAL
@@ -163,7 +174,7 @@ def test_attention_validation():
 def test_select_noalloc_validation():
     """The allocation-free selection shares omnimem_select's checks and refuses a
     problem larger than its static scratch before touching the device."""
-    L = om.lib()
+    L = abi()
     c = cache()
 
     def call(kv=c, p=params(), lq=256, q=FAKE, idx=FAKE, cnt=FAKE):
@@ -182,3 +193,35 @@ def test_select_noalloc_validation():
     awe = ctypes.c_int32(-5)
     assert L.omnimem_select_noalloc(ctypes.byref(c), None, 0, ctypes.byref(params()), None, None, None,
                                     ctypes.byref(awe), None) == 0 and awe.value == 0
+
+
+def test_per_head_tables_and_chunk_decode_validation():
+    """Per-head page tables are accepted where they are supported and refused by the
+    union-gather comparator; the chunk decode checks its lists and mask."""
+    L = abi()
+    c = cache(page_table_head_stride=12)
+    assert L.omnimem_sparse_attn(ctypes.byref(c), None, 0, None, None, 4, 256, 0.125, None, None, None) == 0
+    uws = L.omnimem_union_workspace_bytes(ctypes.byref(c))
+    assert L.omnimem_union_gather_attn(ctypes.byref(c), FAKE, 256, FAKE, FAKE, 4, 256, 0.125, FAKE, None, FAKE, FAKE,
+                                       uws, None) == EUNSUP
+    sc = L.omnimem_selected_chunks
+    assert sc(ctypes.byref(c), FAKE, FAKE, 1, 0, FAKE, None) == EINVAL          # top_k < 1
+    assert sc(ctypes.byref(c), FAKE, FAKE, -1, 4, FAKE, None) == EINVAL         # groups < 0
+    assert sc(ctypes.byref(c), 0, FAKE, 1, 4, FAKE, None) == EINVAL             # no idx
+    assert sc(ctypes.byref(c), FAKE, FAKE + 2, 1, 4, FAKE, None) == EINVAL      # misaligned cnt
+    assert sc(ctypes.byref(c), FAKE, FAKE, 1, 4, 0, None) == EINVAL             # no mask
+    assert sc(ctypes.byref(cache(num_chunks=0)), FAKE, FAKE, 1, 4, 0, None) == 0  # empty history: nothing to do
+    assert sc(ctypes.byref(cache(head_dim=96)), FAKE, FAKE, 1, 4, FAKE, None) == EUNSUP
+
+
+def test_gated_combine_validation():
+    L = abi()
+    g = L.omnimem_gated_combine
+    assert g(2, 8, 2, 64, FAKE, None, None, FAKE, FAKE, None) == EUNSUP        # dtype
+    assert g(0, 8, 2, 96, FAKE, None, None, FAKE, FAKE, None) == EUNSUP        # head_dim
+    assert g(0, -1, 2, 64, FAKE, None, None, FAKE, FAKE, None) == EINVAL
+    assert g(0, 8, 2, 64, None, None, None, FAKE, FAKE, None) == EINVAL        # no branch
+    assert g(0, 8, 2, 64, FAKE, FAKE + 8, None, FAKE, FAKE, None) == EINVAL    # misaligned branch
+    assert g(0, 8, 2, 64, FAKE, None, None, FAKE + 2, FAKE, None) == EINVAL    # misaligned gates
+    assert g(0, 8, 2, 64, FAKE, None, None, FAKE, None, None) == EINVAL        # no output
+    assert g(0, 0, 2, 64, None, None, None, None, None, None) == 0             # empty: no-op

@@ -1,19 +1,27 @@
 """The LRU hot cache of full-resolution chunks (App. B "Inference and Offloading",
-App. F, Alg. 1's WaitUntilReload) through the C ABI: selection from the compressed
-history with every block a candidate, the selected chunks made resident by
-omnimem_lru_require (reloaded from pinned host pools into a pool of a few GPU
-slots), then selection attention over the hot cache.  The attention output must
-equal, bit for bit, the same kernel over the fully resident cache: only the
-physical pages differ.  The bookkeeping (hits, misses, evictions, page-table rows)
-is checked against an LRU simulated on the host.
+App. F, Alg. 1's pointer table and WaitUntilReload) through the C ABI.
+
+Each step selects from the compressed history with every block a candidate,
+decodes the selected (head, chunk) pairs on the GPU (omnimem_selected_chunks,
+Alg. 1 Step 1), makes them resident with omnimem_lru_require (reloads on a second
+stream from pinned host pools into each head's few GPU slots), orders the
+attention after the reloads (omnimem_lru_wait) and runs selection attention over
+the hot cache.  Checked at every step:
+  * the attention output against the fp64 oracle on the same selection, and bit
+    for bit against the same kernel over a fully resident cache;
+  * the chunk decode against the selected ids;
+  * per head, the slots, hits, misses and evictions against the oracle's model of
+    the LRU policy (oracle.lru_simulate), and the page-table rows against the slots;
+  * the reloaded pages against the host pages.
 """
 import numpy as np
 import pytest
 import torch
 
-from paper_2605_30519_amd import (CompressedCache, LruOffload, PagedKVCache, omnimem_compress_chunk,
-                                  omnimem_select_compressed, omnimem_sparse_attn, selected_chunks, synth)
-from parity import say
+import oracle
+from paper_2605_30519_amd import (CompressedCache, LruOffload, OmniMemError, PagedKVCache, omnimem_compress_chunk,
+                                  omnimem_select_compressed, omnimem_selected_chunks, omnimem_sparse_attn, synth)
+from parity import check_bf16, check_f32, say
 
 pytestmark = pytest.mark.gpu
 NAN = float("nan")
@@ -42,33 +50,36 @@ def host_pools(x, B, pad_value=NAN):
     return pools
 
 
-def simulate_lru(requests, slots):
-    """Host model of the policy: per request, hits refresh recency; misses fill a free
-    slot or evict the least recently used chunk not in the request."""
-    resident, clock, hits, misses, evictions = {}, 0, 0, 0, 0
-    for req in requests:
-        want = list(dict.fromkeys(req))
-        for c in want:
-            if c in resident:
-                clock += 1
-                resident[c] = clock
-                hits += 1
-        for c in want:
-            if c in resident:
-                continue
-            if len(resident) >= slots:
-                victim = min((k for k in resident if k not in want), key=lambda k: resident[k])
-                del resident[victim]
-                evictions += 1
-            clock += 1
-            resident[c] = clock
-            misses += 1
-    return set(resident), hits, misses, evictions
+def gpu_pool(H, d, B, S, n, slots, dtype, dev):
+    Bpc = -(-S // B)
+    return PagedKVCache(torch.zeros((slots * Bpc, H, B, d), dtype=dtype, device=dev),
+                        torch.zeros((slots * Bpc, H, B, d), dtype=dtype, device=dev),
+                        torch.zeros((H, n, Bpc), dtype=torch.int32, device=dev), S)
+
+
+def check_state(lru, pool, requests, slots, H, n, Bpc):
+    """Slots, counters and page-table rows against the oracle's LRU model, per head."""
+    table = pool.page_table.cpu().numpy()
+    hits = misses = evictions = 0
+    for h in range(H):
+        ref = oracle.lru_simulate(requests[h], slots)
+        got = {c: lru.slot_of(h, c) for c in range(n) if lru.slot_of(h, c) >= 0}
+        assert got == ref["slot_of"], (h, got, ref["slot_of"])
+        for c in range(n):
+            s = got.get(c, -1)
+            want = np.arange(s * Bpc, s * Bpc + Bpc) if s >= 0 else np.full(Bpc, -1)
+            assert np.array_equal(table[h, c], want), (h, c, table[h, c], s)
+        hits, misses, evictions = hits + ref["hits"], misses + ref["misses"], evictions + ref["evictions"]
+    st = lru.stats()
+    assert (st["hits"], st["misses"], st["evictions"]) == (hits, misses, evictions), (st, hits, misses, evictions)
+    return st
 
 
 @pytest.mark.parametrize("dtype", [torch.bfloat16, torch.float32])
-def test_lru_hot_cache_matches_resident(dev, dtype):
-    H, d, S, Lq, B, n, K, G, E, T = 2, 128, 300, 257, 64, 8, 3, 100, 1, 2
+def test_lru_hot_cache_against_oracle(dev, dtype):
+    # K = 2 blocks for each of R = 2 groups: a head reads at most 4 chunks per step,
+    # within its 5 slots; the requests between steps evict some of them
+    H, d, S, Lq, B, n, K, G, E, T = 3, 128, 300, 257, 64, 8, 2, 150, 1, 2
     say(f"lru hot cache {dtype}")
     w = synth.Workload("lru", H, d, S, Lq, B, n, n, K, G, E, T, dtype, dtype == torch.bfloat16, 1, 10)
     x = synth.make_layer(w, 0, device=dev)
@@ -78,79 +89,100 @@ def test_lru_hot_cache_matches_resident(dev, dtype):
     for c in range(n):
         omnimem_compress_chunk(full, c, cc)
     k_host, v_host = host_pools(x, B)
-    slots = 7
-    pool = PagedKVCache(torch.zeros((slots * Bpc, H, B, d), dtype=dtype, device=dev),
-                        torch.zeros((slots * Bpc, H, B, d), dtype=dtype, device=dev),
-                        torch.zeros((n, Bpc), dtype=torch.int32, device=dev), S)
+    slots = 5
+    pool = gpu_pool(H, d, B, S, n, slots, dtype, dev)
+    copy = torch.cuda.Stream()
     lru = LruOffload(pool, slots, k_host, v_host)
     torch.cuda.synchronize()
     assert (pool.page_table == -1).all()
-    with pytest.raises(Exception):   # more distinct chunks than slots
-        lru.require(list(range(n)))
-    requests, last = [], []
-    for step in range(6):
+    requests = [[] for _ in range(H)]
+    rng = np.random.default_rng(3)
+    for step in range(7):
         if step:
-            # other work between steps touches chunks outside the last selection, so that
-            # some of the next selection's chunks have been evicted and must be reloaded
-            other = [c for c in range(n) if c not in last][: 2 + step % 2]
-            requests.append(other)
-            lru.require(other)
-        # queries of several AR steps: different selections over the same history
+            # other work between steps touches other chunks, so that some of the next
+            # selection's chunks have been evicted and must be reloaded
+            other = (rng.random((H, n)) < 0.35).astype(np.uint8)
+            for h in range(H):
+                while other[h].sum() > slots:
+                    other[h, np.nonzero(other[h])[0][-1]] = 0
+                requests[h].append(np.nonzero(other[h])[0].tolist())
+            lru.require(other, copy_stream=copy)
         q = synth.queries(w, 0, n + step, x.rel, dev) if step else x.q
         sel = omnimem_select_compressed(pool, cc, q, K, G, E, T, w.scale, all_candidates=True)
-        chunks = selected_chunks(sel, Bpc)
-        assert len(chunks) <= slots, chunks
-        requests.append(chunks)
-        got = lru.require(chunks)
-        say(f"  step {step}: chunks {chunks}, reloaded {got}")
+        needed_dev = omnimem_selected_chunks(pool, sel.idx, sel.cnt)
+        needed = needed_dev.cpu()
+        idx, cnt = sel.idx.cpu().numpy(), sel.cnt.cpu().numpy()
+        want = np.zeros((H, n), np.uint8)
+        for h in range(H):
+            for r in range(idx.shape[1]):
+                for b in idx[h, r, : cnt[h, r]]:
+                    want[h, b // Bpc] = 1
+        assert np.array_equal(needed.numpy(), want)
+        for h in range(H):
+            requests[h].append(np.nonzero(want[h])[0].tolist())
+        got = lru.require(needed, copy_stream=copy)
+        lru.wait()
+        say(f"  step {step}: {int(want.sum())} (head, chunk) pairs, reloaded {got}")
         out, lse = omnimem_sparse_attn(pool, q, sel.idx, sel.cnt, G, w.scale)
         ref, ref_lse = omnimem_sparse_attn(full, q, sel.idx, sel.cnt, G, w.scale)
         torch.cuda.synchronize()
         view = torch.int16 if dtype == torch.bfloat16 else torch.int32
         assert torch.equal(out.view(view), ref.view(view)) and torch.equal(lse, ref_lse)
-        table = pool.page_table.cpu().numpy()
+        o_ref, l_ref, hs, qs = oracle.sparse_attn(q.cpu(), x.k.cpu(), x.v.cpu(), B, idx, cnt, G, w.scale)
+        (check_bf16 if dtype == torch.bfloat16 else check_f32)(out.float().cpu().numpy()[qs, hs], o_ref,
+                                                               f"hot-cache sparse step {step}")
+        st = check_state(lru, pool, requests, slots, H, n, Bpc)
+    page_bytes = B * d * (2 if dtype == torch.bfloat16 else 4)
+    assert st["bytes_reloaded"] == 2 * st["misses"] * Bpc * page_bytes
+    # the reloaded slabs hold the host slabs
+    for h in range(H):
         for c in range(n):
-            slot = lru.slot_of(c)
-            want_row = np.arange(slot * Bpc, slot * Bpc + Bpc) if slot >= 0 else np.full(Bpc, -1)
-            assert np.array_equal(table[c], want_row), (c, table[c], slot)
-        last = chunks
-    resident, hits, misses, evictions = simulate_lru(requests, slots)
-    st = lru.stats()
-    assert (st["hits"], st["misses"], st["evictions"]) == (hits, misses, evictions), (st, hits, misses, evictions)
-    assert {c for c in range(n) if lru.slot_of(c) >= 0} == resident
-    page_bytes = H * B * d * (2 if dtype == torch.bfloat16 else 4)
-    assert st["bytes_reloaded"] == 2 * misses * Bpc * page_bytes
+            s = lru.slot_of(h, c)
+            if s < 0:
+                continue
+            for pool_t, host_t in ((pool.k_pages, k_host), (pool.v_pages, v_host)):
+                a = pool_t[s * Bpc:(s + 1) * Bpc, h].cpu()
+                b = host_t[c * Bpc:(c + 1) * Bpc, h]
+                assert torch.equal(a.view(torch.int16) if dtype == torch.bfloat16 else a.view(torch.int32),
+                                   b.view(torch.int16) if dtype == torch.bfloat16 else b.view(torch.int32))
     lru.close()
 
 
 def test_lru_policy_and_errors(dev):
-    """Thrash and reuse patterns against the host model; oversized requests and bad
-    chunk ids are refused without changing anything."""
-    H, d, S, B, n = 1, 64, 64, 64, 6
+    """Thrash and reuse patterns per head against the oracle's model; a head that asks
+    for more chunks than it has slots, and a request longer than the table, are
+    refused without changing anything; waiting with nothing reloaded is a no-op."""
+    H, d, S, B, n = 2, 64, 64, 64, 6
     w = synth.Workload("lru2", H, d, S, 8, B, n, n, 2, 8, 0, 0, torch.bfloat16, False, 1, 11)
     x = synth.make_layer(w, 0, device=dev)
     k_host, v_host = host_pools(x, B)
     slots = 3
-    pool = PagedKVCache(torch.zeros((slots, H, B, d), dtype=torch.bfloat16, device=dev),
-                        torch.zeros((slots, H, B, d), dtype=torch.bfloat16, device=dev),
-                        torch.zeros((n, 1), dtype=torch.int32, device=dev), S)
+    pool = gpu_pool(H, d, B, S, n, slots, torch.bfloat16, dev)
     lru = LruOffload(pool, slots, k_host, v_host)
-    reqs = [[0, 1], [2], [0, 3], [4, 5], [1, 1, 1], [5, 4], [2, 3, 0]]
-    for r in reqs:
-        lru.require(r)
-    resident, hits, misses, evictions = simulate_lru(reqs, slots)
-    st = lru.stats()
-    assert (st["hits"], st["misses"], st["evictions"]) == (hits, misses, evictions)
-    assert {c for c in range(n) if lru.slot_of(c) >= 0} == resident
-    # the reloaded pages hold the host pages
+    lru.wait()
+    reqs = [([0, 1], [5]), ([2], [5, 4]), ([0, 3], [1, 2, 3]), ([4, 5], []), ([1], [0]), ([5, 4], [1]),
+            ([2, 3, 0], [4])]
+    requests = [[], []]
+    for a, b in reqs:
+        needed = np.zeros((H, n), np.uint8)
+        needed[0, a] = 1
+        needed[1, b] = 1
+        requests[0].append(a)
+        requests[1].append(b)
+        lru.require(needed)
+    lru.wait()
     torch.cuda.synchronize()
-    for c in resident:
-        s = lru.slot_of(c)
-        assert torch.equal(pool.k_pages[s].cpu().view(torch.int16), k_host[c].view(torch.int16))
-        assert torch.equal(pool.v_pages[s].cpu().view(torch.int16), v_host[c].view(torch.int16))
+    check_state(lru, pool, requests, slots, H, n, 1)
+    for h in range(H):
+        for c in range(n):
+            s = lru.slot_of(h, c)
+            if s >= 0:
+                assert torch.equal(pool.k_pages[s, h].cpu().view(torch.int16), k_host[c, h].view(torch.int16))
     before = lru.stats()
-    for bad in ([0, 1, 2, 3], [6], [-1]):
-        with pytest.raises(Exception):
+    too_many = np.zeros((H, n), np.uint8)
+    too_many[1, :4] = 1
+    for bad in (too_many, np.zeros((H, n + 1), np.uint8), np.zeros((H + 1, n), np.uint8)):
+        with pytest.raises((OmniMemError, ValueError)):
             lru.require(bad)
     assert lru.stats() == before
     lru.close()

@@ -395,3 +395,56 @@ def test_wan14b_stress(dev):
     say(f"  union {tot} of {omega} candidate blocks ({100.0 * tot / omega:.1f}%), sum_h |U_h| = {int(per.sum())}")
     assert int(ub.item()) == tot and tot > 0.8 * omega
     assert torch.equal(uout.view(torch.int16), out.view(torch.int16)) and torch.equal(ulse, lse)
+
+
+def test_per_head_page_tables(dev):
+    """The same layer paged with one table per head (each head's blocks on pages of
+    its own permutation, so a page holds different chunks for different heads):
+    selection, sparse, dense and union-free outputs equal the shared-table ones bit
+    for bit, and blocks made non-resident for one head only are skipped for that
+    head alone, against the oracle head by head."""
+    H, d, S, Lq, B, n, K, G = 3, 128, 300, 300, 64, 6, 7, 130
+    w = synth.Workload("perhead", H, d, S, Lq, B, n, n, K, G, 1, 2, torch.bfloat16, True, 1, 7)
+    x = synth.make_layer(w, 0, device=dev)
+    shared = synth.page_layer(x.k, x.v, B, seed=3, pad_value=NAN)
+    per = synth.page_layer_per_head(x.k, x.v, B, seed=4, pad_value=NAN)
+    say("per-head tables: same data, other pages")
+    a = run_select(shared, x, w)
+    b = run_select(per, x, w)
+    assert torch.equal(a.idx, b.idx) and torch.equal(a.cnt, b.cnt) and torch.equal(a.score, b.score)
+    for cache_pair in ((shared, per),):
+        o1, l1 = omnimem_sparse_attn(cache_pair[0], x.q, a.idx, a.cnt, G, w.scale)
+        o2, l2 = omnimem_sparse_attn(cache_pair[1], x.q, a.idx, a.cnt, G, w.scale)
+        d1, m1 = omnimem_dense_attn(cache_pair[0], x.q, 0, n, w.scale)
+        d2, m2 = omnimem_dense_attn(cache_pair[1], x.q, 0, n, w.scale)
+        torch.cuda.synchronize()
+        assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)) and torch.equal(l1, l2)
+        assert torch.equal(d1.view(torch.int16), d2.view(torch.int16)) and torch.equal(m1, m2)
+    from paper_2605_30519_amd import CompressedCache, omnimem_compress_chunk
+    c1, c2 = CompressedCache.allocate(shared, n), CompressedCache.allocate(per, n)
+    for c in range(n):
+        omnimem_compress_chunk(shared, c, c1)
+        omnimem_compress_chunk(per, c, c2)
+    torch.cuda.synchronize()
+    assert torch.equal(c1.k_mean, c2.k_mean) and torch.equal(c1.k_pages.view(torch.int16), c2.k_pages.view(torch.int16))
+    say("per-head tables: residency differs by head")
+    Bpc = w.blocks_per_chunk
+    nonres = {0: [1, 7], 2: [3, n * Bpc - 2]}
+    per2 = synth.page_layer_per_head(x.k, x.v, B, seed=4, pad_value=NAN, nonresident=nonres)
+    mask = synth.resident_mask(per2).numpy()
+    sel = run_select(per2, x, w)
+    out, lse = omnimem_sparse_attn(per2, x.q, sel.idx, sel.cnt, G, w.scale)
+    dout, dlse = omnimem_dense_attn(per2, x.q, 0, n, w.scale)
+    for h in range(H):
+        ref = oracle.select(host(x.q), host(x.k), B, K, G, 1, 2, w.scale, resident=mask[h], heads=(h, h + 1),
+                            want_all_scores=True)
+        check_selection(host(sel.idx).numpy(), host(sel.cnt).numpy(), ref, heads=[h])
+        assert not np.isin(host(sel.idx).numpy()[h], nonres.get(h, [])).any()
+        hs = np.full(Lq, h, np.int32)
+        qs = np.arange(Lq, dtype=np.int32)
+        o_ref, l_ref, _, _ = oracle.sparse_attn(host(x.q), host(x.k), host(x.v), B, host(sel.idx).numpy(),
+                                                host(sel.cnt).numpy(), G, w.scale, resident=mask[h], hs=hs, qs=qs)
+        attn_check(out, lse, o_ref, l_ref, hs, qs, torch.bfloat16, f"per-head sparse h={h}")
+        d_ref, dl_ref, _, _ = oracle.dense_attn(host(x.q), host(x.k), host(x.v), B, 0, n, w.scale, resident=mask[h],
+                                                hs=hs, qs=qs)
+        attn_check(dout, dlse, d_ref, dl_ref, hs, qs, torch.bfloat16, f"per-head dense h={h}")

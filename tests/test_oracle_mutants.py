@@ -95,6 +95,12 @@ PY_MUTANTS = [
     ("bf16_rounds_to_7_bits", "round_bf16", "np.round(m * 256.0) / 256.0", "np.round(m * 128.0) / 128.0"),
     ("cmp_cache_values_from_keys", "cmp_cache", "kc, vc = pool_keys(k, B), pool_keys(v, B)",
      "kc, vc = pool_keys(k, B), pool_keys(k, B)"),
+    ("lru_evicts_most_recent", "lru_simulate", "victim = next(v for v in order if v not in want)",
+     "victim = next(v for v in reversed(order) if v not in want)"),
+    ("lru_hits_do_not_refresh", "lru_simulate", "                order.remove(c)\n                order.append(c)\n",
+     ""),
+    ("lru_evicts_with_free_slots", "lru_simulate", "if free:", "if free and not slot_of:"),
+    ("lru_highest_free_slot", "lru_simulate", "s = free[0]", "s = free[-1]"),
 ]
 
 
