@@ -57,7 +57,7 @@ def parse():
     p.add_argument("--warmup", type=int, default=2000)
     p.add_argument("--no-sweep", action="store_true", help="skip the history-length sweep")
     p.add_argument("--no-cpu-baseline", action="store_true", help="skip timing the CPU oracle")
-    p.add_argument("--stress", action="store_true", help="add the 14B-shaped union-gather comparison")
+    p.add_argument("--no-stress", action="store_true", help="skip the 14B-shaped union-gather comparison")
     p.add_argument("--no-ramp", action="store_true", help="skip the 30-layer, 1 -> 60 chunk ramp")
     p.add_argument("--no-compressed", action="store_true", help="skip the compressed-history path")
     p.add_argument("--no-lru", action="store_true", help="skip the LRU hot-cache measurement")
@@ -377,7 +377,7 @@ def main():
         result["achievable"] = probe_peaks(dev, result)
 
     # ---------------------------------------------------------------- 14B comparator
-    if args.stress:
+    if not args.no_stress:
         log("14B-shaped union-gather comparison")
         result["stress"] = stress_comparison(dev)
 
@@ -626,20 +626,33 @@ def small_group_measure(dev, reps=50):
             "gathered_kv_bytes": gather, "gather_gbs": round(gather / (ta * 1e-3) / 1e9, 1)}
 
 
-def lru_measure(dev, x, w, steps=60, working=4, sizes=(4, 5, 7, 10), seed=17):
-    """The GPU hot cache of App. B / App. F on the bench layer (20 chunks in pinned
-    host pools).  Access pattern (synthetic, with the locality the paper reports):
-    each step reads a working set of `working` chunks -- three anchors that change
-    every 15 steps plus one chunk drawn at random -- and each head's 64 blocks are
-    drawn from the working set's blocks.  Per LRU size: require + selection attention
-    per step (HIP events around the step, PCIe copies included), hit rate, and the
-    GPU pool's bytes."""
+def lru_measure(dev, x, w, steps=60, sizes=(5, 6, 8, 10), recent=4, seed=17):
+    """The GPU hot cache of App. B / App. F on the bench layer: its chunks in pinned
+    host pools (allocated after binding the thread to the GPU's NUMA node), a GPU
+    pool of `slots` chunk slots per head, residency per (head, chunk).
+
+    Access pattern (synthetic, with locality): per head, 3 anchor chunks that change
+    every 15 steps and one chunk drawn from a per-head set of `recent` chunks; each
+    head's 64 blocks are drawn from those 4 chunks.  The window chunk, read by the
+    SWA branch, is requested for every head as well.
+
+    A step is Eq. 1's three-branch forward with reloads: the selected (head, chunk)
+    pairs decoded on the GPU (Alg. 1 Step 1) and copied to the host, omnimem_lru_require,
+    the CMP and SWA branches, omnimem_lru_wait, the SLC branch over the hot cache,
+    and the gated fusion.  Two modes: reloads on the compute stream (serial), and on
+    a second stream, overlapping the CMP and SWA branches (overlap).  HIP events on
+    the compute stream bracket each step, host round trip included.  The SWA branch
+    waits for the reloads only while its window chunk is not yet resident."""
     import numpy as np
     import torch
 
-    from paper_2605_30519_amd import LruOffload, PagedKVCache, omnimem_sparse_attn
+    from paper_2605_30519_amd import (CompressedCache, LruOffload, PagedKVCache, omnimem_cmp_attn,
+                                      omnimem_compress_chunk, omnimem_dense_attn, omnimem_gated_combine,
+                                      omnimem_numa_bind, omnimem_selected_chunks, omnimem_sparse_attn, synth)
     n, S, H, d = (int(s) for s in x.k.shape)
     B, K, Bpc = w.block_size, w.top_k, w.blocks_per_chunk
+    saved_affinity = os.sched_getaffinity(0)
+    node = omnimem_numa_bind(0)
     pools = []
     for t in (x.k, x.v):
         pad = Bpc * B - S
@@ -648,60 +661,97 @@ def lru_measure(dev, x, w, steps=60, working=4, sizes=(4, 5, 7, 10), seed=17):
         pinned.copy_(y.reshape(n * Bpc, B, H, d).permute(0, 2, 1, 3).cpu())
         pools.append(pinned)
         del y
+    full = synth.page_layer(x.k, x.v, B, seed=7)
+    cc = CompressedCache.allocate(full, n)
+    for c in range(n):
+        omnimem_compress_chunk(full, c, cc)
+    del full
     rng = np.random.default_rng(seed)
+    win = n - w.window_chunks
+    candidates = list(range(win))
+    recent_sets = [rng.choice(candidates, recent, replace=False).tolist() for _ in range(H)]
     plan = []
-    anchors = []
+    anchors = None
     for step in range(steps):
         if step % 15 == 0:
-            anchors = rng.choice(n, working - 1, replace=False).tolist()
-        extra = int(rng.choice([c for c in range(n) if c not in anchors]))
-        ws = anchors + [extra]
-        blocks = np.array([c * Bpc + o for c in ws for o in range(Bpc)])
-        idx = np.stack([np.sort(rng.choice(blocks, K, replace=False)) for _ in range(H)])[:, None, :]
-        plan.append((ws, torch.tensor(idx, dtype=torch.int32, device=dev)))
+            anchors = [rng.choice([c for c in candidates if c not in recent_sets[h]], 3, replace=False).tolist()
+                       for h in range(H)]
+        idx = np.zeros((H, 1, K), np.int32)
+        for h in range(H):
+            chunks = anchors[h] + [int(rng.choice(recent_sets[h]))]
+            blocks = np.array([c * Bpc + o for c in chunks for o in range(Bpc)])
+            idx[h, 0] = np.sort(rng.choice(blocks, K, replace=False))
+        plan.append(torch.tensor(idx, dtype=torch.int32, device=dev))
     cnt = torch.full((H, 1), K, dtype=torch.int32, device=dev)
-    out = torch.empty_like(x.q)
+    o_slc, o_cmp, o_swa, o_out = (torch.empty_like(x.q) for _ in range(4))
     lse = torch.empty((H, w.query_tokens), dtype=torch.float32, device=dev)
-    page_bytes = H * B * d * x.k.element_size()
-    res = {"workload": f"bench layer, {n} chunks in pinned host pools; {steps} steps, working set of {working} "
-                       f"chunks (3 anchors changing every 15 steps + 1 random), {K} blocks per head drawn from it",
-           "sizes": []}
-    # raw reload rate: the whole history, slot by slot
-    big = PagedKVCache(torch.empty((n * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
-                       torch.empty((n * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
-                       torch.zeros((n, Bpc), dtype=torch.int32, device=dev), S)
-    lru = LruOffload(big, n, pools[0], pools[1])
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    lru.require(list(range(n)))
-    e1.record()
-    torch.cuda.synchronize()
-    ms = e0.elapsed_time(e1)
-    res["reload_gbs"] = round(2 * n * Bpc * page_bytes / (ms * 1e-3) / 1e9, 1)
-    res["reload_ms_per_chunk"] = round(ms / n, 3)
-    lru.close()
-    del big
-    for slots in sizes:
-        gpu = PagedKVCache(torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
-                           torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
-                           torch.zeros((n, Bpc), dtype=torch.int32, device=dev), S)
-        lru = LruOffload(gpu, slots, pools[0], pools[1])
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
-        for step, (ws, idx) in enumerate(plan):
-            evs[step][0].record()
-            lru.require(ws)
-            omnimem_sparse_attn(gpu, x.q, idx, cnt, w.group_size, w.scale, out=out, lse=lse)
-            evs[step][1].record()
+    gate = torch.randn((w.query_tokens, H, 3), generator=torch.Generator(device=dev).manual_seed(3), device=dev)
+    slab = B * d * x.k.element_size()
+    res = {"workload": f"bench layer, {n} chunks in pinned host pools, residency per (head, chunk); {steps} steps; "
+                       f"per head 3 anchor chunks changing every 15 steps + 1 of {recent} recent chunks, {K} blocks "
+                       f"per head drawn from them, window chunk for the SWA branch",
+           "numa_node": node, "pcie_peak_gbs": 63.0, "modes": []}
+
+    def pool_of(slots):
+        return PagedKVCache(torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                            torch.empty((slots * Bpc, H, B, d), dtype=x.k.dtype, device=dev),
+                            torch.zeros((H, n, Bpc), dtype=torch.int32, device=dev), S)
+
+    # raw reload rates: every head's copy of every chunk (heads merge into whole-page
+    # copies), then alternate heads only (one strided copy per head and chunk)
+    for name, mask in (("whole_chunks", np.ones((H, n), np.uint8)),
+                       ("every_other_head", (np.add.outer(np.arange(H), np.arange(n)) % 2 == 0).astype(np.uint8))):
+        gpu = pool_of(n)
+        lru = LruOffload(gpu, n, pools[0], pools[1])
         torch.cuda.synchronize()
-        st = lru.stats()
-        t = [e[0].elapsed_time(e[1]) for e in evs]
-        res["sizes"].append({"lru_chunks": slots, "hit_rate": round(st["hits"] / max(1, st["hits"] + st["misses"]), 4),
-                             "reloaded_chunks": st["misses"], "ms_per_step": round(float(np.mean(t)), 4),
-                             "ms_per_step_median": round(float(np.median(t)), 4),
-                             "gpu_pool_gb": round(2 * slots * Bpc * page_bytes / 1e9, 3)})
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        lru.require(mask)
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1)
+        gbs = 2 * int(mask.sum()) * Bpc * slab / (ms * 1e-3) / 1e9
+        res[f"reload_{name}_gbs"] = round(gbs, 1)
+        res[f"reload_{name}_frac_of_pcie"] = round(gbs / 63.0, 3)
         lru.close()
         del gpu
+    copy_stream = torch.cuda.Stream()
+    for slots in sizes:
+        for mode in ("serial", "overlap"):
+            gpu = pool_of(slots)
+            lru = LruOffload(gpu, slots, pools[0], pools[1])
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(steps)]
+            xs = copy_stream if mode == "overlap" else None
+            for step, idx in enumerate(plan):
+                evs[step][0].record()
+                needed = omnimem_selected_chunks(gpu, idx, cnt).cpu()
+                needed[:, win:] = 1                                 # the SWA window, every head
+                # a window chunk already resident is a hit, untouched by this request's
+                # reloads: the SWA branch then need not wait for them
+                window_ready = all(lru.slot_of(h, c) >= 0 for h in range(H) for c in range(win, n))
+                lru.require(needed, copy_stream=xs)
+                omnimem_cmp_attn(cc, n, x.q, w.scale, out=o_cmp, lse=lse)
+                if not window_ready:
+                    lru.wait()
+                omnimem_dense_attn(gpu, x.q, win, n, w.scale, out=o_swa, lse=lse)
+                lru.wait()                                          # Alg. 1's WaitUntilReload
+                omnimem_sparse_attn(gpu, x.q, idx, cnt, w.group_size, w.scale, out=o_slc, lse=lse)
+                omnimem_gated_combine(o_cmp, o_slc, o_swa, gate, out=o_out)
+                evs[step][1].record()
+            torch.cuda.synchronize()
+            st = lru.stats()
+            t = np.array([e[0].elapsed_time(e[1]) for e in evs])
+            pairs = st["hits"] + st["misses"]
+            res["modes"].append({"lru_chunks_per_head": slots, "mode": mode,
+                                 "hit_rate": round(st["hits"] / max(1, pairs), 4),
+                                 "reloaded_pairs": st["misses"],
+                                 "reloaded_gb_per_step": round(st["bytes_reloaded"] / steps / 1e9, 4),
+                                 "ms_per_step": round(float(t.mean()), 4),
+                                 "ms_per_step_median": round(float(np.median(t)), 4),
+                                 "gpu_pool_gb": round(2 * slots * Bpc * H * slab / 1e9, 3)})
+            lru.close()
+            del gpu
+    os.sched_setaffinity(0, saved_affinity)
     return res
 
 
@@ -772,11 +822,73 @@ def ramp_measure(dev, layers_n=30, warm_passes=20):
             "steps": steps}
 
 
-def probe_peaks(dev, result):
-    """Achievable peaks on this GPU, measured next to the spec ones: a device copy
-    (HBM read + write) and a large bf16 GEMM (the vendor library's MFMA rate)."""
+def hip_probes(dev):
+    """The HIP roofline probes of libomnimem_probe.so: an MFMA issue loop (4
+    independent v_mfma_f32_32x32x16_bf16 chains per wave), a streaming read and a
+    streaming copy of 1 GiB.  Best of a few launch shapes each; HIP events on the
+    launch stream."""
+    import ctypes
+
     import torch
-    out = {}
+
+    from paper_2605_30519_amd import _build
+    P = ctypes.CDLL(_build.PROBE_LIB)
+    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
+                                     ctypes.c_void_p]
+    P.omnimem_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                     ctypes.c_void_p]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    sink = torch.zeros(4, dtype=torch.float32, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(call, reps):
+        for _ in range(2):
+            assert call() == 0
+        e0.record()
+        for _ in range(reps):
+            assert call() == 0
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    out = {"probe_library": os.path.basename(_build.PROBE_LIB)}
+    mfma = []
+    for wgs, wps, iters in ((256, 1, 100000), (1024, 1, 25000), (512, 2, 50000)):
+        ms = timed(lambda: P.omnimem_probe_mfma_bf16(iters, wgs, wps, ctypes.c_void_p(sink.data_ptr()), stream), 5)
+        flops = wgs * 4 * wps * iters * 4 * 32768.0
+        mfma.append({"workgroups": wgs, "waves_per_simd": wps, "tflops": round(flops / (ms * 1e-3) / 1e12, 1)})
+    best = max(m["tflops"] for m in mfma)
+    out["mfma_bf16"] = mfma
+    out["mfma_bf16_tflops"] = best
+    # 2.5 PFLOP/s bf16 is 1024 flops per cycle per SIMD on 1024 SIMDs at 2.4 GHz
+    out["mfma_implied_clock_ghz"] = round(best / PEAK_BF16_TFLOPS * 2.4, 3)
+    nbytes = 1 << 30
+    a = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
+    b = torch.empty_like(a)
+    reads, copies = [], []
+    for wgs in (1024, 2048, 4096, 8192):
+        ms = timed(lambda: P.omnimem_probe_read(ctypes.c_void_p(a.data_ptr()), nbytes, wgs,
+                                                ctypes.c_void_p(sink.data_ptr()), stream), 10)
+        reads.append({"workgroups": wgs, "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1)})
+        ms = timed(lambda: P.omnimem_probe_copy(ctypes.c_void_p(a.data_ptr()), ctypes.c_void_p(b.data_ptr()), nbytes,
+                                                wgs, stream), 10)
+        copies.append({"workgroups": wgs, "gbs": round(2 * nbytes / (ms * 1e-3) / 1e9, 1)})
+    out["hbm_read"] = reads
+    out["hbm_read_gbs"] = max(r["gbs"] for r in reads)
+    out["hbm_copy"] = copies
+    out["hbm_copy_gbs"] = max(c["gbs"] for c in copies)
+    del a, b
+    return out
+
+
+def probe_peaks(dev, result):
+    """Achievable peaks on this GPU, measured next to the spec ones: the HIP roofline
+    probes (MFMA issue loop, streaming read and copy), a torch device copy and a
+    large bf16 GEMM (the vendor library's MFMA rate)."""
+    import torch
+    out = {"hip": hip_probes(dev)}
     a = torch.empty(1 << 29, dtype=torch.bfloat16, device=dev).fill_(1.0)  # 1 GiB
     b = torch.empty_like(a)
     for _ in range(5):
@@ -788,7 +900,7 @@ def probe_peaks(dev, result):
         b.copy_(a)
     e1.record()
     torch.cuda.synchronize()
-    out["hbm_copy_gbs"] = round(2 * a.numel() * 2 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
+    out["torch_copy_gbs"] = round(2 * a.numel() * 2 * reps / (e0.elapsed_time(e1) * 1e-3) / 1e9, 1)
     del a, b
     m = 8192
     x = torch.randn((m, m), device=dev).to(torch.bfloat16)
@@ -805,8 +917,9 @@ def probe_peaks(dev, result):
     out["gemm_shape"] = f"{m}x{m}x{m} bf16, torch.matmul"
     att = result["stages"]["attention_roofline"]["achieved"]
     sel = result["stages"]["select_roofline"]["achieved"]
+    out["attention_frac_of_mfma_probe"] = round(att / out["hip"]["mfma_bf16_tflops"], 4)
     out["attention_frac_of_gemm"] = round(att / out["bf16_gemm_tflops"], 4)
-    out["select_frac_of_copy"] = round(sel / out["hbm_copy_gbs"], 4)
+    out["select_frac_of_read_probe"] = round(sel / out["hip"]["hbm_read_gbs"], 4)
     return out
 
 
@@ -837,13 +950,25 @@ def stress_comparison(dev):
     U = int(ub.item())
     idx = s.idx.cpu().numpy()
     per_head = [len(set(idx[h][idx[h] >= 0].tolist())) for h in range(w.heads)]
-    slab = w.block_size * w.head_dim * 2 * 2
-    return {"workload": "Wan2.1-14B-shaped layer: 40 heads x 128, B=128, K=32, 3 query groups, 60 chunks",
-            "select_ms": round(med(0, 1), 4), "scattered_attn_ms": round(med(1, 2), 4),
-            "union_gather_attn_ms": round(med(2, 3), 4),
+    slab = w.block_size * w.head_dim * 2 * 2          # K and V of one (block, head), bf16
+    t_sel, t_att, t_uni = med(0, 1), med(1, 2), med(2, 3)
+    fl = attn_flops(s.idx, s.cnt, w, w.history_chunks)
+    sbytes = select_bytes(w, w.history_chunks, s.awe_active)
+    merged = w.heads * U * slab
+    return {"workload": "Wan2.1-14B-shaped layer: 40 heads x 128, 4680-token chunk, 60-chunk history "
+                        "(280,800 keys) in 128-token blocks, top-32 per (head, group), 3 query groups of 1560 rows",
+            "select_ms": round(t_sel, 4), "select_gbs": round(sbytes / (t_sel * 1e-3) / 1e9, 1),
+            "select_frac_of_hbm": round(sbytes / (t_sel * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "scattered_attn_ms": round(t_att, 4),
+            "scattered_attn_tflops": round(fl / (t_att * 1e-3) / 1e12, 2),
+            "scattered_attn_frac_of_mfma": round(fl / (t_att * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "ms_per_chunk_layer": round(t_sel + t_att, 4),
+            "union_gather_attn_ms": round(t_uni, 4),
             "union_blocks": U, "candidate_blocks": nb - w.window_chunks * w.blocks_per_chunk,
             "union_fraction": round(U / (nb - w.window_chunks * w.blocks_per_chunk), 4),
-            "scattered_kv_bytes": int(sum(per_head)) * slab, "merged_buffer_bytes": w.heads * U * slab,
+            "scattered_kv_bytes": int(sum(per_head)) * slab, "merged_buffer_bytes": merged,
+            "merged_over_scattered": round(merged / max(1, int(sum(per_head)) * slab), 2),
+            "union_gather_over_scattered_time": round(t_uni / t_att, 2),
             "outputs_bit_equal": bool(torch.equal(uo.view(torch.int16), out.view(torch.int16)))}
 
 

@@ -1,0 +1,40 @@
+/*
+ * omnimem_probe.h -- C ABI of libomnimem_probe.so: roofline probes that measure
+ * what one MI355X (gfx950) sustains, next to the published peaks that the
+ * benchmark's roofline fractions use.  Measurement only; the attention path does
+ * not use this library.
+ *
+ * Every pointer is a DEVICE pointer; every call is asynchronous on `stream` (a
+ * hipStream_t, NULL = null stream) and returns 0 on success, -1 on an invalid
+ * argument (nothing launched), -4 when the launch failed.
+ */
+#ifndef OMNIMEM_PROBE_H
+#define OMNIMEM_PROBE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* MFMA issue loop: `workgroups` workgroups of 4*waves_per_simd waves, each wave
+   issuing `iters` rounds of 4 independent v_mfma_f32_32x32x16_bf16 (4 x 32768
+   flops per round).  sink: >= 1 float, written only if the sums take an impossible
+   value (it keeps the loop from being optimised away). */
+int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
+                                void* stream);
+
+/* Streaming copy of `bytes` (a multiple of 16, 16-byte aligned buffers) from src
+   to dst with 16-byte loads and stores, grid-stride over `workgroups` workgroups of
+   256 threads. */
+int32_t omnimem_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
+
+/* Streaming read of `bytes` (a multiple of 16, 16-byte aligned) with 16-byte loads;
+   sink as above. */
+int32_t omnimem_probe_read(const void* src, int64_t bytes, int32_t workgroups, float* sink, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OMNIMEM_PROBE_H */

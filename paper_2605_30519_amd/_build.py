@@ -8,6 +8,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(PKG, "csrc")
 OBJ_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libomnimem.so")
+PROBE_LIB = os.path.join(PKG, "libomnimem_probe.so")
 SOURCES = ["api.hip", "select.hip", "prob.hip", "attention.hip", "union_gather.hip", "fuse.hip", "offload.hip"]
 # host-only C++ (no HIP): argument checks, work plans, the LRU bookkeeping and the
 # NUMA binding, built by the host compiler; tests also build them under sanitizers
@@ -64,8 +65,13 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + ".tmp%d" % os.getpid()
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
     os.replace(tmp, LIB)
+    # the roofline probes: a library of their own, outside the attention ABI
+    tmp = PROBE_LIB + ".tmp%d" % os.getpid()
+    subprocess.check_call([HIPCC, *FLAGS, "-shared", os.path.join(CSRC, "probe.hip"), "-o", tmp],
+                          stderr=subprocess.DEVNULL if not verbose else None)
+    os.replace(tmp, PROBE_LIB)
     return LIB
 
 
 def is_built() -> bool:
-    return os.path.exists(LIB)
+    return os.path.exists(LIB) and os.path.exists(PROBE_LIB)

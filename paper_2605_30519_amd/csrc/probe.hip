@@ -1,0 +1,97 @@
+// probe.hip -- roofline probes for gfx950 (libomnimem_probe.so): an MFMA issue
+// loop and streaming HBM copy / read kernels, so that the fractions of the published
+// peaks can be set beside what the chip sustains at its working clock.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/omnimem_probe.h"
+#include "launch.h"
+
+#define PROBE_API extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__global__ __launch_bounds__(512) void k_mfma_loop(int64_t iters, float* __restrict__ sink) {
+  // operands depend on the lane so that nothing folds; their values do not matter
+  const float x = 1.0f + 1e-3f * static_cast<float>(threadIdx.x % 64);
+  bf16x8 a, b;
+  for (int i = 0; i < 8; ++i) {
+    a[i] = static_cast<__bf16>(x * static_cast<float>(i + 1) * 1e-3f);
+    b[i] = static_cast<__bf16>(x * static_cast<float>(8 - i) * 1e-3f);
+  }
+  f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+  for (int64_t it = 0; it < iters; ++it) {
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+  }
+  float s = 0.f;
+  for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+  if (s == -1.2345e30f) sink[0] = s;
+}
+
+constexpr int kThreads = 256;
+constexpr int kUnroll = 4;
+
+__global__ __launch_bounds__(kThreads) void k_copy(const uint4* __restrict__ src, uint4* __restrict__ dst,
+                                                   int64_t n) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+  int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  for (; i + (kUnroll - 1) * stride < n; i += kUnroll * stride) {
+    uint4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) dst[i + u * stride] = v[u];
+  }
+  for (; i < n; i += stride) dst[i] = src[i];
+}
+
+__global__ __launch_bounds__(kThreads) void k_read(const uint4* __restrict__ src, int64_t n,
+                                                   float* __restrict__ sink) {
+  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
+  int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+  uint32_t acc = 0;
+  for (; i + (kUnroll - 1) * stride < n; i += kUnroll * stride) {
+    uint4 v[kUnroll];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) v[u] = src[i + u * stride];
+#pragma unroll
+    for (int u = 0; u < kUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+  }
+  for (; i < n; i += stride) acc ^= src[i].x ^ src[i].y ^ src[i].z ^ src[i].w;
+  if (acc == 0x9e3779b9u && threadIdx.x == 0) sink[0] = static_cast<float>(acc);
+}
+
+int32_t status(hipError_t e) { return e == hipSuccess ? 0 : -4; }
+
+using omnimem::launch_kernel;
+
+}  // namespace
+
+PROBE_API int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
+                                          void* stream) {
+  if (iters < 1 || workgroups < 1 || waves_per_simd < 1 || waves_per_simd > 2 || sink == nullptr) return -1;
+  return status(launch_kernel(k_mfma_loop, dim3(workgroups), dim3(256 * waves_per_simd), 0,
+                              static_cast<hipStream_t>(stream), iters, sink));
+}
+
+PROBE_API int32_t omnimem_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {
+  if (src == nullptr || dst == nullptr || bytes < 16 || bytes % 16 || workgroups < 1 ||
+      (reinterpret_cast<uintptr_t>(src) | reinterpret_cast<uintptr_t>(dst)) & 15u)
+    return -1;
+  return status(launch_kernel(k_copy, dim3(workgroups), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+                              static_cast<const uint4*>(src), static_cast<uint4*>(dst), bytes / 16));
+}
+
+PROBE_API int32_t omnimem_probe_read(const void* src, int64_t bytes, int32_t workgroups, float* sink, void* stream) {
+  if (src == nullptr || sink == nullptr || bytes < 16 || bytes % 16 || workgroups < 1 ||
+      (reinterpret_cast<uintptr_t>(src) & 15u))
+    return -1;
+  return status(launch_kernel(k_read, dim3(workgroups), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
+                              static_cast<const uint4*>(src), bytes / 16, sink));
+}

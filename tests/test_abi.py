@@ -225,3 +225,17 @@ def test_gated_combine_validation():
     assert g(0, 8, 2, 64, FAKE, None, None, FAKE + 2, FAKE, None) == EINVAL    # misaligned gates
     assert g(0, 8, 2, 64, FAKE, None, None, FAKE, None, None) == EINVAL        # no output
     assert g(0, 0, 2, 64, None, None, None, None, None, None) == 0             # empty: no-op
+
+
+def test_probe_library_exports_its_header():
+    """The roofline probes (a measurement library outside the attention ABI) load and
+    export exactly what include/omnimem_probe.h declares."""
+    import subprocess
+    from paper_2605_30519_amd import _build
+    text = re.sub(r"/\*.*?\*/", "", open(os.path.join(ROOT, "include", "omnimem_probe.h")).read(), flags=re.S)
+    declared = sorted(set(re.findall(r"\b(omnimem_probe_[a-z_0-9]+)\s*\(", text)))
+    assert declared
+    ctypes.CDLL(_build.PROBE_LIB)
+    out = subprocess.run(["nm", "-D", "--defined-only", _build.PROBE_LIB], capture_output=True, text=True).stdout
+    exported = sorted({line.split()[-1] for line in out.splitlines() if " T " in line and "omnimem" in line})
+    assert exported == declared
