@@ -63,6 +63,12 @@ def parse():
     p.add_argument("--no-lru", action="store_true", help="skip the LRU hot-cache measurement")
     p.add_argument("--no-small-group", action="store_true", help="skip the paper's small-group setting")
     p.add_argument("--no-probe", action="store_true", help="skip the achievable-peak probes (copy, GEMM)")
+    p.add_argument("--attn-only", type=int, default=0, metavar="N",
+                   help="only run N sparse-attention calls on the bench workload's first layer (a profiling "
+                        "target), print their mean time, and exit")
+    p.add_argument("--select-only", type=int, default=0, metavar="N",
+                   help="only run N selections over the bench workload's rotated layer caches (a profiling "
+                        "target), print their median time, and exit")
     p.add_argument("--prob-only", type=int, default=0, metavar="G",
                    help="only time selection by probability-averaged scores from the pooled history, "
                         "query groups of G rows (top-64 for one group per head, else top-4), and exit")
@@ -99,6 +105,69 @@ def prob_only(dev, G, reps=50):
     logit_fl = 2.0 * w.query_tokens * n * w.blocks_per_chunk * w.head_dim * w.heads
     print(json.dumps({"prob_select": {"workload": WORKLOAD, "group_size": G, "top_k": K, "select_ms": round(ms, 4),
                                       "logit_tflops": round(logit_fl / (ms * 1e-3) / 1e12, 2)}}), flush=True)
+
+
+def attn_only(dev, calls, warm=200):
+    """Sparse attention alone on the bench workload's first layer, back to back: a
+    profiling target for the attention kernel."""
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select, omnimem_sparse_attn, synth
+    w = synth.WORKLOADS[WORKLOAD]
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=1000)
+    sel = omnimem_select(cache, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    out = torch.empty_like(x.q)
+    lse = torch.empty((w.heads, w.query_tokens), dtype=torch.float32, device=dev)
+    for _ in range(warm):
+        omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale, out=out, lse=lse)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(calls):
+        omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale, out=out, lse=lse)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / calls
+    fl = attn_flops(sel.idx, sel.cnt, w, w.history_chunks)
+    print(json.dumps({"attn_only": {"workload": WORKLOAD, "calls": calls, "ms": round(ms, 4),
+                                    "tflops": round(fl / (ms * 1e-3) / 1e12, 1), "flops_per_call": fl}}), flush=True)
+
+
+def select_only(dev, calls, warm=100):
+    """omnimem_select alone over the bench workload's rotated layer caches (so that K
+    is read from HBM, as in the bench), HIP events around each call: a profiling
+    target for the selection kernels."""
+    import numpy as np
+    import torch
+
+    from paper_2605_30519_amd import omnimem_select, synth
+    w = synth.WORKLOADS[WORKLOAD]
+    layers = []
+    for layer in range(ROTATE_LAYERS):
+        x = synth.make_layer(w, layer, device=dev)
+        layers.append((x.q, synth.page_layer(x.k, x.v, w.block_size, seed=1000 + layer)))
+        del x
+    sels = [omnimem_select(c, q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+            for q, c in layers]
+
+    def call(i):
+        q, c = layers[i % ROTATE_LAYERS]
+        omnimem_select(c, q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                       out=sels[i % ROTATE_LAYERS], want_score=False)
+    for i in range(warm):
+        call(i)
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(calls)]
+    torch.cuda.synchronize()
+    for i in range(calls):
+        ev[i][0].record()
+        call(i)
+        ev[i][1].record()
+    torch.cuda.synchronize()
+    t = np.array([a.elapsed_time(b) for a, b in ev])
+    sb = select_bytes(w, w.history_chunks, sels[0].awe_active)
+    print(json.dumps({"select_only": {"workload": WORKLOAD, "calls": calls, "ms": round(float(np.median(t)), 4),
+                                      "gbs": round(sb / (float(np.median(t)) * 1e-3) / 1e9, 1)}}), flush=True)
 
 
 def attn_flops(idx, cnt, w, n_chunks):
@@ -164,6 +233,12 @@ def main():
     if args.prob_only:
         prob_only(dev, args.prob_only)
         return
+    if args.attn_only:
+        attn_only(dev, args.attn_only)
+        return
+    if args.select_only:
+        select_only(dev, args.select_only)
+        return
     w = synth.WORKLOADS[WORKLOAD]
     n = w.history_chunks
     H, R, K = w.heads, w.groups, w.top_k
@@ -225,6 +300,23 @@ def main():
     for i in range(args.steps):
         step(i, evs[i])
     torch.cuda.synchronize()
+    # the same steps replayed from HIP graphs (one per rotated layer cache)
+    graphs = []
+    for i in range(ROTATE_LAYERS):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            step(i)
+        graphs.append(g)
+    for i in range(2 * ROTATE_LAYERS):
+        graphs[i % ROTATE_LAYERS].replay()
+    torch.cuda.synchronize()
+    t_start.record()
+    for i in range(args.steps):
+        graphs[i % ROTATE_LAYERS].replay()
+    t_end.record()
+    torch.cuda.synchronize()
+    graph_ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    del graphs
     sel_ms = np.array([e[0].elapsed_time(e[1]) for e in evs])
     att_ms = np.array([e[1].elapsed_time(e[2]) for e in evs])
     flops_steps = np.array([flops_per_layer[i % ROTATE_LAYERS] for i in range(args.steps)])
@@ -270,7 +362,10 @@ def main():
                                          round(float(np.percentile(sel_ms, 90)), 4)],
                    "sparse_attn_ms_p10_p90": [round(float(np.percentile(att_ms, 10)), 4),
                                               round(float(np.percentile(att_ms, 90)), 4)],
-                   "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe},
+                   "select_roofline": sel_roof, "attention_roofline": attn_roof, "awe_active": awe,
+                   "graph_replay": {"ms_per_step": round(graph_ms_per_step, 4),
+                                    "effective_tflops": round(float((flops_steps.mean() + sflops) /
+                                                                    (graph_ms_per_step * 1e-3) / 1e12), 2)}},
     }
 
     # ---------------------------------------------------------------- select, cache state
@@ -543,7 +638,7 @@ def select_cache_state(layers, sels, ws, w, sbytes, reps=30):
     """Select alone, HIP events around each call, layers in rotation: (a) after a
     1 GiB read that evicts the MALL with clean lines; (b) after a 1 GiB write, which
     leaves the MALL full of dirty lines that the select's reads must first write
-    back; (c) warm, one layer back to back."""
+    back; (c) warm, one layer back to back; (d) as (a), replayed from a HIP graph."""
     import numpy as np
     import torch
 
@@ -572,9 +667,28 @@ def select_cache_state(layers, sels, ws, w, sbytes, reps=30):
     for i in range(reps):
         sel(0, ev[2 * reps + i])
     torch.cuda.synchronize()
+    # (d) as (a), each layer's select replayed from a HIP graph (no launch gaps
+    # between its three kernels)
+    graphs = []
+    for i in range(len(layers)):
+        g = torch.cuda.CUDAGraph()
+        q, cache = layers[i]
+        with torch.cuda.graph(g):
+            omnimem_select(cache, q, K, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale,
+                           workspace=ws, out=sels[i], want_score=False)
+        graphs.append(g)
+    torch.cuda.synchronize()
+    evg = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(reps)]
+    for i in range(reps):
+        total += scratch.sum()
+        evg[i][0].record()
+        graphs[i % len(layers)].replay()
+        evg[i][1].record()
+    torch.cuda.synchronize()
+    del graphs
     out = {}
     for name, part in (("mall_evicted_by_1gib_read", ev[:reps]), ("after_1gib_write_dirty_mall", ev[reps:2 * reps]),
-                       ("warm_same_layer", ev[2 * reps:])):
+                       ("warm_same_layer", ev[2 * reps:]), ("mall_evicted_graph_replay", evg)):
         t = np.array([a.elapsed_time(b) for a, b in part])
         gbs = sbytes / (float(np.median(t)) * 1e-3) / 1e9
         out[name] = {"select_ms": round(float(np.median(t)), 4),
