@@ -16,9 +16,15 @@
 // S^T accumulator registers line up with the B-operand layout of P^T, so P goes from
 // accumulator to MFMA operand with a bf16 pack and nothing else.
 //
+// The same arithmetic runs in three data-movement shapes: k_attn_bf16_r64 (d = 128,
+// groups of more than 32 rows: 64 rows per wave, tiles by buffer-to-LDS DMA),
+// k_attn_bf16 (d = 64, more than 32 rows) and k_attn_bf16_groups (groups of at most
+// 32 rows: one wave per group, every wave streaming its own groups' tiles).
+//
 // f32 kernel (k_attn_f32): one lane per query row, fp32 dot products and exact
 // expf-based online softmax, for fp32 inputs.
 #include <math.h>
+#include <atomic>
 #include <type_traits>
 
 #include "device_common.h"
@@ -159,8 +165,7 @@ __device__ int decode_tiles(const AttnArgs& a, const int32_t* pt, const int32_t*
 }
 
 // ------------------------------------------------------------------ bf16 / MFMA
-constexpr int kWaves = 8;       // 256 query rows per workgroup, two waves per SIMD
-constexpr int kSmallWaves = 4;  // groups of at most 32 rows: one wave per SIMD, two workgroups per CU
+constexpr int kWaves = 8;  // 256 query rows per workgroup, two waves per SIMD
 
 // A-operand row order for S^T = K Q^T: swapping bits 2 and 3 of the row makes the
 // accumulator element i of lane l hold key 8*(l/32)+i (i < 8) or 16+8*(l/32)+(i-8).
@@ -172,25 +177,22 @@ __device__ __forceinline__ int s_row_perm(int x) { return (x & ~12) | ((x & 4) <
 //  V rows are read by ds_read_b64_tr_b16, 4 rows x 32 B per 16-lane group and two
 //    groups per pass: a stride of 16 or 48 (mod 64) dwords makes the 8 row segments of a
 //    pass disjoint.
-template <int D, bool PHASED>
+template <int D>
 struct AttnLds {
   static constexpr int K_STRIDE = D == 128 ? 136 : 72;
   static constexpr int V_STRIDE = D == 128 ? 160 : 96;
   static constexpr int K_ELEMS = kTileKeys * K_STRIDE;
   static constexpr int V_ELEMS = kTileKeys * V_STRIDE;
   static constexpr int K_STAGES = 2;
-  static constexpr int V_STAGES = PHASED ? 3 : 2;  // the phase-shifted waves still read the previous tile's V
+  static constexpr int V_STAGES = 3;  // the phase-shifted waves still read the previous tile's V
   static constexpr int TOTAL_ELEMS = K_STAGES * K_ELEMS + V_STAGES * V_ELEMS;
 };
 
-// NW waves of 32 query rows.  PHASED: the upper half of the waves runs half a tile
-// behind the lower half (see below).  Groups of at most 32 rows fill only wave 0, so
-// they take the unshifted four-wave variant: its smaller LDS ring (two V stages) and
-// tile table, and one wave per SIMD, let two workgroups share a CU, so that two
-// groups' loads are in flight at once.
-template <int D, bool PHASED, int NW>
+// NW waves of 32 query rows, the upper half of the waves running half a tile behind
+// the lower half (see below); for d = 64 and groups of more than 32 rows.
+template <int D, int NW>
 __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
-  using L = AttnLds<D, PHASED>;
+  using L = AttnLds<D>;
   constexpr int NT = NW * kWave;
   constexpr int ROWS = NW * 32;
   constexpr int CHUNKS_PER_ROW = D / 8;                        // 16-byte chunks per key row
@@ -271,7 +273,7 @@ __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
   // The two waves that share a SIMD (w and w + 4) run the same tile half a step
   // apart: waves 0-3 do QK(t), softmax(t), PV(t); waves 4-7 do PV(t-1), QK(t),
   // softmax(t).  While one of them is in its softmax (VALU) the other issues MFMAs.
-  const bool late = PHASED && wave >= NW / 2;
+  const bool late = wave >= NW / 2;
   bf16x8 pb[4];
   auto pv = [&](const uint16_t* v_lds) {
 #pragma unroll
@@ -420,6 +422,308 @@ __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
   if (a.lse && lane < 32 && my_row < row_end)
     a.lse[static_cast<int64_t>(h) * a.lq + my_row] =
         l_tot > 0.f ? (m_run * c + __log2f(l_tot)) * kLn2 : -INFINITY;
+}
+
+// ------------------------------------------------------------------ bf16 / MFMA, one wave per query group
+// Query groups of at most 32 rows (the small-group setting of App. B, where every
+// group of G_q rows keeps its own top-K blocks, and short dense calls): a group is
+// one 32-row MFMA tile, so its attention is a gather with little arithmetic per
+// byte.  Every wave runs on its own, with no barrier: it walks a sequence of
+// (head, group) pairs (pair first + k * stride, the grid resident at once), and
+// the tiles of consecutive groups form one stream, the next tile's K and V always
+// in flight while the current one is computed, across group boundaries too.  K
+// goes from memory straight into registers in the MFMA A-operand layout; V passes
+// through the wave's own LDS tile for the transposing reads.  The next group's list
+// entries are fetched when the walk enters a group, its Q rows with its first tile.
+// The arithmetic is that of the 32-row kernel: the same operand layouts, the same
+// online softmax, the same rounding.
+constexpr int kGrpWaves = 4;
+
+
+template <int D>
+__global__ __launch_bounds__(kGrpWaves* kWave, 1) void k_attn_bf16_groups(AttnArgs a) {
+  using L = AttnLds<D>;
+  constexpr int KK = D / 16;                       // k-steps of QK^T
+  constexpr int DT = D / 32;                       // 32-wide output tiles along d
+  constexpr int CPR = D / 8;                       // 16-byte chunks per key row
+  constexpr int VROWS = kWave / CPR;               // V rows per load instruction
+  constexpr int VLOADS = kTileKeys / VROWS;        // V load instructions per tile
+  __shared__ __attribute__((aligned(16))) uint16_t v_all[kGrpWaves * L::V_ELEMS];
+
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave, half = lane / 32;
+  uint16_t* const v_lds = v_all + wave * L::V_ELEMS;
+  const int total = a.H * a.R;
+  const int stride = gridDim.x * kGrpWaves;
+  const int first = xcd_contiguous_id(blockIdx.x, gridDim.x) * kGrpWaves + wave;
+  if (first >= total) return;  // wave-uniform; no barrier anywhere below
+  const uint16_t* qp = static_cast<const uint16_t*>(a.q);
+  const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
+  const uint16_t* vp = static_cast<const uint16_t*>(a.v_pages);
+  uint16_t* op = static_cast<uint16_t*>(a.out);
+  const float c = a.scale * kLog2e;
+  const int krow = s_row_perm(lane % 32);
+
+  // ---- the walk over groups and tiles (wave-uniform state; w_* and nx_id per lane)
+  int p_hr = first, p_count = 0, p_base = 0, p_e = 0, p_sub = 0, p_emitted = 0;
+  const int32_t* p_list = nullptr;
+  int w_page = -1, w_nvb = 0;  // entry p_base + lane: page (-1: no tile) and valid tokens
+  int nx_id = -1, nx_count = 0;
+  const int32_t* nx_list = nullptr;
+
+  auto group_list = [&](int hr, const int32_t*& list) -> int {
+    int count;
+    resolve_list(a, hr, list, count);
+    return count;
+  };
+  auto entry_id = [&](const int32_t* list, int count, int e) -> int {
+    if (e >= count) return -1;
+    return list ? list[e] : a.dense_first + e;
+  };
+  // this lane's entry of the window: its page and valid tokens, or no tile
+  auto resolve_window = [&](int id) {
+    w_page = -1;
+    w_nvb = 0;
+    if (id >= 0 && id < a.nb) {
+      const int32_t p = head_table(a, p_hr / a.R)[id];
+      const int o = id % a.Bpc;
+      const int nvb = o == a.Bpc - 1 ? a.S - o * a.B : a.B;
+      if (p >= 0 && p < a.num_pages && nvb > 0) {
+        w_page = p;
+        w_nvb = nvb;
+      }
+    }
+  };
+  auto prefetch_next_ids = [&]() {
+    const int nhr = p_hr + stride;
+    nx_count = 0;
+    nx_id = -1;
+    if (nhr < total) {
+      nx_count = group_list(nhr, nx_list);
+      nx_id = entry_id(nx_list, nx_count, lane);
+    }
+  };
+  // output of a group without a single tile: O = 0, lse = -inf
+  auto write_empty = [&](int hr) {
+    const int h = hr / a.R, g0 = (hr % a.R) * a.G, rows = min(g0 + a.G, a.lq) - g0;
+    for (int i = lane; i < rows * CPR; i += kWave)
+      *reinterpret_cast<uint4*>(op + (static_cast<int64_t>(g0 + i / CPR) * a.H + h) * D + (i % CPR) * 8) =
+          make_uint4(0, 0, 0, 0);
+    if (a.lse && lane < rows) a.lse[static_cast<int64_t>(h) * a.lq + g0 + lane] = -INFINITY;
+  };
+  // first group: its ids now, then the next group's
+  p_count = group_list(p_hr, p_list);
+  resolve_window(entry_id(p_list, p_count, lane));
+  prefetch_next_ids();
+
+  // the next tile of the walk: page, (sub-tile << 8) | valid keys, its group, and
+  // whether it opens the group; false at the end
+  auto next_tile = [&](int& page, int& meta, int& hr, bool& opens) -> bool {
+    for (;;) {
+      while (p_e < p_count) {
+        if (p_e >= p_base + kWave) {  // lists longer than a wave: the next window
+          p_base += kWave;
+          resolve_window(entry_id(p_list, p_count, p_base + lane));
+          continue;
+        }
+        const uint64_t live = __ballot(w_page >= 0) & (~0ull << (p_e - p_base));
+        if (live == 0) {
+          p_e = p_base + kWave;
+          p_sub = 0;
+          continue;
+        }
+        const int l = __builtin_ctzll(live);
+        if (p_base + l != p_e) {
+          p_e = p_base + l;
+          p_sub = 0;
+        }
+        const int nvb = __builtin_amdgcn_readlane(w_nvb, l);
+        page = __builtin_amdgcn_readlane(w_page, l);
+        const int left = nvb - p_sub * kTileKeys;
+        meta = (p_sub << 8) | (left < kTileKeys ? left : kTileKeys);
+        hr = p_hr;
+        opens = p_emitted == 0;
+        ++p_emitted;
+        if (++p_sub * kTileKeys >= nvb) {
+          ++p_e;
+          p_sub = 0;
+        }
+        return true;
+      }
+      if (p_emitted == 0) write_empty(p_hr);
+      p_hr += stride;
+      if (p_hr >= total) return false;
+      p_list = nx_list;
+      p_count = nx_count;
+      p_base = p_e = p_sub = p_emitted = 0;
+      resolve_window(nx_id);
+      prefetch_next_ids();
+    }
+  };
+
+  // ---- registers of the stream: K of two tiles (current, next), V of the next, Q
+  bf16x8 ka[2][KK], kb[2][KK], q[KK], qn[KK];
+  uint4 vn[VLOADS];
+  auto load_tile = [&](int page, int meta, int hr, bf16x8 (&kf)[2][KK]) {
+    const int sub = meta >> 8, nv = meta & 255;
+    const int64_t slab = (static_cast<int64_t>(page) * a.H + hr / a.R) * a.B * D + static_cast<int64_t>(sub) * kTileKeys * D;
+    const uint16_t* ks = kp + slab;
+    const uint16_t* vs = vp + slab;
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+      const int row = 32 * t2 + krow;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) {
+        uint4 raw = make_uint4(0, 0, 0, 0);
+        if (row < nv) raw = *reinterpret_cast<const uint4*>(ks + row * D + 16 * kk + 8 * half);
+        kf[t2][kk] = __builtin_bit_cast(bf16x8, raw);
+      }
+    }
+#pragma unroll
+    for (int i = 0; i < VLOADS; ++i) {
+      const int row = i * VROWS + lane / CPR;
+      vn[i] = row < nv ? *reinterpret_cast<const uint4*>(vs + row * D + (lane % CPR) * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto load_q = [&](int hr) {
+    const int h = hr / a.R, g0 = (hr % a.R) * a.G, g1 = min(g0 + a.G, a.lq);
+    const int row = g0 + lane % 32;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      uint4 raw = make_uint4(0, 0, 0, 0);
+      if (row < g1) raw = *reinterpret_cast<const uint4*>(qp + (static_cast<int64_t>(row) * a.H + h) * D + 16 * kk + 8 * half);
+      qn[kk] = __builtin_bit_cast(bf16x8, raw);
+    }
+  };
+
+  // ---- per-group softmax state
+  f32x16 o_acc[DT];
+  float m_run = -INFINITY, l_run = 0.f;
+  int cur_hr = -1;
+  auto finish = [&](int hr) {
+    const int h = hr / a.R, g0 = (hr % a.R) * a.G, g1 = min(g0 + a.G, a.lq);
+    const int row = g0 + lane % 32;
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+    if (row < g1) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i4 = 0; i4 < 4; ++i4) {
+          bf16x4 w;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) w[e] = static_cast<__bf16>(o_acc[dt][4 * i4 + e] * inv);
+          *reinterpret_cast<bf16x4*>(op + (static_cast<int64_t>(row) * a.H + h) * D + 32 * dt + 8 * i4 + 4 * half) = w;
+        }
+      if (a.lse && lane < 32)
+        a.lse[static_cast<int64_t>(h) * a.lq + row] = l_tot > 0.f ? (m_run * c + __log2f(l_tot)) * kLn2 : -INFINITY;
+    }
+  };
+  auto open_group = [&](int hr) {
+    if (cur_hr >= 0) finish(cur_hr);
+    cur_hr = hr;
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) q[kk] = qn[kk];
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) o_acc[dt][i] = 0.f;
+    m_run = -INFINITY;
+    l_run = 0.f;
+  };
+
+  bf16x8 pb[4];
+  auto pv = [&]() {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int key0 = 16 * j + 8 * half + (lane % 16) / 4;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int col = 32 * dt + 16 * ((lane / 16) % 2) + 4 * (lane % 4);
+        typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
+        const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + key0 * L::V_STRIDE + col));
+        const i16x4 hi =
+            __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4*)(v_lds + (key0 + 4) * L::V_STRIDE + col));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+        o_acc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pb[j], o_acc[dt], 0, 0, 0);
+      }
+    }
+  };
+  // QK^T, online softmax and PV of one tile whose K is in kf and V in the LDS tile
+  auto compute = [&](const bf16x8 (&kf)[2][KK], int nvalid) {
+    f32x16 s_acc[2];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s_acc[t2][i] = 0.f;
+#pragma unroll
+      for (int kk = 0; kk < KK; ++kk) s_acc[t2] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[t2][kk], q[kk], s_acc[t2], 0, 0, 0);
+    }
+    if (nvalid < kTileKeys) {  // partial tile: mask the keys past the block's end
+#pragma unroll
+      for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = 32 * t2 + (i < 8 ? 8 * half + i : 16 + 8 * half + (i - 8));
+          if (key >= nvalid) s_acc[t2][i] = -INFINITY;
+        }
+    }
+    float mloc = s_acc[0][0];
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mloc = fmaxf(mloc, s_acc[t2][i]);
+    const float m_tile = fmaxf(mloc, __shfl_xor(mloc, 32));
+    if (__any(m_tile > m_run)) {  // rescale only when some lane's running max grows
+      const float m_new = fmaxf(m_run, m_tile);
+      const float alpha = m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) o_acc[dt][i] *= alpha;
+      m_run = m_new;
+    }
+    const float mc = m_run == -INFINITY ? 0.f : m_run * c;
+    float psum = 0.f;
+#pragma unroll
+    for (int t2 = 0; t2 < 2; ++t2)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(s_acc[t2][i], c, -mc));
+        psum += p;
+        pb[2 * t2 + i / 8][i % 8] = static_cast<__bf16>(p);
+      }
+    l_run += psum;
+    pv();
+  };
+
+  int page = 0, meta = 0, hr = 0;
+  bool opens = false;
+  bool have = next_tile(page, meta, hr, opens);
+  if (have) {
+    load_tile(page, meta, hr, ka);
+    if (opens) load_q(hr);
+  }
+  // one tile: its K in kc, its V in vn; the next tile's loads go to kn and vn
+  auto step = [&](bf16x8 (&kc)[2][KK], bf16x8 (&kn)[2][KK]) {
+    const int nvalid = meta & 255;
+    if (opens) open_group(hr);
+#pragma unroll
+    for (int i = 0; i < VLOADS; ++i)
+      *reinterpret_cast<uint4*>(v_lds + (i * VROWS + lane / CPR) * L::V_STRIDE + (lane % CPR) * 8) = vn[i];
+    have = next_tile(page, meta, hr, opens);
+    if (have) {
+      load_tile(page, meta, hr, kn);
+      if (opens) load_q(hr);
+    }
+    compute(kc, nvalid);
+  };
+  while (have) {
+    step(ka, kb);
+    if (!have) break;
+    step(kb, ka);
+  }
+  if (cur_hr >= 0) finish(cur_hr);
 }
 
 // ------------------------------------------------------------------ bf16 / MFMA, 64 rows per wave
@@ -1027,6 +1331,31 @@ __global__ __launch_bounds__(kWave) void k_attn_f32(AttnArgs a) {
   if (a.lse) a.lse[static_cast<int64_t>(h) * a.lq + my_row] = l > 0.f ? m + logf(l) : -INFINITY;
 }
 
+// Workgroups of the one-wave-per-group kernel: one wave per group, at most as many
+// workgroups as the device holds at once (its CU count times the kernel's
+// occupancy, looked up once per device).
+template <int D>
+int group_workgroups(int64_t groups) {
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int> resident[kMaxDevices];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev >= kMaxDevices) dev = -1;
+  int n = dev >= 0 ? resident[dev].load(std::memory_order_relaxed) : 0;
+  if (n <= 0) {
+    int cus = 0, per_cu = 0;
+    if (dev < 0 || hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus <= 0)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_attn_bf16_groups<D>, kGrpWaves * kWave, 0) !=
+            hipSuccess ||
+        per_cu <= 0)
+      per_cu = 1;
+    n = cus * per_cu;
+    if (dev >= 0) resident[dev].store(n, std::memory_order_relaxed);
+  }
+  const int64_t need = (groups + kGrpWaves - 1) / kGrpWaves;
+  return static_cast<int>(need < n ? need : n);
+}
+
 }  // namespace
 
 hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t stream) {
@@ -1056,8 +1385,8 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   const int rows = L.group_size < L.lq ? L.group_size : L.lq;
   // bf16, d = 128 and groups of more than 32 rows: 64 rows per wave; else 32
   const bool r64 = g.dtype == 0 && g.D == 128 && rows > 32;
-  const bool small = rows <= 32;  // one wave's rows per group: the four-wave unshifted variant
-  const int rows_per_wg = g.dtype != 0 ? kWave : r64 ? kR64Waves * 64 : (small ? kSmallWaves : kWaves) * 32;
+  const bool small = rows <= 32;  // one 32-row tile per group: a wave per group
+  const int rows_per_wg = g.dtype != 0 ? kWave : r64 ? kR64Waves * 64 : small ? 32 : kWaves * 32;
   a.tiles_per_group = (rows + rows_per_wg - 1) / rows_per_wg;
   const int64_t nwg = static_cast<int64_t>(g.H) * L.R * a.tiles_per_group;
   if (nwg <= 0) return hipSuccess;
@@ -1066,10 +1395,12 @@ hipError_t launch_attention(const CacheGeom& g, const AttnLaunch& L, hipStream_t
   // bf16 with d = 128 and more than 32 rows per group always takes the 64-row kernel
   if (r64) return launch_kernel(k_attn_bf16_r64<128>, grid, dim3(kR64Waves * kWave), 0, stream, a);
   if (g.dtype == 0) {
-    if (!small) return launch_kernel(k_attn_bf16<64, true, kWaves>, grid, dim3(kWaves * kWave), 0, stream, a);
+    if (!small) return launch_kernel(k_attn_bf16<64, kWaves>, grid, dim3(kWaves * kWave), 0, stream, a);
     if (g.D == 128)
-      return launch_kernel(k_attn_bf16<128, false, kSmallWaves>, grid, dim3(kSmallWaves * kWave), 0, stream, a);
-    return launch_kernel(k_attn_bf16<64, false, kSmallWaves>, grid, dim3(kSmallWaves * kWave), 0, stream, a);
+      return launch_kernel(k_attn_bf16_groups<128>, dim3(group_workgroups<128>(nwg)), dim3(kGrpWaves * kWave), 0,
+                           stream, a);
+    return launch_kernel(k_attn_bf16_groups<64>, dim3(group_workgroups<64>(nwg)), dim3(kGrpWaves * kWave), 0, stream,
+                         a);
   }
   if (g.D == 128) return launch_kernel(k_attn_f32<128>, grid, dim3(kWave), 0, stream, a);
   return launch_kernel(k_attn_f32<64>, grid, dim3(kWave), 0, stream, a);
