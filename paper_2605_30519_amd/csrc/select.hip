@@ -12,7 +12,8 @@
 //   k_topk           one workgroup per (head, group): exact top-K over Omega by
 //                    histogram refinement of the key interval holding the K-th key,
 //                    keys held in registers, ties to the lower block id, ids written
-//                    in ascending order.
+//                    in ascending order (for K <= 16, k_topk_small: one wave per row,
+//                    per-lane sorted lists merged by wave-wide maxima).
 // The dominant cost is the K stream in k_pool_score, which is HBM-bound: each wave
 // owns whole (page, head) slabs (B*d contiguous elements) and reads them with
 // 16-byte loads, all lanes of a wave in flight on one slab at a time.
@@ -803,6 +804,115 @@ __global__ __launch_bounds__(NT) void k_topk(const uint32_t* __restrict__ keys, 
   topk_row<NT>(keys + row * nbp, nb, K, idx + row * K, score_out ? score_out + row * K : nullptr, cnt + row);
 }
 
+// Top-K for small K (at most kTopkSmallK; the small-group setting selects K = 4):
+// one wave per (head, group) row.  Lane l reads the ids 4 l + 256 j + e in increasing
+// order and keeps the KM best (key, id) pairs it has seen in a sorted register list
+// (an equal key arriving later has a higher id, so it ranks below); K rounds of a
+// wave-wide maximum over the lanes' list heads, keyed by (key, lower id), then name
+// the winners, which are written in ascending id order.
+constexpr int kTopkSmallK = 16;
+constexpr int kTopkSmallWaves = 4;  // rows per workgroup
+
+template <int KM>
+__global__ __launch_bounds__(kTopkSmallWaves* kWave) void k_topk_small(const uint32_t* __restrict__ keys, int rows,
+                                                                         int nb, int nbp, int K,
+                                                                         int32_t* __restrict__ idx,
+                                                                         int32_t* __restrict__ cnt,
+                                                                         float* __restrict__ score_out) {
+  constexpr int kBatch = 8;  // 16-byte loads in flight per lane
+  const int lane = threadIdx.x % kWave;
+  const int64_t row = static_cast<int64_t>(blockIdx.x) * kTopkSmallWaves + threadIdx.x / kWave;
+  if (row >= rows) return;  // wave-uniform
+  const uint32_t* kp = keys + row * nbp;
+
+  uint32_t lk[KM];
+  int li[KM];
+#pragma unroll
+  for (int j = 0; j < KM; ++j) {
+    lk[j] = 0u;
+    li[j] = 0;
+  }
+  auto insert = [&](uint32_t k, int id) {
+    if (k <= lk[KM - 1]) return;  // also drops non-candidates (key 0)
+    bool placed = false;
+#pragma unroll
+    for (int j = KM - 1; j > 0; --j) {
+      if (!placed) {
+        if (k > lk[j - 1]) {
+          lk[j] = lk[j - 1];
+          li[j] = li[j - 1];
+        } else {
+          lk[j] = k;
+          li[j] = id;
+          placed = true;
+        }
+      }
+    }
+    if (!placed) {
+      lk[0] = k;
+      li[0] = id;
+    }
+  };
+  for (int b0 = 0; b0 < nb; b0 += kBatch * 4 * kWave) {
+    uint4 v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = b0 + (u * kWave + lane) * 4;
+      v[u] = i < nb ? *reinterpret_cast<const uint4*>(kp + i) : make_uint4(0u, 0u, 0u, 0u);  // i + 3 < nbp
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const int i = b0 + (u * kWave + lane) * 4;
+      insert(v[u].x, i);
+      insert(i + 1 < nb ? v[u].y : 0u, i + 1);
+      insert(i + 2 < nb ? v[u].z : 0u, i + 2);
+      insert(i + 3 < nb ? v[u].w : 0u, i + 3);
+    }
+  }
+
+  // K rounds: the largest (key, lower id) among the lanes' heads wins and leaves its list
+  uint32_t wkey = 0u;
+  int wid = 0, taken = 0;
+  for (int r = 0; r < KM; ++r) {
+    if (r >= K) break;
+    const uint64_t mine =
+        lk[0] == 0u ? 0ull : (static_cast<uint64_t>(lk[0]) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(li[0]));
+    uint64_t best = mine;
+#pragma unroll
+    for (int off = kWave / 2; off >= 1; off >>= 1) {
+      const uint64_t o = __shfl_xor(best, off);
+      best = o > best ? o : best;
+    }
+    if (best == 0ull) break;  // fewer than K candidates
+    if (mine == best) {
+#pragma unroll
+      for (int j = 0; j + 1 < KM; ++j) {
+        lk[j] = lk[j + 1];
+        li[j] = li[j + 1];
+      }
+      lk[KM - 1] = 0u;
+    }
+    if (lane == r) {
+      wkey = static_cast<uint32_t>(best >> 32);
+      wid = static_cast<int>(~static_cast<uint32_t>(best));
+    }
+    ++taken;
+  }
+  // ascending ids: lane r < taken writes winner r at its rank among the winners' ids
+  int rank = 0;
+  for (int s = 0; s < taken; ++s) rank += __shfl(wid, s) < wid;
+  int32_t* out_idx = idx + row * K;
+  float* out_score = score_out ? score_out + row * K : nullptr;
+  if (lane < taken) {
+    out_idx[rank] = wid;
+    if (out_score) out_score[rank] = key_score(wkey);
+  } else if (lane < K) {
+    out_idx[lane] = -1;
+    if (out_score) out_score[lane] = -INFINITY;
+  }
+  if (lane == 0) cnt[row] = taken;
+}
+
 // Top-K for rows longer than the register-resident kernel holds: one wavefront,
 // keys re-read at every step of a plain bisection.
 __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
@@ -905,6 +1015,15 @@ hipError_t launch_qmean(const SelectPlan& p, const CacheGeom& g, const T* q, flo
 hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* keys, int nbp, int32_t* idx,
                        int32_t* cnt, float* score, hipStream_t stream) {
   const dim3 tgrid(p.R, g.H);
+  // small K: one wave per row
+  const int rows = p.R * g.H;
+  const dim3 sgrid((rows + kTopkSmallWaves - 1) / kTopkSmallWaves);
+  if (p.K <= 4)
+    return launch_kernel(k_topk_small<4>, sgrid, dim3(kTopkSmallWaves * kWave), 0, stream, keys, rows, g.nb, nbp, p.K,
+                         idx, cnt, score);
+  if (p.K <= kTopkSmallK)
+    return launch_kernel(k_topk_small<kTopkSmallK>, sgrid, dim3(kTopkSmallWaves * kWave), 0, stream, keys, rows, g.nb,
+                         nbp, p.K, idx, cnt, score);
   // 512 threads hold rows of up to 16384 keys in registers (32 per lane), 1024 twice
   // that; with many rows (small query groups) 256-thread workgroups pack more rows
   // per CU
