@@ -80,37 +80,44 @@ __device__ __forceinline__ void lse_merge(float& m, float& l, float m2, float l2
   m = mx;
 }
 
-// 8 fp32 values -> bf16 hi and lo pieces (x ~= hi + lo), packed as MFMA operands.
+// 8 fp32 values -> bf16 hi and lo pieces (x ~= hi + lo), packed as MFMA operands;
+// both roundings to nearest even (the hardware conversion).
 __device__ __forceinline__ void split8(const float (&x)[8], uint4& hi, uint4& lo) {
-  uint32_t h[4], l[4];
+  bf16x8 h, l;
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const uint16_t h0 = f32_to_bf16_rne(x[2 * e]), h1 = f32_to_bf16_rne(x[2 * e + 1]);
-    const uint16_t l0 = f32_to_bf16_rne(x[2 * e] - bf16_to_f32(h0));
-    const uint16_t l1 = f32_to_bf16_rne(x[2 * e + 1] - bf16_to_f32(h1));
-    h[e] = static_cast<uint32_t>(h0) | (static_cast<uint32_t>(h1) << 16);
-    l[e] = static_cast<uint32_t>(l0) | (static_cast<uint32_t>(l1) << 16);
+  for (int e = 0; e < 8; ++e) {
+    h[e] = static_cast<__bf16>(x[e]);
+    l[e] = static_cast<__bf16>(x[e] - static_cast<float>(h[e]));
   }
-  hi = make_uint4(h[0], h[1], h[2], h[3]);
-  lo = make_uint4(l[0], l[1], l[2], l[3]);
+  hi = __builtin_bit_cast(uint4, h);
+  lo = __builtin_bit_cast(uint4, l);
 }
 
-// One workgroup per (tile of 64 keys, head); keys past nb are zero.
+// One workgroup per (tile of 64 keys, head); keys past nb are zero.  Every load of
+// a thread is in flight before the first split.
 template <int D>
 __global__ __launch_bounds__(kPThreads) void k_split_keys(const float* __restrict__ kbar, int64_t kbar_stride, int nb,
                                                           int ntiles, uint4* __restrict__ ksplit) {
   constexpr int CH = D / 8;
+  constexpr int PER = kPKeys * CH / kPThreads;  // 8-element chunks per thread
+  static_assert(PER * kPThreads == kPKeys * CH, "whole chunks per thread");
   const int t = blockIdx.x, h = blockIdx.y;
   uint4* dst = ksplit + (static_cast<int64_t>(h) * ntiles + t) * (2 * kPKeys * CH);
-  for (int e = threadIdx.x; e < kPKeys * CH; e += kPThreads) {
-    const int row = e / CH, c = e % CH, b = t * kPKeys + row;
-    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float4 x0[PER], x1[PER];
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + u * kPThreads, row = e / CH, c = e % CH, b = t * kPKeys + row;
+    x0[u] = x1[u] = make_float4(0.f, 0.f, 0.f, 0.f);
     if (b < nb) {
       const float* src = kbar + (static_cast<int64_t>(h) * kbar_stride + b) * D + 8 * c;
-      const float4 x0 = *reinterpret_cast<const float4*>(src), x1 = *reinterpret_cast<const float4*>(src + 4);
-      x[0] = x0.x; x[1] = x0.y; x[2] = x0.z; x[3] = x0.w;
-      x[4] = x1.x; x[5] = x1.y; x[6] = x1.z; x[7] = x1.w;
+      x0[u] = *reinterpret_cast<const float4*>(src);
+      x1[u] = *reinterpret_cast<const float4*>(src + 4);
     }
+  }
+#pragma unroll
+  for (int u = 0; u < PER; ++u) {
+    const int e = threadIdx.x + u * kPThreads;
+    const float x[8] = {x0[u].x, x0[u].y, x0[u].z, x0[u].w, x1[u].x, x1[u].y, x1[u].z, x1[u].w};
     uint4 hi, lo;
     split8(x, hi, lo);
     dst[e] = hi;
@@ -384,7 +391,17 @@ __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restric
   const int rows = min(r * G + G, lq) - r * G;
   float s = 0.f;
   const int parts = (rows + kPRows - 1) / kPRows;
-  for (int k = 0; k < parts; ++k) s += part[(static_cast<int64_t>(h) * nseg + r * spg + k) * nb + b];
+  // the parts added in slice order, kBatch loads in flight before their adds
+  constexpr int kBatch = 16;
+  const float* src = part + (static_cast<int64_t>(h) * nseg + r * spg) * nb + b;
+  for (int k0 = 0; k0 < parts; k0 += kBatch) {
+    float v[kBatch];
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) v[u] = k0 + u < parts ? src[static_cast<int64_t>(k0 + u) * nb] : 0.f;
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u)
+      if (k0 + u < parts) s += v[u];
+  }
   s = s / static_cast<float>(rows);
   const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
   const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
