@@ -937,9 +937,9 @@ def ramp_measure(dev, layers_n=30, warm_passes=20):
 
 
 def hip_probes(dev):
-    """The HIP roofline probes of libomnimem_probe.so: an MFMA issue loop (4
-    independent v_mfma_f32_32x32x16_bf16 chains per wave), a streaming read and a
-    streaming copy of 1 GiB.  Best of a few launch shapes each; HIP events on the
+    """The HIP roofline probes of libomnimem_probe.so: MFMA issue loops (4
+    independent v_mfma_f32_32x32x16_bf16 chains per wave; the same with the fp32
+    16x16x4 and 32x32x2 MFMAs), a streaming read and a streaming copy of 1 GiB.  Best of a few launch shapes each; HIP events on the
     launch stream."""
     import ctypes
 
@@ -949,6 +949,8 @@ def hip_probes(dev):
     P = ctypes.CDLL(_build.PROBE_LIB)
     P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
                                           ctypes.c_void_p]
+    P.omnimem_probe_mfma_f32.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
                                      ctypes.c_void_p]
     P.omnimem_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
@@ -978,6 +980,17 @@ def hip_probes(dev):
     out["mfma_bf16_tflops"] = best
     # 2.5 PFLOP/s bf16 is 1024 flops per cycle per SIMD on 1024 SIMDs at 2.4 GHz
     out["mfma_implied_clock_ghz"] = round(best / PEAK_BF16_TFLOPS * 2.4, 3)
+    # fp32 MFMA (the selection's score products): 16x16x4 and 32x32x2, against 157.3 TF
+    f32 = []
+    for shape, fl in ((0, 2048.0), (1, 4096.0)):
+        for wgs, wps, iters in ((256, 1, 50000), (512, 2, 25000)):
+            ms = timed(lambda: P.omnimem_probe_mfma_f32(shape, iters, wgs, wps, ctypes.c_void_p(sink.data_ptr()),
+                                                        stream), 5)
+            flops = wgs * 4 * wps * iters * 4 * fl
+            f32.append({"shape": ["16x16x4", "32x32x2"][shape], "workgroups": wgs, "waves_per_simd": wps,
+                        "tflops": round(flops / (ms * 1e-3) / 1e12, 1)})
+    out["mfma_f32"] = f32
+    out["mfma_f32_tflops"] = max(m["tflops"] for m in f32)
     nbytes = 1 << 30
     a = torch.empty(nbytes, dtype=torch.uint8, device=dev).fill_(1)
     b = torch.empty_like(a)

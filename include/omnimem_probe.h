@@ -24,6 +24,12 @@ extern "C" {
 int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
                                 void* stream);
 
+/* fp32 MFMA issue loop, as above with 4 independent chains of
+   v_mfma_f32_16x16x4_f32 (shape 0, 2048 flops each) or v_mfma_f32_32x32x2_f32
+   (shape 1, 4096 flops each) per round. */
+int32_t omnimem_probe_mfma_f32(int32_t shape, int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
+                               void* stream);
+
 /* Streaming copy of `bytes` (a multiple of 16, 16-byte aligned buffers) from src
    to dst with 16-byte loads and stores, grid-stride over `workgroups` workgroups of
    256 threads. */

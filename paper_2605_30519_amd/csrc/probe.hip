@@ -34,6 +34,36 @@ __global__ __launch_bounds__(512) void k_mfma_loop(int64_t iters, float* __restr
   if (s == -1.2345e30f) sink[0] = s;
 }
 
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
+// fp32 MFMA issue loop: SHAPE 0 = v_mfma_f32_16x16x4_f32 (2048 flops), 1 =
+// v_mfma_f32_32x32x2_f32 (4096 flops); 4 independent chains per wave.
+template <int SHAPE>
+__global__ __launch_bounds__(512) void k_mfma_f32_loop(int64_t iters, float* __restrict__ sink) {
+  const float a = 1.0f + 1e-3f * static_cast<float>(threadIdx.x % 64), b = 1.0f - 1e-3f * static_cast<float>(threadIdx.x % 64);
+  float s = 0.f;
+  if constexpr (SHAPE == 0) {
+    f32x4 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    for (int64_t it = 0; it < iters; ++it) {
+      c0 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c1, 0, 0, 0);
+      c2 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c2, 0, 0, 0);
+      c3 = __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c3, 0, 0, 0);
+    }
+    for (int i = 0; i < 4; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+  } else {
+    f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
+    for (int64_t it = 0; it < iters; ++it) {
+      c0 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c0, 0, 0, 0);
+      c1 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c1, 0, 0, 0);
+      c2 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c2, 0, 0, 0);
+      c3 = __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c3, 0, 0, 0);
+    }
+    for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
+  }
+  if (s == -1.2345e30f) sink[0] = s;
+}
+
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
@@ -72,6 +102,17 @@ int32_t status(hipError_t e) { return e == hipSuccess ? 0 : -4; }
 using omnimem::launch_kernel;
 
 }  // namespace
+
+PROBE_API int32_t omnimem_probe_mfma_f32(int32_t shape, int64_t iters, int32_t workgroups, int32_t waves_per_simd,
+                                         float* sink, void* stream) {
+  if (shape < 0 || shape > 1 || iters < 1 || workgroups < 1 || waves_per_simd < 1 || waves_per_simd > 2 ||
+      sink == nullptr)
+    return -1;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (shape == 0)
+    return status(launch_kernel(k_mfma_f32_loop<0>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
+  return status(launch_kernel(k_mfma_f32_loop<1>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
+}
 
 PROBE_API int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
                                           void* stream) {

@@ -913,6 +913,217 @@ __global__ __launch_bounds__(kTopkSmallWaves* kWave) void k_topk_small(const uin
   if (lane == 0) cnt[row] = taken;
 }
 
+// Scores and top-K in one kernel, for many query groups and small K (the small-group
+// setting: groups of G_q rows, K blocks each): no score row is stored.  A workgroup
+// takes 16 groups of one head; its NW waves split the head's blocks, each streaming
+// its share 16 blocks at a time, two tiles ahead.  A tile's 16 x 16 scores come from fp32 MFMA
+// (16x16x4): at step (u, e) lane group j = l / 16 supplies dimension 16 u + 4 j + e
+// of its lane's group (A operand) and block (B operand), so the proxy queries stay
+// in registers and the four lane groups of a block read 64 contiguous bytes of its
+// row per load.  Lane l ends
+// a tile with block b0 + l % 16 scored against groups 4 j .. 4 j + 3 and keeps, per
+// group, the KM best (key, id) pairs it has seen (ids arrive in increasing order).
+// The lists meet in LDS, where half a wave per group merges them; ranking and ties
+// are those of k_topk (key, then lower id).
+constexpr int kStkGroups = 16;
+
+template <int D, int KM, int NW>
+__global__ __launch_bounds__(NW* kWave) void k_score_topk(
+    const float* __restrict__ kbar, int64_t kbar_stride, const float* __restrict__ qpart, int nsplit, int lq, int G,
+    const int32_t* __restrict__ page_table, int64_t pt_stride, int64_t num_pages, int nb, int first_excluded, int R,
+    float scale, int K, int32_t* __restrict__ idx, int32_t* __restrict__ cnt, float* __restrict__ score_out) {
+  constexpr int DS = D / 4;    // dimensions per lane group
+  constexpr int NV = DS / 4;   // 16-byte loads per lane per tile: load u covers dimensions [16 u, 16 u + 16)
+  __shared__ uint64_t cand[kStkGroups][NW * 16 * KM];
+  const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+  const int col = lane % 16, j = lane / 16;
+  // workgroups of one head on one XCD, whose L2 then holds that head's pooled keys
+  const int wg = xcd_contiguous_id(blockIdx.x, gridDim.x), tiles = (R + kStkGroups - 1) / kStkGroups;
+  const int h = wg / tiles, g0 = (wg % tiles) * kStkGroups;
+
+  // the proxy query of group g0 + col, dimensions 16 u + 4 j + e: its partial sums
+  // added in split order, divided by the group's row count
+  float qa[DS];
+  {
+    const int g = g0 + col;
+    float4 sum[NV];
+#pragma unroll
+    for (int u = 0; u < NV; ++u) sum[u] = make_float4(0.f, 0.f, 0.f, 0.f);
+    float inv_rows = 0.f;
+    if (g < R) {
+      const int rows = min(g * G + G, lq) - g * G;
+      const int used = (rows + kQRowsPerSplit - 1) / kQRowsPerSplit;
+      const float* src = qpart + (static_cast<int64_t>(h) * R + g) * nsplit * D + 4 * j;
+      for (int sp = 0; sp < used; ++sp) {
+        float4 v[NV];
+#pragma unroll
+        for (int u = 0; u < NV; ++u) v[u] = *reinterpret_cast<const float4*>(src + static_cast<int64_t>(sp) * D + 16 * u);
+#pragma unroll
+        for (int u = 0; u < NV; ++u) {
+          sum[u].x += v[u].x;
+          sum[u].y += v[u].y;
+          sum[u].z += v[u].z;
+          sum[u].w += v[u].w;
+        }
+      }
+      inv_rows = 1.0f / static_cast<float>(rows);
+    }
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      qa[4 * u + 0] = sum[u].x * inv_rows;
+      qa[4 * u + 1] = sum[u].y * inv_rows;
+      qa[4 * u + 2] = sum[u].z * inv_rows;
+      qa[4 * u + 3] = sum[u].w * inv_rows;
+    }
+  }
+
+  // this wave's blocks [bw0, bw1): share (wave + group tile) mod NW, so that the
+  // workgroups of one head read different rows of its pooled keys at a time
+  const int per = ((nb + NW - 1) / NW + 15) / 16 * 16;
+  const int share = (wave + wg % tiles) % NW;
+  const int bw0 = share * per, bw1 = min(bw0 + per, nb);
+  const int32_t* table = page_table ? page_table + static_cast<int64_t>(h) * pt_stride : nullptr;
+  const float* kh = kbar + static_cast<int64_t>(h) * kbar_stride * D;
+
+  uint32_t lk[4][KM];
+  int li[4][KM];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < KM; ++t) {
+      lk[i][t] = 0u;
+      li[i][t] = 0;
+    }
+  // insertion into a descending list without branches (k > lk[t] holds for a prefix
+  // of t), skipped as a whole when no lane of the wave has a key to insert
+  auto insert = [&](uint32_t (&lkk)[KM], int (&lii)[KM], uint32_t k, int id) {
+    if (!__any(k > lkk[KM - 1])) return;
+    bool gt[KM];
+#pragma unroll
+    for (int t = 0; t < KM; ++t) gt[t] = k > lkk[t];
+#pragma unroll
+    for (int t = KM - 1; t > 0; --t) {
+      lkk[t] = gt[t - 1] ? lkk[t - 1] : (gt[t] ? k : lkk[t]);
+      lii[t] = gt[t - 1] ? lii[t - 1] : (gt[t] ? id : lii[t]);
+    }
+    lkk[0] = gt[0] ? k : lkk[0];
+    lii[0] = gt[0] ? id : lii[0];
+  };
+
+  // three tile buffers: tile t is scored while tiles t + 1 and t + 2 are in flight.
+  // A tile's page ids are loaded with it and looked at only when it is scored, so
+  // that no wait for its loads is placed at the fetch.
+  float4 kb0[NV], kb1[NV], kb2[NV];
+  int pg0 = -1, pg1 = -1, pg2 = -1;
+  // Loads are unconditional (rows past the wave's share read a valid row, whose
+  // scores are then not candidates): no branch around them, so the compiler's
+  // waits count the loads still in flight instead of draining them all.
+  auto fetch = [&](int b0, float4 (&dst)[NV], int& page) {
+    const int b = min(b0 + col, nb - 1);
+#pragma unroll
+    for (int u = 0; u < NV; ++u)
+      dst[u] = *reinterpret_cast<const float4*>(kh + static_cast<int64_t>(b) * D + 16 * u + 4 * j);
+    page = table ? table[b] : 0;
+  };
+  // scores of the tile in kv (block b0 + col), four independent MFMA chains
+  auto score_tile = [&](int b0, const float4 (&kv)[NV], int page) {
+    const int b = b0 + col;
+    const bool live = b < bw1 && b < first_excluded && page >= 0 && (table == nullptr || page < num_pages);
+    f32x4 acc[4] = {};
+#pragma unroll
+    for (int u = 0; u < NV; ++u) {
+      acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[4 * u + 0], kv[u].x, acc[0], 0, 0, 0);
+      acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[4 * u + 1], kv[u].y, acc[1], 0, 0, 0);
+      acc[2] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[4 * u + 2], kv[u].z, acc[2], 0, 0, 0);
+      acc[3] = __builtin_amdgcn_mfma_f32_16x16x4f32(qa[4 * u + 3], kv[u].w, acc[3], 0, 0, 0);
+    }
+    // acc: block b0 + col against groups g0 + 4 j + i
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float dot = (acc[0][i] + acc[1][i]) + (acc[2][i] + acc[3][i]);
+      insert(lk[i], li[i], live ? score_key(scale * dot) : 0u, b0 + col);
+    }
+  };
+  fetch(bw0, kb0, pg0);
+  fetch(bw0 + 16, kb1, pg1);
+  for (int b0 = bw0; b0 < bw1; b0 += 48) {
+    fetch(b0 + 32, kb2, pg2);
+    score_tile(b0, kb0, pg0);
+    if (b0 + 16 >= bw1) break;
+    fetch(b0 + 48, kb0, pg0);
+    score_tile(b0 + 16, kb1, pg1);
+    if (b0 + 32 >= bw1) break;
+    fetch(b0 + 64, kb1, pg1);
+    score_tile(b0 + 32, kb2, pg2);
+  }
+
+  // every lane's lists to LDS, per group: candidate (wave, col, t) of group 4 j + i
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int t = 0; t < KM; ++t)
+      cand[4 * j + i][(wave * 16 + col) * KM + t] =
+          lk[i][t] == 0u ? 0ull
+                         : (static_cast<uint64_t>(lk[i][t]) << 32) | static_cast<uint32_t>(~static_cast<uint32_t>(li[i][t]));
+  __syncthreads();
+
+  // half-wave (32 lanes) per group: each lane keeps the KM best of its share of the
+  // group's NW * 16 * KM candidates, then K rounds of a 32-lane maximum name the
+  // winners (the largest (key, lower id) composite), written in ascending id order
+  constexpr int kPerLane = NW * 16 * KM / 32;
+  const int half = lane / 32, l32 = lane % 32;
+  for (int m = 2 * wave + half; m < kStkGroups; m += 2 * NW) {
+    uint64_t top[KM];
+#pragma unroll
+    for (int t = 0; t < KM; ++t) top[t] = 0ull;
+#pragma unroll
+    for (int c = 0; c < kPerLane; ++c) {
+      uint64_t v = cand[m][l32 + 32 * c];
+      if (v > top[KM - 1]) {
+#pragma unroll
+        for (int t = 0; t < KM; ++t) {  // insertion into the descending list
+          const uint64_t hi = top[t] > v ? top[t] : v, lo = top[t] > v ? v : top[t];
+          top[t] = hi;
+          v = lo;
+        }
+      }
+    }
+    uint64_t win = 0ull;
+    int taken = 0;
+    for (int r = 0; r < K; ++r) {
+      uint64_t best = top[0];
+#pragma unroll
+      for (int off = 16; off >= 1; off >>= 1) {
+        const uint64_t o = __shfl_xor(best, off);
+        best = o > best ? o : best;
+      }
+      if (best == 0ull) break;  // fewer than K candidates (uniform within the half)
+      if (top[0] == best) {
+#pragma unroll
+        for (int t = 0; t + 1 < KM; ++t) top[t] = top[t + 1];
+        top[KM - 1] = 0ull;
+      }
+      if (l32 == r) win = best;
+      ++taken;
+    }
+    const int g = g0 + m;
+    if (g < R) {
+      const int id = static_cast<int>(~static_cast<uint32_t>(win));
+      int rank = 0;
+      for (int s2 = 0; s2 < taken; ++s2) rank += __shfl(id, half * 32 + s2) < id;
+      const int64_t row = static_cast<int64_t>(h) * R + g;
+      if (l32 < taken) {
+        idx[row * K + rank] = id;
+        if (score_out) score_out[row * K + rank] = key_score(static_cast<uint32_t>(win >> 32));
+      } else if (l32 < K) {
+        idx[row * K + l32] = -1;
+        if (score_out) score_out[row * K + l32] = -INFINITY;
+      }
+      if (l32 == 0) cnt[row] = taken;
+    }
+  }
+}
+
 // Top-K for rows longer than the register-resident kernel holds: one wavefront,
 // keys re-read at every step of a plain bisection.
 __global__ __launch_bounds__(kWave) void k_topk_wide(const uint32_t* __restrict__ keys, int nb, int nbp, int K,
@@ -1036,6 +1247,23 @@ hipError_t launch_topk(const CacheGeom& g, const SelectPlan& p, const uint32_t* 
   return launch_kernel(k_topk_wide, tgrid, dim3(kWave), 0, stream, keys, g.nb, nbp, p.K, idx, cnt, score);
 }
 
+// Many groups and small K: the scores and their top-K in one kernel.
+bool fused_score_topk(const SelectPlan& p) { return p.K <= kTopkSmallK && p.R >= kScoreTiledMinGroups; }
+
+template <int D>
+hipError_t launch_score_topk(const CacheGeom& g, const SelectPlan& p, const float* kbar, int64_t kbar_stride,
+                             const float* qpart, int32_t* idx, int32_t* cnt, float* score, hipStream_t stream) {
+  // eight waves (two per SIMD) for K <= 4; the longer lists of K <= 16 take four
+  const dim3 grid((p.R + kStkGroups - 1) / kStkGroups * g.H);
+  if (p.K <= 4)
+    return launch_kernel(k_score_topk<D, 4, 8>, grid, dim3(8 * kWave), 0, stream, kbar, kbar_stride, qpart, p.qsplit,
+                         p.lq, p.G, g.page_table, g.pt_stride, g.num_pages, g.nb, p.first_excluded, p.R, p.scale, p.K,
+                         idx, cnt, score);
+  return launch_kernel(k_score_topk<D, kTopkSmallK, 4>, grid, dim3(4 * kWave), 0, stream, kbar, kbar_stride, qpart,
+                       p.qsplit, p.lq, p.G, g.page_table, g.pt_stride, g.num_pages, g.nb, p.first_excluded, p.R,
+                       p.scale, p.K, idx, cnt, score);
+}
+
 template <typename T, int D>
 hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
                                float* score, void* workspace, hipStream_t stream) {
@@ -1080,8 +1308,11 @@ hipError_t launch_select_typed(const CacheGeom& g, const SelectPlan& p, const vo
       else if (p.R == 1) pool(k_pool_score<T, D, 128, 1>);
       else pool(k_pool_score<T, D, 128, kInlineGroups>);
     }
-    if (!p.inline_scores && st.err == hipSuccess)
+    if (!p.inline_scores && st.err == hipSuccess) {
+      if (fused_score_topk(p))
+        return launch_score_topk<D>(g, p, kbar, static_cast<int64_t>(g.nb), qpart, idx, cnt, score, stream);
       st.add(launch_score<D>(g, p, kbar, static_cast<int64_t>(g.nb), qpart, nbp, keys, stream));
+    }
   }
   if (st.err != hipSuccess) return st.err;
   return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
@@ -1129,6 +1360,8 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
     return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);
   }
   hipError_t e = launch_qmean<T, D>(p, g, static_cast<const T*>(q), qpart, stream);
+  if (e == hipSuccess && g.nb > 0 && fused_score_topk(p))
+    return launch_score_topk<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, idx, cnt, score, stream);
   if (e == hipSuccess && g.nb > 0)
     e = launch_score<D>(g, p, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), qpart, nbp, keys, stream);
   if (e != hipSuccess) return e;

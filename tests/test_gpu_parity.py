@@ -266,6 +266,37 @@ def test_long_lists_and_ties(dev, n, zero_q):
         assert got[0, 0].tolist() == omega[:64]
 
 
+@pytest.mark.parametrize("d,K,per_head,zero_q", [(64, 10, True, False), (128, 4, False, False), (64, 16, False, True),
+                                                  (128, 7, True, True), (64, 3, False, False)])
+def test_many_groups_small_k(dev, d, K, per_head, zero_q):
+    """Many query groups (R = 75) and K <= 16: scores and top-K in one kernel, with 240
+    candidate blocks split over its waves in several 16-block tiles, non-resident
+    blocks, per-head tables; zero queries make every score 0, so each group takes its
+    K lowest candidate ids."""
+    H, S, Lq, B, n, G = 2, 200, 600, 64, 60, 8
+    say(f"many groups d={d} K={K} per_head={per_head} zero_q={zero_q}")
+    w = synth.Workload("groups", H, d, S, Lq, B, n, n, K, G, 1, 2, torch.bfloat16, True, 1, 13)
+    x = synth.make_layer(w, 0, device=dev)
+    if zero_q:
+        x.q.zero_()
+    nb = n * w.blocks_per_chunk
+    if per_head:
+        cache = synth.page_layer_per_head(x.k, x.v, B, seed=8, nonresident={0: [2, 40, nb - 9], 1: [0, 1]})
+    else:
+        cache = synth.page_layer(x.k, x.v, B, seed=8, nonresident=[3, 77, 150])
+    mask = synth.resident_mask(cache).numpy()
+    sel = run_select(cache, x, w)
+    got = host(sel.idx).numpy()
+    for h in range(H):
+        res = mask[h] if mask.ndim == 2 else mask
+        ref = oracle.select(host(x.q), host(x.k), B, K, G, 1, 2, w.scale, resident=res, heads=(h, h + 1),
+                            want_all_scores=True)
+        check_selection(got, host(sel.cnt).numpy(), ref, heads=[h])
+        if zero_q:
+            omega = [b for b in range(nb - w.blocks_per_chunk) if res[b]]  # the last chunk is the window
+            assert (got[h] == np.array(omega[:K], np.int32)).all()
+
+
 # ------------------------------------------------------------ full-size workloads
 
 def planted_recall(sel, x, w, n):
