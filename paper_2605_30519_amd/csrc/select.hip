@@ -63,7 +63,7 @@ __global__ __launch_bounds__(NT) void k_qmean_partial(const T* __restrict__ q, i
 #pragma unroll
     for (int u = 0; u < UNROLL; ++u) {
       const int rr = row + u * PHASES;
-      raw[u] = rr < r1 ? *reinterpret_cast<const uint4*>(q + (static_cast<int64_t>(rr) * H + h) * D + cs * DC + c * VEC)
+      raw[u] = rr < r1 ? load_once(q + (static_cast<int64_t>(rr) * H + h) * D + cs * DC + c * VEC)
                        : make_uint4(0, 0, 0, 0);
     }
 #pragma unroll
@@ -150,7 +150,7 @@ __device__ __forceinline__ void load_slab(const T* __restrict__ slab, int nvalid
 #pragma unroll
   for (int i = 0; i < Sh::PASSES; ++i) {
     const int row = ph + i * Sh::ROWS_PER_PASS;
-    raw[i] = row < nvalid ? *reinterpret_cast<const uint4*>(slab + row * D + c * Sh::VEC) : make_uint4(0, 0, 0, 0);
+    raw[i] = row < nvalid ? load_once(slab + row * D + c * Sh::VEC) : make_uint4(0, 0, 0, 0);
   }
 }
 
