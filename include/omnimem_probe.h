@@ -31,12 +31,12 @@ int32_t omnimem_probe_mfma_f32(int32_t shape, int64_t iters, int32_t workgroups,
                                void* stream);
 
 /* Streaming copy of `bytes` (a multiple of 16, 16-byte aligned buffers) from src
-   to dst with 16-byte loads and stores, grid-stride over `workgroups` workgroups of
-   256 threads. */
+   to dst with 16-byte loads (nontemporal) and stores, grid-stride over `workgroups`
+   workgroups of 256 threads. */
 int32_t omnimem_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream);
 
-/* Streaming read of `bytes` (a multiple of 16, 16-byte aligned) with 16-byte loads;
-   sink as above. */
+/* Streaming read of `bytes` (a multiple of 16, 16-byte aligned) with nontemporal
+   16-byte loads; sink as above. */
 int32_t omnimem_probe_read(const void* src, int64_t bytes, int32_t workgroups, float* sink, void* stream);
 
 #ifdef __cplusplus

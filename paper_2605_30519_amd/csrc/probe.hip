@@ -67,6 +67,14 @@ __global__ __launch_bounds__(512) void k_mfma_f32_loop(int64_t iters, float* __r
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
+// 16-byte load with the nontemporal hint (streamed data: on gfx950 it raises a
+// streaming read from ~5.6 to ~6.3 TB/s)
+typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 load_once(const uint4* p) {
+  const u32x4v v = __builtin_nontemporal_load(reinterpret_cast<const u32x4v*>(p));
+  return make_uint4(v[0], v[1], v[2], v[3]);
+}
+
 __global__ __launch_bounds__(kThreads) void k_copy(const uint4* __restrict__ src, uint4* __restrict__ dst,
                                                    int64_t n) {
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
@@ -74,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void k_copy(const uint4* __restrict__ src
   for (; i + (kUnroll - 1) * stride < n; i += kUnroll * stride) {
     uint4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) v[u] = src[i + u * stride];
+    for (int u = 0; u < kUnroll; ++u) v[u] = load_once(src + i + u * stride);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) dst[i + u * stride] = v[u];
   }
@@ -89,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void k_read(const uint4* __restrict__ src
   for (; i + (kUnroll - 1) * stride < n; i += kUnroll * stride) {
     uint4 v[kUnroll];
 #pragma unroll
-    for (int u = 0; u < kUnroll; ++u) v[u] = src[i + u * stride];
+    for (int u = 0; u < kUnroll; ++u) v[u] = load_once(src + i + u * stride);
 #pragma unroll
     for (int u = 0; u < kUnroll; ++u) acc ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
   }

@@ -47,21 +47,39 @@ __global__ __launch_bounds__(kScanThreads) void k_union_scan(const int32_t* __re
   if (threadIdx.x == 0) *union_blocks = total;
 }
 
-// copy the (page, head) slabs of every union block into its slot, for K and V
+// copy the (page, head) slabs of every union block into its slot, for K and V; the
+// sources are read once (nontemporal loads), four rounds of loads in flight before
+// their stores
 __global__ __launch_bounds__(256) void k_union_gather(const uint4* __restrict__ k_pages,
                                                       const uint4* __restrict__ v_pages,
                                                       const int32_t* __restrict__ page_table,
                                                       const int32_t* __restrict__ table, int H,
                                                       int64_t slab_vec, uint4* __restrict__ kbuf,
                                                       uint4* __restrict__ vbuf) {
+  constexpr int kRounds = 4;
   const int b = blockIdx.x, h = blockIdx.y;
   const int slot = table[b];
   if (slot < 0) return;
   const int64_t src = (static_cast<int64_t>(page_table[b]) * H + h) * slab_vec;
   const int64_t dst = (static_cast<int64_t>(slot) * H + h) * slab_vec;
-  for (int64_t i = threadIdx.x; i < slab_vec; i += blockDim.x) {
-    kbuf[dst + i] = k_pages[src + i];
-    vbuf[dst + i] = v_pages[src + i];
+  for (int64_t i0 = threadIdx.x; i0 < slab_vec; i0 += kRounds * blockDim.x) {
+    uint4 kv[kRounds], vv[kRounds];
+#pragma unroll
+    for (int u = 0; u < kRounds; ++u) {
+      const int64_t i = i0 + static_cast<int64_t>(u) * blockDim.x;
+      if (i < slab_vec) {
+        kv[u] = load_once(k_pages + src + i);
+        vv[u] = load_once(v_pages + src + i);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kRounds; ++u) {
+      const int64_t i = i0 + static_cast<int64_t>(u) * blockDim.x;
+      if (i < slab_vec) {
+        kbuf[dst + i] = kv[u];
+        vbuf[dst + i] = vv[u];
+      }
+    }
   }
 }
 
