@@ -69,6 +69,9 @@ def parse():
     p.add_argument("--select-only", type=int, default=0, metavar="N",
                    help="only run N selections over the bench workload's rotated layer caches (a profiling "
                         "target), print their median time, and exit")
+    p.add_argument("--small-group-only", action="store_true",
+                   help="only run the small-group setting (G_q = 15, top-4: select and sparse attention, 150 "
+                        "calls each; a profiling target), print its line, and exit")
     p.add_argument("--prob-only", type=int, default=0, metavar="G",
                    help="only time selection by probability-averaged scores from the pooled history, "
                         "query groups of G rows (top-64 for one group per head, else top-4), and exit")
@@ -230,6 +233,9 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     lib()
+    if args.small_group_only:
+        print(json.dumps({"small_group": small_group_measure(dev)}))
+        return
     if args.prob_only:
         prob_only(dev, args.prob_only)
         return
