@@ -238,15 +238,17 @@ def test_running_max_jumps(dev):
 
 # ------------------------------------------------------------- long block lists
 
-@pytest.mark.parametrize("n,zero_q", [(5000, True), (5000, False), (20000, False), (20000, True), (33000, False),
-                                      (33000, True)])
-def test_long_lists_and_ties(dev, n, zero_q):
+@pytest.mark.parametrize("n,zero_q,K", [(5000, True, 64), (5000, False, 64), (20000, False, 64), (20000, True, 64),
+                                        (33000, False, 64), (33000, True, 64), (20000, False, 16), (33000, True, 16),
+                                        (33000, False, 3)])
+def test_long_lists_and_ties(dev, n, zero_q, K):
     """Top-K over long block lists: 5000 blocks spread over several key partitions of
     the register-resident search (512 threads), 20000 blocks need the 1024-thread
-    register search, 33000 blocks take the streaming search.  Zero queries make every
-    score exactly 0, so the lowest candidate ids must be chosen."""
-    say(f"long list n={n} zero_q={zero_q}")
-    w = synth.Workload("long", 1, 64, 64, 8, 64, n, n, 64, 8, 1, 1, torch.bfloat16, False, 1, 9)
+    register search, 33000 blocks take the streaming search; with K <= 16 the
+    one-wave-per-row kernel walks all of them.  Zero queries make every score
+    exactly 0, so the lowest candidate ids must be chosen."""
+    say(f"long list n={n} zero_q={zero_q} K={K}")
+    w = synth.Workload("long", 1, 64, 64, 8, 64, n, n, K, 8, 1, 1, torch.bfloat16, False, 1, 9)
     g = torch.Generator(device=dev).manual_seed(17 + n)
     k = torch.randn((n, 64, 1, 64), generator=g, device=dev).to(torch.bfloat16)
     q = torch.randn((8, 1, 64), generator=g, device=dev).to(torch.bfloat16)
@@ -263,7 +265,7 @@ def test_long_lists_and_ties(dev, n, zero_q):
     if zero_q:
         assert (got == ref["idx"]).all()
         omega = [b for b in range(n - 1) if resident[b]]  # the last chunk is the excluded window
-        assert got[0, 0].tolist() == omega[:64]
+        assert got[0, 0].tolist() == omega[:K]
 
 
 @pytest.mark.parametrize("d,K,per_head,zero_q", [(64, 10, True, False), (128, 4, False, False), (64, 16, False, True),
