@@ -439,7 +439,6 @@ __global__ __launch_bounds__(NW* kWave) void k_attn_bf16(AttnArgs a) {
 // online softmax, the same rounding.
 constexpr int kGrpWaves = 4;
 
-
 template <int D>
 __global__ __launch_bounds__(kGrpWaves* kWave, 1) void k_attn_bf16_groups(AttnArgs a) {
   using L = AttnLds<D>;

@@ -916,15 +916,15 @@ __global__ __launch_bounds__(kTopkSmallWaves* kWave) void k_topk_small(const uin
 // Scores and top-K in one kernel, for many query groups and small K (the small-group
 // setting: groups of G_q rows, K blocks each): no score row is stored.  A workgroup
 // takes 16 groups of one head; its NW waves split the head's blocks, each streaming
-// its share 16 blocks at a time, two tiles ahead.  A tile's 16 x 16 scores come from fp32 MFMA
-// (16x16x4): at step (u, e) lane group j = l / 16 supplies dimension 16 u + 4 j + e
-// of its lane's group (A operand) and block (B operand), so the proxy queries stay
-// in registers and the four lane groups of a block read 64 contiguous bytes of its
-// row per load.  Lane l ends
-// a tile with block b0 + l % 16 scored against groups 4 j .. 4 j + 3 and keeps, per
-// group, the KM best (key, id) pairs it has seen (ids arrive in increasing order).
-// The lists meet in LDS, where half a wave per group merges them; ranking and ties
-// are those of k_topk (key, then lower id).
+// its share 16 blocks at a time, two tiles ahead.  A tile's 16 x 16 scores come from
+// fp32 MFMA (16x16x4): at step (u, e) lane group j = l / 16 supplies dimension
+// 16 u + 4 j + e of its lane's group (A operand) and block (B operand), so the proxy
+// queries stay in registers and the four lane groups of a block read 64 contiguous
+// bytes of its row per load.  Lane l ends a tile with block b0 + l % 16 scored
+// against groups 4 j .. 4 j + 3 and keeps, per group, the KM best (key, id) pairs it
+// has seen (ids arrive in increasing order).  The lists meet in LDS, where half a
+// wave per group merges them; ranking and ties are those of k_topk (key, then lower
+// id).
 constexpr int kStkGroups = 16;
 
 template <int D, int KM, int NW>
