@@ -239,3 +239,29 @@ def test_probe_library_exports_its_header():
     out = subprocess.run(["nm", "-D", "--defined-only", _build.PROBE_LIB], capture_output=True, text=True).stdout
     exported = sorted({line.split()[-1] for line in out.splitlines() if " T " in line and "omnimem" in line})
     assert exported == declared
+
+
+def test_probe_argument_checks():
+    """Every probe refuses bad arguments with -1 before it touches the GPU (so this
+    runs without one)."""
+    from paper_2605_30519_amd import _build
+    P = ctypes.CDLL(_build.PROBE_LIB)
+    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
+                                          ctypes.c_void_p]
+    P.omnimem_probe_mfma_f32.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                         ctypes.c_void_p, ctypes.c_void_p]
+    P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
+    P.omnimem_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
+    sink = ctypes.c_void_p(0x1000)
+    assert P.omnimem_probe_mfma_bf16(0, 1, 1, sink, None) == -1          # no iterations
+    assert P.omnimem_probe_mfma_bf16(1, 1, 3, sink, None) == -1          # three waves per SIMD
+    assert P.omnimem_probe_mfma_bf16(1, 1, 1, None, None) == -1          # no sink
+    assert P.omnimem_probe_mfma_f32(2, 1, 1, 1, sink, None) == -1        # unknown shape
+    assert P.omnimem_probe_mfma_f32(0, 1, 0, 1, sink, None) == -1        # no workgroups
+    assert P.omnimem_probe_mfma_f32(1, 1, 1, 1, None, None) == -1        # no sink
+    buf = ctypes.c_void_p(0x10000)
+    assert P.omnimem_probe_copy(buf, None, 64, 1, None) == -1            # no destination
+    assert P.omnimem_probe_copy(buf, buf, 24, 1, None) == -1             # not a multiple of 16
+    assert P.omnimem_probe_copy(ctypes.c_void_p(0x10008), buf, 64, 1, None) == -1  # misaligned
+    assert P.omnimem_probe_read(buf, 64, 0, sink, None) == -1            # no workgroups
+    assert P.omnimem_probe_read(buf, 64, 1, None, None) == -1            # no sink
