@@ -98,9 +98,9 @@ SMALL = [
     (2, 128, 300, 1000, 64, 14, 4, 15, 1, 3, torch.bfloat16),  # G = 15, R = 67: tiled scoring, ragged tiles
     (2, 128, 300, 100, 128, 4, 3, 40, 0, 0, torch.float32),    # fp32, d = 128, B = 128, no window
     (1, 64, 64, 1, 64, 3, 2, 1, 2, 0, torch.float32),          # one query row, exact-block chunks
-    (2, 64, 200, 100, 64, 5, 4, 15, 1, 3, torch.bfloat16),     # bf16, d = 64, groups of at most 32 rows
-    (3, 64, 200, 30, 64, 5, 4, 30, 1, 2, torch.bfloat16),      # bf16, d = 64, Lq <= 32: dense on the small variant
-    (2, 128, 130, 20, 64, 4, 3, 7, 1, 1, torch.bfloat16),      # bf16, d = 128, Lq <= 32: dense on the small variant
+    (2, 64, 200, 100, 64, 5, 4, 15, 1, 3, torch.bfloat16),     # bf16, d = 64, groups of at most 32 rows (one wave per group)
+    (3, 64, 200, 30, 64, 5, 4, 30, 1, 2, torch.bfloat16),      # bf16, d = 64, Lq <= 32: dense, one wave per group
+    (2, 128, 130, 20, 64, 4, 3, 7, 1, 1, torch.bfloat16),      # bf16, d = 128, Lq <= 32: dense, one wave per group
     (2, 64, 300, 130, 128, 4, 3, 65, 1, 2, torch.bfloat16),    # bf16, d = 64, B = 128, groups of 65 rows
 ]
 
