@@ -72,6 +72,10 @@ def parse():
     p.add_argument("--small-group-only", action="store_true",
                    help="only run the small-group setting (G_q = 15, top-4: select and sparse attention, 150 "
                         "calls each; a profiling target), print its line, and exit")
+    p.add_argument("--power-clock", action="store_true",
+                   help="only sample socket power and GFX clock while the attention kernel (the bench layer's "
+                        "queries, then Q = 0) and the MFMA issue loop (smooth, then random operands) each run "
+                        "back to back for a few seconds, print the line, and exit")
     p.add_argument("--prob-only", type=int, default=0, metavar="G",
                    help="only time selection by probability-averaged scores from the pooled history, "
                         "query groups of G rows (top-64 for one group per head, else top-4), and exit")
@@ -135,6 +139,78 @@ def attn_only(dev, calls, warm=200):
     fl = attn_flops(sel.idx, sel.cnt, w, w.history_chunks)
     print(json.dumps({"attn_only": {"workload": WORKLOAD, "calls": calls, "ms": round(ms, 4),
                                     "tflops": round(fl / (ms * 1e-3) / 1e12, 1), "flops_per_call": fl}}), flush=True)
+
+
+def power_clock(dev, secs=6.0):
+    """Socket power and GFX clock, read through torch.cuda (the SMI library) twice
+    while each load runs back to back for `secs`: the attention kernel on the bench
+    workload's first layer with its queries and with Q = 0 (all scores 0, so P is
+    constant and few MFMA operand bits toggle), and the MFMA issue loop of the probe
+    library with smooth and with random operands.  The chip holds its clock only
+    while its power stays within the limit, and MFMA power grows with the operand
+    bits that toggle: this is what sets the clock at which the kernels run."""
+    import ctypes
+    import threading
+
+    import torch
+
+    from paper_2605_30519_amd import _build, omnimem_select, omnimem_sparse_attn, synth
+    w = synth.WORKLOADS[WORKLOAD]
+    x = synth.make_layer(w, 0, device=dev)
+    cache = synth.page_layer(x.k, x.v, w.block_size, seed=1000)
+    sel = omnimem_select(cache, x.q, w.top_k, w.group_size, w.window_chunks, w.awe_min_outside_chunks, w.scale)
+    out = torch.empty_like(x.q)
+    lse = torch.empty((w.heads, w.query_tokens), dtype=torch.float32, device=dev)
+    q0 = torch.zeros_like(x.q)
+    fl = attn_flops(sel.idx, sel.cnt, w, w.history_chunks)
+    P = ctypes.CDLL(_build.PROBE_LIB)
+    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    sink = torch.zeros(4, dtype=torch.float32, device=dev)
+    iters = 100000  # 256 workgroups of 4 waves: ~6 ms per launch
+    mfma_fl = 256 * 4 * iters * 4 * 32768.0
+
+    def mfma(operands):
+        assert P.omnimem_probe_mfma_bf16(operands, iters, 256, 1, ctypes.c_void_p(sink.data_ptr()), stream) == 0
+
+    loads = [("attention", lambda: omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale,
+                                                       out=out, lse=lse), fl, 1000),
+             ("attention_q0", lambda: omnimem_sparse_attn(cache, q0, sel.idx, sel.cnt, w.group_size, w.scale,
+                                                          out=out, lse=lse), fl, 1000),
+             ("mfma_smooth", lambda: mfma(0), mfma_fl, 20),
+             ("mfma_random", lambda: mfma(1), mfma_fl, 20)]
+    res = {"workload": WORKLOAD, "seconds_per_load": secs}
+    for name, call, flops, batch in loads:
+        samples = []
+
+        def sampler():
+            for delay in (0.5 * secs, 0.25 * secs):
+                time.sleep(delay)
+                samples.append((float(torch.cuda.power_draw(dev)), float(torch.cuda.clock_rate(dev))))
+
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(batch):
+            call()
+        torch.cuda.synchronize()
+        th = threading.Thread(target=sampler)
+        calls = 0
+        t_stop = time.time() + secs
+        th.start()
+        e0.record()
+        while time.time() < t_stop:
+            for _ in range(batch):
+                call()
+            calls += batch
+            torch.cuda.synchronize()
+        e1.record()
+        torch.cuda.synchronize()
+        th.join()
+        ms = e0.elapsed_time(e1) / calls
+        res[name] = {"us_per_call": round(ms * 1e3, 1), "tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+                     "socket_power_w": [s[0] for s in samples], "gfx_clock_mhz": [s[1] for s in samples]}
+        log(f"{name}: {res[name]}")
+    print(json.dumps({"power_clock": res}), flush=True)
 
 
 def select_only(dev, calls, warm=100):
@@ -235,6 +311,9 @@ def main():
     lib()
     if args.small_group_only:
         print(json.dumps({"small_group": small_group_measure(dev)}))
+        return
+    if args.power_clock:
+        power_clock(dev)
         return
     if args.prob_only:
         prob_only(dev, args.prob_only)
@@ -953,8 +1032,8 @@ def hip_probes(dev):
 
     from paper_2605_30519_amd import _build
     P = ctypes.CDLL(_build.PROBE_LIB)
-    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                          ctypes.c_void_p]
+    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_mfma_f32.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
@@ -976,16 +1055,18 @@ def hip_probes(dev):
         return e0.elapsed_time(e1) / reps
 
     out = {"probe_library": os.path.basename(_build.PROBE_LIB)}
-    mfma = []
-    for wgs, wps, iters in ((256, 1, 100000), (1024, 1, 25000), (512, 2, 50000)):
-        ms = timed(lambda: P.omnimem_probe_mfma_bf16(iters, wgs, wps, ctypes.c_void_p(sink.data_ptr()), stream), 5)
-        flops = wgs * 4 * wps * iters * 4 * 32768.0
-        mfma.append({"workgroups": wgs, "waves_per_simd": wps, "tflops": round(flops / (ms * 1e-3) / 1e12, 1)})
-    best = max(m["tflops"] for m in mfma)
-    out["mfma_bf16"] = mfma
-    out["mfma_bf16_tflops"] = best
-    # 2.5 PFLOP/s bf16 is 1024 flops per cycle per SIMD on 1024 SIMDs at 2.4 GHz
-    out["mfma_implied_clock_ghz"] = round(best / PEAK_BF16_TFLOPS * 2.4, 3)
+    for operands, key in ((0, "mfma_bf16"), (1, "mfma_bf16_random")):
+        mfma = []
+        for wgs, wps, iters in ((256, 1, 100000), (1024, 1, 25000), (512, 2, 50000)):
+            ms = timed(lambda: P.omnimem_probe_mfma_bf16(operands, iters, wgs, wps, ctypes.c_void_p(sink.data_ptr()),
+                                                         stream), 5)
+            flops = wgs * 4 * wps * iters * 4 * 32768.0
+            mfma.append({"workgroups": wgs, "waves_per_simd": wps, "tflops": round(flops / (ms * 1e-3) / 1e12, 1)})
+        best = max(m["tflops"] for m in mfma)
+        out[key] = mfma
+        out[key + "_tflops"] = best
+        # 2.5 PFLOP/s bf16 is 1024 flops per cycle per SIMD on 1024 SIMDs at 2.4 GHz
+        out[key.replace("mfma_bf16", "mfma_implied_clock_ghz")] = round(best / PEAK_BF16_TFLOPS * 2.4, 3)
     # fp32 MFMA (the selection's score products): 16x16x4 and 32x32x2, against 157.3 TF
     f32 = []
     for shape, fl in ((0, 2048.0), (1, 4096.0)):
@@ -1051,6 +1132,7 @@ def probe_peaks(dev, result):
     att = result["stages"]["attention_roofline"]["achieved"]
     sel = result["stages"]["select_roofline"]["achieved"]
     out["attention_frac_of_mfma_probe"] = round(att / out["hip"]["mfma_bf16_tflops"], 4)
+    out["attention_frac_of_mfma_random_probe"] = round(att / out["hip"]["mfma_bf16_random_tflops"], 4)
     out["attention_frac_of_gemm"] = round(att / out["bf16_gemm_tflops"], 4)
     out["select_frac_of_read_probe"] = round(sel / out["hip"]["hbm_read_gbs"], 4)
     return out

@@ -19,10 +19,13 @@ extern "C" {
 
 /* MFMA issue loop: `workgroups` workgroups of 4*waves_per_simd waves, each wave
    issuing `iters` rounds of 4 independent v_mfma_f32_32x32x16_bf16 (4 x 32768
-   flops per round).  sink: >= 1 float, written only if the sums take an impossible
-   value (it keeps the loop from being optimised away). */
-int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
-                                void* stream);
+   flops per round).  operands: 0 = one smooth per-lane operand pair for all four
+   chains (few operand bits toggle), 1 = four pairs of random unit-order operands,
+   one per chain (consecutive MFMAs see unrelated data; the chip's power limit then
+   sets a lower clock).  sink: >= 1 float, written only if the sums take an
+   impossible value (it keeps the loop from being optimised away). */
+int32_t omnimem_probe_mfma_bf16(int32_t operands, int64_t iters, int32_t workgroups, int32_t waves_per_simd,
+                                float* sink, void* stream);
 
 /* fp32 MFMA issue loop, as above with 4 independent chains of
    v_mfma_f32_16x16x4_f32 (shape 0, 2048 flops each) or v_mfma_f32_32x32x2_f32

@@ -733,12 +733,13 @@ __global__ __launch_bounds__(kGrpWaves* kWave, 1) void k_attn_bf16_groups(AttnAr
 // from inside the wave: the instruction stream alternates MFMAs of one half with
 // the softmax VALU work of the other (QK of half 1 with the exponentials of half
 // 0, PV of half 0 with the exponentials of half 1), and MFMAs run asynchronously.
-// The running max may lag the true one: O and l are rescaled only when exponentials
-// against the stale max could exceed 2^8, well inside fp32 and bf16 range, and the
-// final normalisation cancels the stale max exactly.
+// The running max starts as the first tile's own max and may then lag the true one:
+// O and l are rescaled only when exponentials against the stale max could exceed 2^8,
+// well inside fp32 and bf16 range, and the final normalisation cancels the stale max
+// exactly.
 constexpr int kR64Waves = 4;
 constexpr float kSlackSum = 256.0f;  // 2^8: how far exponentials may exceed 1 before O is rescaled
-constexpr float kNoMax = -1.0e30f;   // initial running max: finite, below any score (first tile rescales)
+constexpr float kNoMax = -1.0e30f;   // running max before the first tile: finite, below any score
 
 // max / sum of a value over the lane pair (l, l ^ 32)
 __device__ __forceinline__ float pair_max(float v) {
@@ -1021,14 +1022,16 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   };
   // The exponentials of a half are computed against its running max before the
-  // tile's own max is known.  They stand (every p <= 2^8) unless some lane's sum of
-  // them exceeds 2^8 or overflowed; only then is the tile's S formed again from the K
-  // still in LDS (stage kst, nvalid keys), its max taken, O and l moved to the new max
-  // and the exponentials redone.  The next tile's exponentials are formed after this
-  // point, against the new max.
+  // tile's own max is known (the first tile's against its own max, taken once).  They
+  // stand (every p <= 2^8) unless some lane's sum of them exceeds 2^8 or overflowed,
+  // which takes a rise of the max by more than 3 log2 units; only then is the tile's S
+  // formed again from the K still in LDS (stage kst, nvalid keys), its max taken, O
+  // and l moved to the new max and the exponentials redone.  The next tile's
+  // exponentials are formed after this point, against the new max.  The rare path is
+  // laid out away from the loop, which then runs straight through.
   auto settle = [&](float& ms, float& l, float acc, f32x16 (&o)[DT], bf16x8 (&pb)[4], const bf16x8 (&q)[KK], int kst,
                     int nvalid) {
-    if (__any(acc > kSlackSum)) {
+    if (__builtin_expect(__any(acc > kSlackSum), 0)) {
       f32x16 s[2];
 #pragma unroll
       for (int f = 0; f < 2 * KK; ++f) {
@@ -1087,6 +1090,18 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   static_assert(2 * KK == 16 && 4 * DT == 16 && DMA_PER_WAVE == 4, "the MFMA runs are laid out for d = 128");
   f32x16 sa0[2], sa1[2], sb0[2], sb1[2];
   bf16x8 pb0[4], pb1[4];
+  // the first tile's max of a half's S in scaled log2 units, from both lanes of each
+  // row (masked keys are -inf: with no valid key at all it stays kNoMax)
+  bool first_tile = true;
+  auto tile_max = [&](const f32x16 (&s)[2]) {
+    float m0 = fmaxf(s[0][0], s[1][0]), m1 = fmaxf(s[0][1], s[1][1]);
+#pragma unroll
+    for (int i = 2; i < 16; i += 2) {
+      m0 = fmaxf(m0, fmaxf(s[0][i], s[1][i]));
+      m1 = fmaxf(m1, fmaxf(s[0][i + 1], s[1][i + 1]));
+    }
+    return fmaxf(kNoMax, pair_max(fmaxf(m0, m1)) * c);
+  };
   float acc0 = 0.f, acc1 = 0.f;
   // the two halves' softmax streams (only a few elements of each are live at a time)
   float tq0[32], uq0[32], tq1[32], uq1[32];
@@ -1169,9 +1184,14 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       settle(ms1, l1, acc1, o1, pb1, q1, vst, prev_nvalid);
       acc0 = 0.f;
       acc1 = 0.f;
-      if (cur_nvalid < kTileKeys) {
+      if (__builtin_expect(cur_nvalid < kTileKeys, 0)) {
         mask_tail(sn0, cur_nvalid);
         mask_tail(sn1, cur_nvalid);
+      }
+      if (T == 0 && first_tile) {  // the first tile's exponentials use its own max
+        first_tile = false;
+        ms0 = tile_max(sn0);
+        ms1 = tile_max(sn1);
       }
       // ---- PV run.  Stream slot (g, half) of tile t rides on MFMA 2 g + half + 2,
       // past the last MFMA that reads the previous tile's P fragment it overwrites.

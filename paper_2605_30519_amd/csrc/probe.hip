@@ -14,20 +14,50 @@ namespace {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 
+// A counter-based hash (the 32-bit finaliser of MurmurHash3), for operand values.
+__device__ __forceinline__ uint32_t mix32(uint32_t x) {
+  x ^= x >> 16;
+  x *= 0x85ebca6bu;
+  x ^= x >> 13;
+  x *= 0xc2b2ae35u;
+  x ^= x >> 16;
+  return x;
+}
+
+// RANDOM = 0: one smooth per-lane operand pair shared by the four chains (few bits
+// toggle from one MFMA to the next).  RANDOM = 1: four pairs of random operands, one
+// per chain, roughly normal with unit-order values, so that consecutive MFMAs see
+// unrelated data, as attention's K, Q, P and V fragments do.  The MFMA power, and with
+// it the clock the chip holds, depends on how many operand bits toggle.
+template <int RANDOM>
 __global__ __launch_bounds__(512) void k_mfma_loop(int64_t iters, float* __restrict__ sink) {
-  // operands depend on the lane so that nothing folds; their values do not matter
-  const float x = 1.0f + 1e-3f * static_cast<float>(threadIdx.x % 64);
-  bf16x8 a, b;
-  for (int i = 0; i < 8; ++i) {
-    a[i] = static_cast<__bf16>(x * static_cast<float>(i + 1) * 1e-3f);
-    b[i] = static_cast<__bf16>(x * static_cast<float>(8 - i) * 1e-3f);
-  }
+  bf16x8 a[4], b[4];
+  const uint32_t t = threadIdx.x + 512u * blockIdx.x;
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      float va, vb;
+      if (RANDOM) {
+        // sums of two 16-bit uniforms, centred: triangular on (-1, 1)
+        const uint32_t h = mix32(t * 64u + s * 8u + i), g = mix32(h ^ 0x9e3779b9u);
+        va = static_cast<float>((h & 0xffffu) + (h >> 16)) * (1.0f / 65536.f) - 1.0f;
+        vb = static_cast<float>((g & 0xffffu) + (g >> 16)) * (1.0f / 65536.f) - 1.0f;
+      } else {
+        // depends on the lane so that nothing folds
+        const float x = 1.0f + 1e-3f * static_cast<float>(threadIdx.x % 64);
+        va = x * static_cast<float>(i + 1) * 1e-3f;
+        vb = x * static_cast<float>(8 - i) * 1e-3f;
+      }
+      a[s][i] = static_cast<__bf16>(va);
+      b[s][i] = static_cast<__bf16>(vb);
+    }
   f32x16 c0 = {}, c1 = {}, c2 = {}, c3 = {};
   for (int64_t it = 0; it < iters; ++it) {
-    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c0, 0, 0, 0);
-    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c1, 0, 0, 0);
-    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c2, 0, 0, 0);
-    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c3, 0, 0, 0);
+    c0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[0], b[0], c0, 0, 0, 0);
+    c1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[1], b[1], c1, 0, 0, 0);
+    c2 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[2], b[2], c2, 0, 0, 0);
+    c3 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[3], b[3], c3, 0, 0, 0);
   }
   float s = 0.f;
   for (int i = 0; i < 16; ++i) s += c0[i] + c1[i] + c2[i] + c3[i];
@@ -122,11 +152,15 @@ PROBE_API int32_t omnimem_probe_mfma_f32(int32_t shape, int64_t iters, int32_t w
   return status(launch_kernel(k_mfma_f32_loop<1>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
 }
 
-PROBE_API int32_t omnimem_probe_mfma_bf16(int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
-                                          void* stream) {
-  if (iters < 1 || workgroups < 1 || waves_per_simd < 1 || waves_per_simd > 2 || sink == nullptr) return -1;
-  return status(launch_kernel(k_mfma_loop, dim3(workgroups), dim3(256 * waves_per_simd), 0,
-                              static_cast<hipStream_t>(stream), iters, sink));
+PROBE_API int32_t omnimem_probe_mfma_bf16(int32_t operands, int64_t iters, int32_t workgroups, int32_t waves_per_simd,
+                                          float* sink, void* stream) {
+  if (operands < 0 || operands > 1 || iters < 1 || workgroups < 1 || waves_per_simd < 1 || waves_per_simd > 2 ||
+      sink == nullptr)
+    return -1;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (operands == 0)
+    return status(launch_kernel(k_mfma_loop<0>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
+  return status(launch_kernel(k_mfma_loop<1>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
 }
 
 PROBE_API int32_t omnimem_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {

@@ -246,16 +246,17 @@ def test_probe_argument_checks():
     runs without one)."""
     from paper_2605_30519_amd import _build
     P = ctypes.CDLL(_build.PROBE_LIB)
-    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int64, ctypes.c_int32, ctypes.c_int32, ctypes.c_void_p,
-                                          ctypes.c_void_p]
+    P.omnimem_probe_mfma_bf16.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
+                                          ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_mfma_f32.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p]
     P.omnimem_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p, ctypes.c_void_p]
     sink = ctypes.c_void_p(0x1000)
-    assert P.omnimem_probe_mfma_bf16(0, 1, 1, sink, None) == -1          # no iterations
-    assert P.omnimem_probe_mfma_bf16(1, 1, 3, sink, None) == -1          # three waves per SIMD
-    assert P.omnimem_probe_mfma_bf16(1, 1, 1, None, None) == -1          # no sink
+    assert P.omnimem_probe_mfma_bf16(0, 0, 1, 1, sink, None) == -1       # no iterations
+    assert P.omnimem_probe_mfma_bf16(1, 1, 1, 3, sink, None) == -1       # three waves per SIMD
+    assert P.omnimem_probe_mfma_bf16(0, 1, 1, 1, None, None) == -1       # no sink
+    assert P.omnimem_probe_mfma_bf16(2, 1, 1, 1, sink, None) == -1       # unknown operand kind
     assert P.omnimem_probe_mfma_f32(2, 1, 1, 1, sink, None) == -1        # unknown shape
     assert P.omnimem_probe_mfma_f32(0, 1, 0, 1, sink, None) == -1        # no workgroups
     assert P.omnimem_probe_mfma_f32(1, 1, 1, 1, None, None) == -1        # no sink
