@@ -145,8 +145,9 @@ def power_clock(dev, secs=6.0):
     """Socket power and GFX clock, read through torch.cuda (the SMI library) twice
     while each load runs back to back for `secs`: the attention kernel on the bench
     workload's first layer with its queries and with Q = 0 (all scores 0, so P is
-    constant and few MFMA operand bits toggle), and the MFMA issue loop of the probe
-    library with smooth and with random operands.  The chip holds its clock only
+    constant and few MFMA operand bits toggle), the MFMA issue loop of the probe
+    library with smooth and with random operands, and its softmax-slot loop with
+    operands in registers and from LDS.  The chip holds its clock only
     while its power stays within the limit, and MFMA power grows with the operand
     bits that toggle: this is what sets the clock at which the kernels run."""
     import ctypes
@@ -171,15 +172,25 @@ def power_clock(dev, secs=6.0):
     iters = 100000  # 256 workgroups of 4 waves: ~6 ms per launch
     mfma_fl = 256 * 4 * iters * 4 * 32768.0
 
+    P.omnimem_probe_softmax_slot.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                             ctypes.c_void_p]
+    slot_iters = 25000  # 8 slots per round: ~4 ms per launch
+    slot_fl = 256 * 4 * slot_iters * 8 * 32768.0
+
     def mfma(operands):
         assert P.omnimem_probe_mfma_bf16(operands, iters, 256, 1, ctypes.c_void_p(sink.data_ptr()), stream) == 0
+
+    def slot(lds):
+        assert P.omnimem_probe_softmax_slot(lds, slot_iters, 256, ctypes.c_void_p(sink.data_ptr()), stream) == 0
 
     loads = [("attention", lambda: omnimem_sparse_attn(cache, x.q, sel.idx, sel.cnt, w.group_size, w.scale,
                                                        out=out, lse=lse), fl, 1000),
              ("attention_q0", lambda: omnimem_sparse_attn(cache, q0, sel.idx, sel.cnt, w.group_size, w.scale,
                                                           out=out, lse=lse), fl, 1000),
              ("mfma_smooth", lambda: mfma(0), mfma_fl, 20),
-             ("mfma_random", lambda: mfma(1), mfma_fl, 20)]
+             ("mfma_random", lambda: mfma(1), mfma_fl, 20),
+             ("softmax_slot", lambda: slot(0), slot_fl, 20),
+             ("softmax_slot_lds", lambda: slot(1), slot_fl, 20)]
     res = {"workload": WORKLOAD, "seconds_per_load": secs}
     for name, call, flops, batch in loads:
         samples = []
@@ -1023,8 +1034,9 @@ def ramp_measure(dev, layers_n=30, warm_passes=20):
 
 def hip_probes(dev):
     """The HIP roofline probes of libomnimem_probe.so: MFMA issue loops (4
-    independent v_mfma_f32_32x32x16_bf16 chains per wave; the same with the fp32
-    16x16x4 and 32x32x2 MFMAs), a streaming read and a streaming copy of 1 GiB.  Best of a few launch shapes each; HIP events on the
+    independent v_mfma_f32_32x32x16_bf16 chains per wave, smooth or random operands;
+    the same with the fp32 16x16x4 and 32x32x2 MFMAs), the attention kernel's MFMA
+    slot with its softmax VALU work, a streaming read and a streaming copy of 1 GiB.  Best of a few launch shapes each; HIP events on the
     launch stream."""
     import ctypes
 
@@ -1036,6 +1048,8 @@ def hip_probes(dev):
                                           ctypes.c_void_p, ctypes.c_void_p]
     P.omnimem_probe_mfma_f32.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_int32,
                                          ctypes.c_void_p, ctypes.c_void_p]
+    P.omnimem_probe_softmax_slot.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                             ctypes.c_void_p]
     P.omnimem_probe_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32,
                                      ctypes.c_void_p]
     P.omnimem_probe_read.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
@@ -1067,6 +1081,12 @@ def hip_probes(dev):
         out[key + "_tflops"] = best
         # 2.5 PFLOP/s bf16 is 1024 flops per cycle per SIMD on 1024 SIMDs at 2.4 GHz
         out[key.replace("mfma_bf16", "mfma_implied_clock_ghz")] = round(best / PEAK_BF16_TFLOPS * 2.4, 3)
+    # the attention kernel's MFMA slot (MFMA + fma + exp + add + half a pack), operands in
+    # registers or the A operand from LDS; one wave per SIMD, 8 slots per round
+    for lds, key in ((0, "softmax_slot"), (1, "softmax_slot_lds")):
+        iters = 25000
+        ms = timed(lambda: P.omnimem_probe_softmax_slot(lds, iters, 256, ctypes.c_void_p(sink.data_ptr()), stream), 5)
+        out[key + "_tflops"] = round(256 * 4 * iters * 8 * 32768.0 / (ms * 1e-3) / 1e12, 1)
     # fp32 MFMA (the selection's score products): 16x16x4 and 32x32x2, against 157.3 TF
     f32 = []
     for shape, fl in ((0, 2048.0), (1, 4096.0)):
@@ -1133,6 +1153,7 @@ def probe_peaks(dev, result):
     sel = result["stages"]["select_roofline"]["achieved"]
     out["attention_frac_of_mfma_probe"] = round(att / out["hip"]["mfma_bf16_tflops"], 4)
     out["attention_frac_of_mfma_random_probe"] = round(att / out["hip"]["mfma_bf16_random_tflops"], 4)
+    out["attention_frac_of_softmax_slot_lds_probe"] = round(att / out["hip"]["softmax_slot_lds_tflops"], 4)
     out["attention_frac_of_gemm"] = round(att / out["bf16_gemm_tflops"], 4)
     out["select_frac_of_read_probe"] = round(sel / out["hip"]["hbm_read_gbs"], 4)
     return out

@@ -33,6 +33,16 @@ int32_t omnimem_probe_mfma_bf16(int32_t operands, int64_t iters, int32_t workgro
 int32_t omnimem_probe_mfma_f32(int32_t shape, int64_t iters, int32_t workgroups, int32_t waves_per_simd, float* sink,
                                void* stream);
 
+/* The attention kernel's MFMA slot in isolation: `workgroups` workgroups of 4 waves
+   (one per SIMD), each wave issuing `iters` rounds of 8 slots; a slot is one
+   v_mfma_f32_32x32x16_bf16 (32768 flops, four independent chains, random operands)
+   followed by the softmax VALU work of one score per lane (fma, exponential, add,
+   and a bf16 pack every other slot).  lds_operands: 0 = MFMA operands in registers,
+   1 = the A operand of each slot pair read from LDS two pairs ahead (1 KB per
+   fragment).  sink as above. */
+int32_t omnimem_probe_softmax_slot(int32_t lds_operands, int64_t iters, int32_t workgroups, float* sink,
+                                   void* stream);
+
 /* Streaming copy of `bytes` (a multiple of 16, 16-byte aligned buffers) from src
    to dst with 16-byte loads (nontemporal) and stores, grid-stride over `workgroups`
    workgroups of 256 threads. */

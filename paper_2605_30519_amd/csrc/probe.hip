@@ -64,6 +64,90 @@ __global__ __launch_bounds__(512) void k_mfma_loop(int64_t iters, float* __restr
   if (s == -1.2345e30f) sink[0] = s;
 }
 
+// The attention kernel's MFMA slot in isolation: each v_mfma_f32_32x32x16_bf16 (four
+// independent chains, random operands) is followed by the softmax VALU work of one
+// score per lane: an fma (c s - max), an exponential, a row-sum add, and on every
+// other slot a bf16 pack; no op reads a result of its own slot.  LDS = 1: the MFMAs
+// of each slot pair take their A operand from a 1 KB LDS fragment read two pairs
+// ahead, as the attention kernel's K fragments are.  One wave per SIMD.
+template <int LDS>
+__global__ __launch_bounds__(256) void k_slot_loop(int64_t iters, float* __restrict__ sink) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef __attribute__((address_space(3))) const bf16x8 lds_bf16x8;
+  __shared__ __attribute__((aligned(1024))) uint4 frags[LDS ? 64 * 64 : 1];
+  const uint32_t t = threadIdx.x + 256u * blockIdx.x;
+  auto rnd = [](uint32_t h) {  // triangular on (-1, 1)
+    return static_cast<float>((h & 0xffffu) + (h >> 16)) * (1.0f / 65536.f) - 1.0f;
+  };
+  bf16x8 a[4], b[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t h = mix32(t * 64u + q * 8u + i), g = mix32(h ^ 0x9e3779b9u);
+      a[q][i] = static_cast<__bf16>(rnd(h));
+      b[q][i] = static_cast<__bf16>(rnd(g));
+    }
+  if constexpr (LDS) {
+    for (int i = threadIdx.x; i < 64 * 64; i += 256) {
+      bf16x8 v;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = static_cast<__bf16>(rnd(mix32(i * 8u + e)));
+      frags[i] = __builtin_bit_cast(uint4, v);
+    }
+    __syncthreads();
+  }
+  const uint32_t base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(frags)) + (threadIdx.x % 64) * 16;
+  auto frag = [&](int64_t f) {  // fragment f mod 64: 64 lanes x 16 bytes
+    return *reinterpret_cast<lds_bf16x8*>(static_cast<uintptr_t>(base + static_cast<uint32_t>(f % 64) * 1024));
+  };
+  f32x16 c[4] = {};
+  float x[8], y[8], acc = 0.f;
+  const float cs = 0.125f, ms = 0.5f;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    x[i] = rnd(mix32(t ^ (i * 0x3c6ef372u)));
+    y[i] = 0.f;
+  }
+  bf16x2 pk = {};
+  bf16x8 kf[4];
+  if constexpr (LDS) {
+    kf[0] = frag(0);
+    kf[1] = frag(1);
+  }
+  for (int64_t it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int sl = 0; sl < 8; ++sl) {
+      const int pr = sl / 2;
+      if constexpr (LDS) {
+        c[sl % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[pr], b[sl % 4], c[sl % 4], 0, 0, 0);
+        if (sl % 2 == 0) kf[(pr + 2) % 4] = frag(4 * it + pr + 2);
+      } else {
+        c[sl % 4] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[sl % 4], b[sl % 4], c[sl % 4], 0, 0, 0);
+      }
+      x[sl] = fmaf(x[sl], cs, -ms);
+      asm volatile("" : "+v"(x[sl]));
+      y[sl] = __builtin_amdgcn_exp2f(x[(sl + 7) % 8]);
+      asm volatile("" : "+v"(y[sl]));
+      acc += y[(sl + 6) % 8];
+      asm volatile("" : "+v"(acc));
+      if (sl % 2 == 1) {
+        pk = bf16x2{static_cast<__bf16>(y[(sl + 5) % 8]), static_cast<__bf16>(y[(sl + 4) % 8])};
+        asm volatile("" : "+v"(pk));
+      }
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  float s = acc + static_cast<float>(pk[0]);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) s += c[q][i];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) s += x[i] + y[i];
+  if (s == -1.2345e30f) sink[0] = s;
+}
+
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 // fp32 MFMA issue loop: SHAPE 0 = v_mfma_f32_16x16x4_f32 (2048 flops), 1 =
@@ -161,6 +245,15 @@ PROBE_API int32_t omnimem_probe_mfma_bf16(int32_t operands, int64_t iters, int32
   if (operands == 0)
     return status(launch_kernel(k_mfma_loop<0>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
   return status(launch_kernel(k_mfma_loop<1>, dim3(workgroups), dim3(256 * waves_per_simd), 0, st, iters, sink));
+}
+
+PROBE_API int32_t omnimem_probe_softmax_slot(int32_t lds_operands, int64_t iters, int32_t workgroups, float* sink,
+                                             void* stream) {
+  if (lds_operands < 0 || lds_operands > 1 || iters < 1 || workgroups < 1 || sink == nullptr) return -1;
+  const hipStream_t st = static_cast<hipStream_t>(stream);
+  if (lds_operands == 0)
+    return status(launch_kernel(k_slot_loop<0>, dim3(workgroups), dim3(256), 0, st, iters, sink));
+  return status(launch_kernel(k_slot_loop<1>, dim3(workgroups), dim3(256), 0, st, iters, sink));
 }
 
 PROBE_API int32_t omnimem_probe_copy(const void* src, void* dst, int64_t bytes, int32_t workgroups, void* stream) {

@@ -257,6 +257,12 @@ def test_probe_argument_checks():
     assert P.omnimem_probe_mfma_bf16(1, 1, 1, 3, sink, None) == -1       # three waves per SIMD
     assert P.omnimem_probe_mfma_bf16(0, 1, 1, 1, None, None) == -1       # no sink
     assert P.omnimem_probe_mfma_bf16(2, 1, 1, 1, sink, None) == -1       # unknown operand kind
+    P.omnimem_probe_softmax_slot.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                             ctypes.c_void_p]
+    assert P.omnimem_probe_softmax_slot(2, 1, 1, sink, None) == -1       # unknown operand source
+    assert P.omnimem_probe_softmax_slot(0, 0, 1, sink, None) == -1       # no iterations
+    assert P.omnimem_probe_softmax_slot(1, 1, 0, sink, None) == -1       # no workgroups
+    assert P.omnimem_probe_softmax_slot(0, 1, 1, None, None) == -1       # no sink
     assert P.omnimem_probe_mfma_f32(2, 1, 1, 1, sink, None) == -1        # unknown shape
     assert P.omnimem_probe_mfma_f32(0, 1, 0, 1, sink, None) == -1        # no workgroups
     assert P.omnimem_probe_mfma_f32(1, 1, 1, 1, None, None) == -1        # no sink
