@@ -994,7 +994,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   };
   const int krow = s_row_perm(lane % 32);
   typedef __attribute__((address_space(3))) i16x4 lds_i16x4;
-  // Operand fragments, read from LDS two fragments ahead of the MFMAs that use them.
+  // Operand fragments, read from LDS ahead of the MFMAs that use them: K fragments four
+  // ahead, V fragments three (four would take the PV run past 256 VGPRs).
   // The lane's part of each address is fixed for the whole loop (8 K and 4 V byte
   // offsets, the chunk permutations depending only on the lane); the stage, the key
   // group and the ring base are compile-time constants that fold into the reads'
@@ -1152,6 +1153,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
     if (wave_live) {
       kf[0] = k_frag(kst, 0);
       kf[1] = k_frag(kst, 1);
+      kf[2] = k_frag(kst, 2);
+      kf[3] = k_frag(kst, 3);
     }
     const int2 t2 = scalar_tile(next_tile_raw());  // every thread; refills the table at its end
     const int cur_nvalid = cur.y & 255;
@@ -1163,7 +1166,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         if (i % 2 == 0) {
           sn0[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q0[f % KK], f % KK ? sn0[f / KK] : f32x16{}, 0, 0, 0);
           soft_slot(so0, ms0, acc0, pb0, tq0, uq0, 15 + f);
-          if (f + 2 < 2 * KK) kf[f + 2] = k_frag(kst, f + 2);
+          if (f + 4 < 2 * KK) kf[f + 4] = k_frag(kst, f + 4);
         } else {
           sn1[f / KK] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[f], q1[f % KK], f % KK ? sn1[f / KK] : f32x16{}, 0, 0, 0);
           soft_slot(so1, ms1, acc1, pb1, tq1, uq1, 15 + f);
@@ -1180,6 +1183,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       keep_here(pb1, acc1);
       vf[0] = v_frag(vst, 0);
       vf[1] = v_frag(vst, 1);
+      vf[2] = v_frag(vst, 2);
       settle(ms0, l0, acc0, o0, pb0, q0, vst, prev_nvalid);
       settle(ms1, l1, acc1, o1, pb1, q1, vst, prev_nvalid);
       acc0 = 0.f;
@@ -1206,7 +1210,7 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
         const bf16x8 op_a = vf[f], op_b = i % 2 ? pb1[f / DT] : pb0[f / DT];
         if (i % 2 == 0) {
           pv_mfma(o0[f % DT], op_a, op_b);
-          if (f + 2 < 4 * DT) vf[f + 2] = v_frag(vst, f + 2);
+          if (f + 3 < 4 * DT) vf[f + 3] = v_frag(vst, f + 3);
         } else {
           pv_mfma(o1[f % DT], op_a, op_b);
         }

@@ -69,7 +69,7 @@ __global__ __launch_bounds__(512) void k_mfma_loop(int64_t iters, float* __restr
 // score per lane: an fma (c s - max), an exponential, a row-sum add, and on every
 // other slot a bf16 pack; no op reads a result of its own slot.  LDS = 1: the MFMAs
 // of each slot pair take their A operand from a 1 KB LDS fragment read two pairs
-// ahead, as the attention kernel's K fragments are.  One wave per SIMD.
+// ahead, like the attention kernel's K fragments.  One wave per SIMD.
 template <int LDS>
 __global__ __launch_bounds__(256) void k_slot_loop(int64_t iters, float* __restrict__ sink) {
   typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
