@@ -37,6 +37,28 @@ FLAGS = [
 # ever produced or consumed on purpose there).
 EXTRA_FLAGS = {"attention.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form", "-fno-honor-nans", "-mno-amdgpu-ieee"]}
 
+# Kernels that must keep every value in registers.  The 64-row attention kernel
+# issues its P.V MFMAs from inline asm with O in fixed accumulation registers, and its
+# hazard waits assume that nothing else touches those registers while an MFMA runs; a
+# spill or a private array moved to scratch memory would add such accesses (and be
+# slow).  The build fails if the compiler reports scratch use for them.
+NO_SCRATCH = {"attention.hip": ("k_attn_bf16_r64",)}
+RESOURCE_REMARK = "-Rpass-analysis=kernel-resource-usage"
+
+
+def scratch_users(remarks: str, kernels) -> list:
+    """Kernels among `kernels` (name fragments) whose resource remarks report a
+    nonzero scratch size or spilled VGPRs."""
+    bad, name = [], None
+    for line in remarks.splitlines():
+        if "Function Name:" in line:
+            name = line.split("Function Name:")[1].split()[0]
+        elif name and any(k in name for k in kernels):
+            for key in ("ScratchSize [bytes/lane]:", "VGPRs Spill:"):
+                if key in line and int(line.split(key)[1].split()[0]) != 0:
+                    bad.append(f"{name}: {key} {line.split(key)[1].split()[0]}")
+    return bad
+
 
 def build(verbose: bool = False) -> str:
     """Compile every source (in parallel) and link libomnimem.so.  Always rebuilds."""
@@ -44,7 +66,8 @@ def build(verbose: bool = False) -> str:
     procs = []
     for src in SOURCES:
         obj = os.path.join(OBJ_DIR, src.replace(".hip", ".o"))
-        cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
+        remark = [RESOURCE_REMARK] if src in NO_SCRATCH else []
+        cmd = [HIPCC, *FLAGS, *EXTRA_FLAGS.get(src, []), *remark, "-c", os.path.join(CSRC, src), "-o", obj]
         procs.append((src, obj, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT, text=True)))
     for src in HOST_SOURCES:
         obj = os.path.join(OBJ_DIR, src.replace(".cpp", ".host.o"))
@@ -54,7 +77,12 @@ def build(verbose: bool = False) -> str:
     errors = []
     for src, obj, p in procs:
         out, _ = p.communicate()
-        out = "\n".join(line for line in out.splitlines() if "packed-fp32-ops" not in line)
+        if p.returncode == 0 and src in NO_SCRATCH:
+            bad = scratch_users(out, NO_SCRATCH[src])
+            if bad:
+                errors.append(f"{src}: kernels that must not use scratch memory do:\n" + "\n".join(bad))
+        out = "\n".join(line for line in out.splitlines()
+                        if "packed-fp32-ops" not in line and "kernel-resource-usage" not in line)
         if p.returncode != 0:
             errors.append(f"{src}:\n{out}")
         elif verbose and out.strip():

@@ -272,3 +272,26 @@ def test_probe_argument_checks():
     assert P.omnimem_probe_copy(ctypes.c_void_p(0x10008), buf, 64, 1, None) == -1  # misaligned
     assert P.omnimem_probe_read(buf, 64, 0, sink, None) == -1            # no workgroups
     assert P.omnimem_probe_read(buf, 64, 1, None, None) == -1            # no sink
+
+
+def test_scratch_guard_reads_resource_remarks():
+    """The build's check that the 64-row attention kernel keeps everything in
+    registers: it reads the compiler's per-kernel resource remarks and names a
+    listed kernel that reports scratch memory or spilled VGPRs (canned remarks in
+    the compiler's format, so this runs without compiling)."""
+    from paper_2605_30519_amd import _build
+
+    def remarks(name, scratch, spill):
+        pre = "attention.hip:836:1: remark: "
+        return "\n".join([f"{pre}Function Name: {name} [-Rpass-analysis=kernel-resource-usage]",
+                          f"{pre}    VGPRs: 256 [-Rpass-analysis=kernel-resource-usage]",
+                          f"{pre}    ScratchSize [bytes/lane]: {scratch} [-Rpass-analysis=kernel-resource-usage]",
+                          f"{pre}    VGPRs Spill: {spill} [-Rpass-analysis=kernel-resource-usage]"])
+    r64 = "_ZN7omnimem12_GLOBAL__N_115k_attn_bf16_r64ILi128EEEvNS0_8AttnArgsE"
+    other = "_ZN7omnimem12_GLOBAL__N_110k_attn_f32ILi64EEEvNS0_8AttnArgsE"
+    kernels = _build.NO_SCRATCH["attention.hip"]
+    assert _build.scratch_users(remarks(r64, 0, 0) + "\n" + remarks(other, 64, 3), kernels) == []
+    bad = _build.scratch_users(remarks(other, 0, 0) + "\n" + remarks(r64, 1088, 0), kernels)
+    assert bad == [f"{r64}: ScratchSize [bytes/lane]: 1088"]
+    bad = _build.scratch_users(remarks(r64, 0, 5), kernels)
+    assert bad == [f"{r64}: VGPRs Spill: 5"]
