@@ -254,6 +254,13 @@ const char* omnimem_status_string(int32_t status);
  *               num_pages >= ceil(capacity_chunks*Bpc / 64).
  *   page_table  [num_pages] int32: entry p = p, written by omnimem_compress_chunk
  *               for every page its chunk touches.
+ *   k_lo        optional (NULL: absent), bf16 caches only: [num_pages][H][64][d] bf16,
+ *               the rounding residual of the pooled keys, bf16(k_mean - k_pages), in
+ *               k_pages' layout; written by omnimem_compress_chunk when present.  With
+ *               it, the probability-averaged scores of omnimem_select_compressed read
+ *               the fp32 pooled keys as the two bf16 pieces k_pages + k_lo instead of
+ *               splitting k_mean on every call (the results are the same bit for bit).
+ *               Every chunk must then have been pooled with k_lo present.
  * The caller allocates and owns every buffer (16-byte aligned; page_table 4-byte).
  * Geometry (dtype, H, d, B, S) must equal the full cache's.
  */
@@ -267,7 +274,8 @@ typedef struct {
   void* k_pages;
   void* v_pages;
   int32_t* page_table;
-  int64_t num_pages;            /* pages of k_pages / v_pages */
+  int64_t num_pages;            /* pages of k_pages / v_pages (and k_lo) */
+  void* k_lo;                   /* optional residual of the pooled keys (bf16 caches) */
 } omnimem_cmp_cache_t;
 
 /*

@@ -44,9 +44,12 @@ struct LaunchStatus {
 
 // Probability-averaged score keys (score_mode 1) from pooled keys kbar
 // [H][kbar_stride][D] fp32: order-preserving keys [H][R][nbp], 0 outside Omega.
+// hi_pages / lo_pages: the compressed cache's bf16 pooled keys and their residual
+// ([pages][H][64][D] each), or both null: the pieces are then split from kbar into
+// ksplit first.
 hipError_t launch_prob_keys(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                            int64_t kbar_stride, float* part, void* ksplit, uint32_t* keys, int nbp,
-                            hipStream_t stream);
+                            int64_t kbar_stride, float* part, void* ksplit, const void* hi_pages,
+                            const void* lo_pages, uint32_t* keys, int nbp, hipStream_t stream);
 
 hipError_t launch_select(const CacheGeom& g, const SelectPlan& p, const void* q, int32_t* idx, int32_t* cnt,
                          float* score, void* workspace, hipStream_t stream);

@@ -57,6 +57,7 @@ struct CmpCache {
   int32_t* page_table;   // [num_pages], entry p = p
   int64_t num_pages;
   int cap_blocks;        // capacity in pooled tokens
+  void* k_lo;            // optional [num_pages][H][64][D] bf16 residual of the pooled keys
 };
 constexpr int kCmpPageTokens = 64;
 

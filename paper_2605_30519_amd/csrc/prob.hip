@@ -5,9 +5,12 @@
 // with LSE_i the log-sum-exp of row i over all pooled keys, so that sbar is the
 // group mean of the compression branch's attention weights.
 //
-// k_split_keys: the fp32 pooled keys, split once per call into two bf16 pieces
-// (kbar ~= hi + lo, exact to about 2^-17 relative), stored tile by tile (64 keys,
-// hi then lo) so that a workgroup stages a tile with plain coalesced 16-byte loads.
+// The fp32 pooled keys enter the MFMAs as two bf16 pieces (kbar ~= hi + lo, exact to
+// about 2^-17 relative, both rounded to nearest even).  With a bf16 compressed cache
+// that keeps the residual, the pieces are its pooled-key pages and residual pages,
+// written once per chunk when the chunk is pooled; otherwise k_split_keys splits the
+// fp32 pooled keys once per call, tile by tile (64 keys, hi then lo).  Either way a
+// workgroup stages a tile with plain coalesced 16-byte loads.
 // k_prob_partial: one workgroup per (head, slice of at most 128 query rows), the
 // slices of one head contiguous on one XCD so that its L2 holds that head's keys.
 // Each wave owns 64 rows (two 32-row MFMA tiles that share every key fragment) and
@@ -36,6 +39,7 @@ constexpr int kPThreads = 256;
 constexpr int kPRows = kProbSliceRows;  // query rows per slice: 64 per wave, two waves deep
 static_assert(kPRows == 128, "the wave layout assumes 128-row slices");
 constexpr int kPKeys = 64;    // pooled keys per tile: 32 per wave, two waves wide
+static_assert(kPKeys == kCmpPageTokens, "a key tile is one page of the compressed cache");
 constexpr int kPRedStride = kPKeys + 1;
 constexpr float kLog2eP = 1.4426950408889634f;
 
@@ -53,7 +57,10 @@ struct QueryPieces<float> {
 struct ProbArgs {
   const void* q;
   int lq, H, G, R;
-  const uint4* ksplit;  // [H][ntiles][2][64][D] bf16 pieces of the pooled keys
+  // bf16 pieces of the pooled keys, 64-key tiles of [64][D]: piece p of tile t of
+  // head h starts at piece[p] + t * tile_stride + h * head_stride (16-byte units)
+  const uint4* piece[2];
+  int64_t tile_stride, head_stride;
   int ntiles, nb;
   float scale;
   int multi;            // 1: a slice holds gps whole groups; 0: a slice is part of one group
@@ -131,10 +138,14 @@ __global__ __launch_bounds__(kPThreads) void k_split_keys(const float* __restric
 // columns.
 template <int D>
 __device__ __forceinline__ void fetch_tile(const ProbArgs& a, int h, int t, u32x4 (&kv)[2 * kPKeys * D / 8 / kPThreads]) {
-  constexpr int TILE_CHUNKS = 2 * kPKeys * D / 8;
-  const u32x4* src = reinterpret_cast<const u32x4*>(a.ksplit) + (static_cast<int64_t>(h) * a.ntiles + t) * TILE_CHUNKS;
+  constexpr int PIECE_CHUNKS = kPKeys * D / 8;
+  static_assert(PIECE_CHUNKS % kPThreads == 0, "a thread's chunks of a tile lie in one piece each");
+  const int64_t off = t * a.tile_stride + h * a.head_stride;
 #pragma unroll
-  for (int u = 0; u < TILE_CHUNKS / kPThreads; ++u) kv[u] = src[threadIdx.x + u * kPThreads];
+  for (int u = 0; u < 2 * PIECE_CHUNKS / kPThreads; ++u) {
+    const int e = threadIdx.x + u * kPThreads, piece = e / PIECE_CHUNKS;  // piece: compile-time per u
+    kv[u] = reinterpret_cast<const u32x4*>(a.piece[piece])[off + e % PIECE_CHUNKS];
+  }
 }
 
 template <int D>
@@ -410,18 +421,30 @@ __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restric
 
 template <typename T, int D>
 hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                             int64_t kbar_stride, float* part, uint4* ksplit, uint32_t* keys, int nbp,
-                             hipStream_t stream) {
+                             int64_t kbar_stride, float* part, uint4* ksplit, const uint4* hi_pages,
+                             const uint4* lo_pages, uint32_t* keys, int nbp, hipStream_t stream) {
   const int ntiles = (g.nb + kPKeys - 1) / kPKeys;
+  constexpr int64_t PIECE_CHUNKS = kPKeys * D / 8;
   LaunchStatus st;
-  st(k_split_keys<D>, dim3(ntiles, g.H), dim3(kPThreads), 0, stream, kbar, kbar_stride, g.nb, ntiles, ksplit);
   ProbArgs a;
+  if (hi_pages != nullptr && lo_pages != nullptr) {
+    // the compressed cache's pages: tile t of head h is page t's slab of head h
+    a.piece[0] = hi_pages;
+    a.piece[1] = lo_pages;
+    a.tile_stride = static_cast<int64_t>(g.H) * PIECE_CHUNKS;
+    a.head_stride = PIECE_CHUNKS;
+  } else {
+    st(k_split_keys<D>, dim3(ntiles, g.H), dim3(kPThreads), 0, stream, kbar, kbar_stride, g.nb, ntiles, ksplit);
+    a.piece[0] = ksplit;
+    a.piece[1] = ksplit + PIECE_CHUNKS;
+    a.tile_stride = 2 * PIECE_CHUNKS;
+    a.head_stride = ntiles * 2 * PIECE_CHUNKS;
+  }
   a.q = q;
   a.lq = p.lq;
   a.H = g.H;
   a.G = p.G;
   a.R = p.R;
-  a.ksplit = ksplit;
   a.ntiles = ntiles;
   a.nb = g.nb;
   a.scale = p.scale;
@@ -452,15 +475,20 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
 }  // namespace
 
 hipError_t launch_prob_keys(const CacheGeom& g, const SelectPlan& p, const void* q, const float* kbar,
-                            int64_t kbar_stride, float* part, void* ksplit, uint32_t* keys, int nbp,
-                            hipStream_t stream) {
+                            int64_t kbar_stride, float* part, void* ksplit, const void* hi_pages,
+                            const void* lo_pages, uint32_t* keys, int nbp, hipStream_t stream) {
   uint4* ks = static_cast<uint4*>(ksplit);
+  const uint4* hi = static_cast<const uint4*>(hi_pages);
+  const uint4* lo = static_cast<const uint4*>(lo_pages);
   if (g.dtype == 0) {
-    if (g.D == 128) return launch_prob_typed<uint16_t, 128>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
-    return launch_prob_typed<uint16_t, 64>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
+    if (g.D == 128)
+      return launch_prob_typed<uint16_t, 128>(g, p, q, kbar, kbar_stride, part, ks, hi, lo, keys, nbp, stream);
+    return launch_prob_typed<uint16_t, 64>(g, p, q, kbar, kbar_stride, part, ks, hi, lo, keys, nbp, stream);
   }
-  if (g.D == 128) return launch_prob_typed<float, 128>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
-  return launch_prob_typed<float, 64>(g, p, q, kbar, kbar_stride, part, ks, keys, nbp, stream);
+  // fp32 caches: the pooled keys in k_pages are fp32, so the pieces are always split
+  if (g.D == 128)
+    return launch_prob_typed<float, 128>(g, p, q, kbar, kbar_stride, part, ks, nullptr, nullptr, keys, nbp, stream);
+  return launch_prob_typed<float, 64>(g, p, q, kbar, kbar_stride, part, ks, nullptr, nullptr, keys, nbp, stream);
 }
 
 }  // namespace omnimem

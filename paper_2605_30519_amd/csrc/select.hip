@@ -20,6 +20,8 @@
 #include <float.h>
 #include <math.h>
 
+#include <type_traits>
+
 #include "device_common.h"
 #include "launch.h"
 
@@ -469,6 +471,7 @@ struct CompressArgs {
   float* k_mean;
   void* ck_pages;
   void* cv_pages;
+  void* ck_lo;  // optional: bf16 residual of the pooled keys (bf16 caches)
   int32_t* c_page_table;
   int cap_blocks;
 };
@@ -489,6 +492,19 @@ __device__ __forceinline__ void store_rounded<uint16_t>(uint16_t* dst, const flo
 template <>
 __device__ __forceinline__ void store_rounded<float>(float* dst, const float (&x)[4]) {
   *reinterpret_cast<float4*>(dst) = make_float4(x[0], x[1], x[2], x[3]);
+}
+
+// The residual of 8 fp32 values after their rounding to bf16, itself rounded to bf16
+// (both to nearest even): x ~= hi + lo to about 2^-17 relative.
+__device__ __forceinline__ void store_residual_bf16(uint16_t* dst, const float (&x)[8]) {
+  uint32_t w[4];
+#pragma unroll
+  for (int j = 0; j < 8; j += 2) {
+    const float r0 = x[j] - __uint_as_float(static_cast<uint32_t>(f32_to_bf16_rne(x[j])) << 16);
+    const float r1 = x[j + 1] - __uint_as_float(static_cast<uint32_t>(f32_to_bf16_rne(x[j + 1])) << 16);
+    w[j / 2] = f32_to_bf16_rne(r0) | (static_cast<uint32_t>(f32_to_bf16_rne(r1)) << 16);
+  }
+  *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
 }
 
 template <typename T, int D, int B>
@@ -528,6 +544,8 @@ __global__ __launch_bounds__(kThreads) void k_compress_chunk(CompressArgs a) {
     const int64_t at = ((cp * a.H + h) * kCmpPageTokens + slot) * D + c * VEC;
     store_rounded<T>(static_cast<T*>(a.ck_pages) + at, ks);
     store_rounded<T>(static_cast<T*>(a.cv_pages) + at, vs);
+    if constexpr (std::is_same_v<T, uint16_t>)
+      if (a.ck_lo != nullptr) store_residual_bf16(static_cast<uint16_t*>(a.ck_lo) + at, ks);
     if (lane == 0 && h == 0 && (slot == 0 || o == 0)) a.c_page_table[cp] = static_cast<int32_t>(cp);
   }
 }
@@ -1335,6 +1353,7 @@ hipError_t launch_compress_typed(const CacheGeom& g, const CmpCache& cc, int chu
   a.k_mean = cc.k_mean;
   a.ck_pages = cc.k_pages;
   a.cv_pages = cc.v_pages;
+  a.ck_lo = cc.k_lo;
   a.c_page_table = cc.page_table;
   a.cap_blocks = cc.cap_blocks;
   const dim3 grid((g.Bpc + kThreads / kWave - 1) / (kThreads / kWave), g.H);
@@ -1354,7 +1373,8 @@ hipError_t launch_select_compressed_typed(const CacheGeom& g, const CmpCache& cc
     if (g.nb > 0) {
       float* part = reinterpret_cast<float*>(ws + p.off_part);
       const hipError_t e = launch_prob_keys(g, p, q, cc.k_mean, static_cast<int64_t>(cc.cap_blocks), part,
-                                            ws + p.off_ksplit, keys, nbp, stream);
+                                            ws + p.off_ksplit, cc.k_lo != nullptr ? cc.k_pages : nullptr, cc.k_lo,
+                                            keys, nbp, stream);
       if (e != hipSuccess) return e;
     }
     return launch_topk(g, p, keys, nbp, idx, cnt, score, stream);

@@ -54,6 +54,9 @@ omnimem_status_t resolve_cmp(const omnimem_cmp_cache_t* cc, const CacheGeom& g, 
     return OMNIMEM_EINVAL;
   if (!aligned16(cc->k_mean) || !aligned16(cc->k_pages) || !aligned16(cc->v_pages) || !aligned4(cc->page_table))
     return OMNIMEM_EINVAL;
+  // the pooled keys' residual piece exists for bf16 caches only
+  if (cc->k_lo != nullptr && (g.dtype != 0 || !aligned16(cc->k_lo))) return OMNIMEM_EINVAL;
+  c.k_lo = cc->k_lo;
   c.k_mean = cc->k_mean;
   c.k_pages = cc->k_pages;
   c.v_pages = cc->v_pages;

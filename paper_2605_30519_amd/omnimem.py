@@ -86,6 +86,7 @@ class omnimem_cmp_cache_t(ctypes.Structure):
         ("v_pages", ctypes.c_void_p),
         ("page_table", ctypes.c_void_p),
         ("num_pages", ctypes.c_int64),
+        ("k_lo", ctypes.c_void_p),
     ]
 
 
@@ -544,7 +545,9 @@ CMP_PAGE_TOKENS = 64
 @dataclass
 class CompressedCache:
     """One layer's compressed history (device tensors): k_mean [H, cap*Bpc, d] fp32,
-    k_pages / v_pages [pages, H, 64, d] in the full cache's dtype, page_table [pages]."""
+    k_pages / v_pages [pages, H, 64, d] in the full cache's dtype, page_table [pages],
+    and for bf16 caches optionally k_lo [pages, H, 64, d] bf16, the pooled keys'
+    rounding residual (the probability-averaged scores then skip splitting k_mean)."""
     k_mean: torch.Tensor
     k_pages: torch.Tensor
     v_pages: torch.Tensor
@@ -552,17 +555,21 @@ class CompressedCache:
     block_size: int
     chunk_tokens: int
     capacity_chunks: int
+    k_lo: Optional[torch.Tensor] = None
 
     @classmethod
     def allocate(cls, cache: PagedKVCache, capacity_chunks: int) -> "CompressedCache":
         H, d, dev = cache.num_heads, cache.head_dim, cache.k_pages.device
         tokens = capacity_chunks * cache.blocks_per_chunk
         pages = max(1, -(-tokens // CMP_PAGE_TOKENS))
+        k_lo = None
+        if cache.dtype == torch.bfloat16:
+            k_lo = torch.zeros((pages, H, CMP_PAGE_TOKENS, d), dtype=torch.bfloat16, device=dev)
         return cls(torch.zeros((H, max(tokens, 1), d), dtype=torch.float32, device=dev),
                    torch.zeros((pages, H, CMP_PAGE_TOKENS, d), dtype=cache.dtype, device=dev),
                    torch.zeros((pages, H, CMP_PAGE_TOKENS, d), dtype=cache.dtype, device=dev),
                    torch.zeros(pages, dtype=torch.int32, device=dev),
-                   cache.block_size, cache.chunk_tokens, int(capacity_chunks))
+                   cache.block_size, cache.chunk_tokens, int(capacity_chunks), k_lo)
 
     def check_against(self, cache: PagedKVCache):
         """The pooled tensors must match the full cache's heads, dim, dtype and GPU."""
@@ -579,14 +586,18 @@ class CompressedCache:
             _check_tensor(name, t, (int(t.shape[0]), H, CMP_PAGE_TOKENS, d), cache.dtype)
             _need(int(t.shape[0]) >= pages, f"{name} holds fewer pages than the capacity needs")
         _check_tensor("cmp page_table", self.page_table, (int(self.page_table.shape[0]),), torch.int32)
+        if self.k_lo is not None:
+            _need(cache.dtype == torch.bfloat16, "k_lo exists for bf16 caches only")
+            _check_tensor("cmp k_lo", self.k_lo, tuple(int(x) for x in self.k_pages.shape), torch.bfloat16)
         _on_gpu(cache.k_pages, k_mean=self.k_mean, cmp_k_pages=self.k_pages, cmp_v_pages=self.v_pages,
-                cmp_page_table=self.page_table)
+                cmp_page_table=self.page_table, cmp_k_lo=self.k_lo)
 
     def descriptor(self) -> omnimem_cmp_cache_t:
         return omnimem_cmp_cache_t(
             _DTYPES[self.k_pages.dtype], int(self.k_pages.shape[1]), int(self.k_pages.shape[3]), self.block_size,
             self.chunk_tokens, self.capacity_chunks, self.k_mean.data_ptr(), self.k_pages.data_ptr(),
-            self.v_pages.data_ptr(), self.page_table.data_ptr(), int(self.k_pages.shape[0]))
+            self.v_pages.data_ptr(), self.page_table.data_ptr(), int(self.k_pages.shape[0]),
+            self.k_lo.data_ptr() if self.k_lo is not None else None)
 
 
 def omnimem_compress_chunk(cache: PagedKVCache, chunk: int, cc: CompressedCache, *,

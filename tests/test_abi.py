@@ -146,6 +146,39 @@ def test_select_validation():
     assert st == 0 and awe.value == 1
 
 
+def cmp_cache(**kw):
+    d = dict(dtype=0, num_heads=2, head_dim=64, block_size=64, chunk_tokens=256, capacity_chunks=3,
+             k_mean=FAKE, k_pages=FAKE, v_pages=FAKE, page_table=FAKE, num_pages=1, k_lo=None)
+    d.update(kw)
+    return om.omnimem_cmp_cache_t(**d)
+
+
+def test_compressed_cache_validation():
+    """The compressed cache's checks, k_lo (the pooled keys' residual pages) included:
+    it may be absent, exists for bf16 caches only and must be 16-byte aligned."""
+    L = abi()
+
+    def compress(cc, kv=None):
+        kv = kv or cache()
+        return L.omnimem_compress_chunk(ctypes.byref(kv), 0, ctypes.byref(cc), None)
+
+    def select(cc, kv=None):
+        kv = kv or cache()
+        p = params(score_mode=1)
+        return L.omnimem_select_compressed(ctypes.byref(kv), ctypes.byref(cc), FAKE, 256, ctypes.byref(p), FAKE,
+                                           FAKE, None, None, FAKE, 1 << 20, None)
+
+    assert select(cmp_cache(capacity_chunks=2)) == EINVAL        # fewer chunks than the history
+    assert compress(cmp_cache(capacity_chunks=0)) == EINVAL      # chunk 0 beyond the capacity
+    for call in (compress, select):
+        # every case is refused before anything is launched (the pointers are fake)
+        assert call(cmp_cache(num_heads=3)) == EINVAL            # geometry differs from the full cache
+        assert call(cmp_cache(num_pages=0)) == EINVAL            # 12 pooled tokens need one page
+        assert call(cmp_cache(k_mean=FAKE + 4)) == EINVAL
+        assert call(cmp_cache(k_lo=FAKE + 8)) == EINVAL          # misaligned residual pages
+        assert call(cmp_cache(dtype=1, k_lo=FAKE), cache(dtype=1)) == EINVAL  # fp32 caches keep no residual
+
+
 def test_attention_validation():
     L = abi()
     c = cache()

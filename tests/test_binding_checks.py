@@ -90,6 +90,14 @@ def test_compressed_and_fusion_checks():
     refused("k_mean holds fewer pooled tokens", om.omnimem_select_compressed, c, bad, q(), K, G, 1, 0)
     bad = om.CompressedCache(cc.k_mean, cc.k_pages.float(), cc.v_pages, cc.page_table, B, S, N)
     refused("cmp k_pages must be torch.bfloat16", om.omnimem_select_compressed, c, bad, q(), K, G, 1, 0)
+    lo = torch.zeros((1, H, 64, D), dtype=torch.bfloat16)
+    bad = om.CompressedCache(cc.k_mean, cc.k_pages, cc.v_pages, cc.page_table, B, S, N, lo.float())
+    refused("cmp k_lo must be torch.bfloat16", om.omnimem_select_compressed, c, bad, q(), K, G, 1, 0)
+    bad = om.CompressedCache(cc.k_mean, cc.k_pages, cc.v_pages, cc.page_table, B, S, N, lo[:, :, :32].contiguous())
+    refused("cmp k_lo must have shape", om.omnimem_compress_chunk, c, 0, bad)
+    c32 = cache(torch.float32)
+    bad = om.CompressedCache(cc.k_mean, cc.k_pages.float(), cc.v_pages.float(), cc.page_table, B, S, N, lo)
+    refused("k_lo exists for bf16 caches only", om.omnimem_compress_chunk, c32, 0, bad)
     refused("q must be", om.omnimem_cmp_attn, cc, N, q(torch.float32))
     o = q()
     refused("gate_logits must be", om.omnimem_gated_combine, o, o, None, torch.zeros((LQ, H, 2)))

@@ -14,8 +14,12 @@ Shapes cover both kernel modes: 128-row slices that hold whole groups (G <= 64:
 G = 1, 7, 15, 32, 33, 40, 64) and slices that are parts of one group (G >= 65:
 one, two, three and 37 parts), several 64-key tiles with a ragged last tile,
 d = 64 and 128, B = 64 and 128, bf16 and fp32 queries, ragged last groups and
-non-resident blocks.
+non-resident blocks.  For bf16 caches the two key pieces come from the compressed
+cache's pooled-key and residual pages; the same selection with the pieces split per
+call (no residual pages) must be identical bit for bit.
 """
+import dataclasses
+
 import numpy as np
 import pytest
 import torch
@@ -106,6 +110,27 @@ def test_prob_small(dev, H, d, S, Lq, B, n, K, G, E, T, dtype):
         assert sel.awe_active == int(ref["awe"])
         assert not np.isin(host(sel.idx).numpy(), nonres).any()
         check_prob(sel, ref)
+        if cc.k_lo is not None:
+            check_residual(cc, c * Bpc)
+            say("  the same selection with the pooled keys split per call (no residual pages)")
+            split = omnimem_select_compressed(cache, dataclasses.replace(cc, k_lo=None), x.q, K, G, E, T, w.scale,
+                                              num_chunks=c, score_mode=SCORE_PROB)
+            torch.cuda.synchronize()
+            assert torch.equal(split.idx, sel.idx) and torch.equal(split.cnt, sel.cnt)
+            assert torch.equal(split.score, sel.score)
+
+
+def check_residual(cc, nb):
+    """The residual pages hold bf16(k_mean - bf16(k_mean)) of every pooled token, in
+    the pooled-key pages' layout, next to k_pages = bf16(k_mean) (torch rounds fp32
+    to bf16 to nearest even, as the kernels do)."""
+    H, d = int(cc.k_pages.shape[1]), int(cc.k_pages.shape[3])
+    km = cc.k_mean[:, :nb]
+    hi = km.to(torch.bfloat16)
+    lo = (km - hi.float()).to(torch.bfloat16)
+    tokens = lambda t: t.permute(1, 0, 2, 3).reshape(H, -1, d)[:, :nb]
+    assert torch.equal(tokens(cc.k_pages), hi)
+    assert torch.equal(tokens(cc.k_lo), lo)
 
 
 def test_prob_edge_cases(dev):

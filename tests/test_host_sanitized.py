@@ -49,6 +49,7 @@ test_abi.test_attention_validation()
 test_abi.test_select_noalloc_validation()
 test_abi.test_per_head_tables_and_chunk_decode_validation()
 test_abi.test_gated_combine_validation()
+test_abi.test_compressed_cache_validation()
 print("validation ok")
 
 # 2. the LRU bookkeeping against the oracle's policy model, per head
