@@ -177,6 +177,39 @@ __device__ __forceinline__ void sum_slab(const uint4 (&raw)[SlabShape<T, D, B>::
     for (int j = 0; j < Sh::VEC; ++j) colsum[j] += __shfl_xor(colsum[j], m);
 }
 
+// Column sums of a slab read CHUNK loads per lane at a time (for slabs whose loads
+// would not all fit in registers at once); the same per-lane order of adds as
+// load_slab + sum_slab, so the same sums bit for bit.
+template <typename T, int D, int B, int CHUNK>
+__device__ __forceinline__ void load_sum_slab(const T* __restrict__ slab, int nvalid, int lane,
+                                              float (&colsum)[Vec16<T>::N]) {
+  using Sh = SlabShape<T, D, B>;
+  static_assert(Sh::PASSES % CHUNK == 0, "whole chunks of loads");
+  const int c = lane % Sh::CPR, ph = lane / Sh::CPR;
+#pragma unroll
+  for (int j = 0; j < Sh::VEC; ++j) colsum[j] = 0.f;
+#pragma unroll 1
+  for (int i0 = 0; i0 < Sh::PASSES; i0 += CHUNK) {  // one chunk's loads live at a time
+    uint4 raw[CHUNK];
+#pragma unroll
+    for (int i = 0; i < CHUNK; ++i) {
+      const int row = ph + (i0 + i) * Sh::ROWS_PER_PASS;
+      raw[i] = row < nvalid ? load_once(slab + row * D + c * Sh::VEC) : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < CHUNK; ++i) {
+      float x[Sh::VEC];
+      Vec16<T>::widen(raw[i], x);
+#pragma unroll
+      for (int j = 0; j < Sh::VEC; ++j) colsum[j] += x[j];
+    }
+  }
+#pragma unroll
+  for (int m = Sh::CPR; m < kWave; m <<= 1)
+#pragma unroll
+    for (int j = 0; j < Sh::VEC; ++j) colsum[j] += __shfl_xor(colsum[j], m);
+}
+
 struct PoolArgs {
   const void* k_pages;
   const int32_t* page_table;
@@ -524,11 +557,17 @@ __global__ __launch_bounds__(kThreads) void k_compress_chunk(CompressArgs a) {
   for (int j = 0; j < VEC; ++j) ks[j] = vs[j] = 0.f;
   if (live) {
     const int64_t off = (page * a.H + h) * static_cast<int64_t>(B) * D;
-    uint4 kraw[Sh::PASSES], vraw[Sh::PASSES];  // both slabs' loads in flight before the sums
-    load_slab<T, D, B>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, kraw);
-    load_slab<T, D, B>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, vraw);
-    sum_slab<T, D, B>(kraw, ks);
-    sum_slab<T, D, B>(vraw, vs);
+    if constexpr (Sh::PASSES <= 32) {
+      uint4 kraw[Sh::PASSES], vraw[Sh::PASSES];  // both slabs' loads in flight before the sums
+      load_slab<T, D, B>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, kraw);
+      load_slab<T, D, B>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, vraw);
+      sum_slab<T, D, B>(kraw, ks);
+      sum_slab<T, D, B>(vraw, vs);
+    } else {
+      // fp32 slabs of 128 tokens (64 loads per lane each): K, then V, 32 loads in flight
+      load_sum_slab<T, D, B, 32>(static_cast<const T*>(a.k_pages) + off, nvalid, lane, ks);
+      load_sum_slab<T, D, B, 32>(static_cast<const T*>(a.v_pages) + off, nvalid, lane, vs);
+    }
     const float inv = 1.0f / static_cast<float>(nvalid);
 #pragma unroll
     for (int j = 0; j < VEC; ++j) {
