@@ -55,7 +55,7 @@ typedef enum { OMNIMEM_BF16 = 0, OMNIMEM_F32 = 1 } omnimem_dtype_t;
 typedef enum {
   OMNIMEM_OK = 0,
   OMNIMEM_EINVAL = -1,      /* a null, misaligned or out-of-range argument */
-  OMNIMEM_EUNSUPPORTED = -2,/* a shape or dtype this build has no kernel for */
+  OMNIMEM_EUNSUPPORTED = -2,/* a shape or dtype the library has no kernel for */
   OMNIMEM_EWORKSPACE = -3,  /* the workspace is smaller than the size query returns */
   OMNIMEM_EHIP = -4,        /* the HIP runtime reported an error at launch */
   OMNIMEM_ESCRATCH = -5     /* the problem needs more than omnimem_select_noalloc's static scratch */
