@@ -236,6 +236,31 @@ def test_running_max_jumps(dev):
         attn_check(out, lse, o_ref, l_ref, hs, qs, torch.bfloat16, f"jumps sparse {name}")
 
 
+def test_partial_first_tile(dev):
+    """The 64-row kernel takes its running max from the first tile's own scores: a
+    list that starts with a chunk's ragged tail block (8 valid tokens, NaN padding
+    after them) must set that max from the valid keys only, and the later tiles,
+    below it and then far above it, must still match the oracle."""
+    H, d, S, Lq, B, n = 2, 128, 200, 300, 64, 3   # 4 blocks per chunk, the last with 8 tokens
+    g = torch.Generator().manual_seed(21)
+    q = (0.5 * torch.randn(Lq, H, d, generator=g)).to(torch.bfloat16)
+    k = torch.randn(n, S, H, d, generator=g)
+    k[0, 192:] *= 4.0     # chunk 0's tail block: the first tile's scores, above the next blocks'
+    k[2, :64] *= 16.0     # chunk 2's first block: a jump far above them
+    k = k.to(torch.bfloat16)
+    v = torch.randn(n, S, H, d, generator=g).to(torch.bfloat16)
+    scale = d ** -0.5
+    cache = synth.page_layer(k.to(dev), v.to(dev), B, seed=9, pad_value=NAN)
+    qd = q.to(dev)
+    for ids in ([3, 0, 5, 8, 1, 11, 6], [3], [7, 3, 11]):
+        say(f"partial first tile: list {ids}")
+        idx = torch.tensor(ids, dtype=torch.int32).view(1, 1, -1).expand(H, 1, len(ids)).contiguous().to(dev)
+        cnt = torch.full((H, 1), len(ids), dtype=torch.int32, device=dev)
+        out, lse = omnimem_sparse_attn(cache, qd, idx, cnt, Lq, scale)
+        o_ref, l_ref, hs, qs = oracle.sparse_attn(q, k, v, B, idx.cpu().numpy(), cnt.cpu().numpy(), Lq, scale)
+        attn_check(out, lse, o_ref, l_ref, hs, qs, torch.bfloat16, f"partial first tile {ids}")
+
+
 # ------------------------------------------------------------- long block lists
 
 @pytest.mark.parametrize("n,zero_q,K", [(5000, True, 64), (5000, False, 64), (20000, False, 64), (20000, True, 64),
