@@ -76,6 +76,10 @@ def parse():
                    help="only sample socket power and GFX clock while the attention kernel (the bench layer's "
                         "queries, then Q = 0) and the MFMA issue loop (smooth, then random operands) each run "
                         "back to back for a few seconds, print the line, and exit")
+    p.add_argument("--cu-fill", action="store_true",
+                   help="only time the attention kernel with 228 and with 256 workgroups of 256 query rows "
+                        "(one per CU), 64 or 57-58 key tiles each, sampling socket power and GFX clock, print "
+                        "the line, and exit")
     p.add_argument("--prob-only", type=int, default=0, metavar="G",
                    help="only time selection by probability-averaged scores from the pooled history, "
                         "query groups of G rows (top-64 for one group per head, else top-4), and exit")
@@ -224,6 +228,81 @@ def power_clock(dev, secs=6.0):
     print(json.dumps({"power_clock": res}), flush=True)
 
 
+def cu_fill(dev, secs=3.0):
+    """What a split of each (head, group)'s key list over all 256 CUs could gain.  At
+    the bench shape the 64-row kernel runs 228 workgroups (12 heads x 19 tiles of 256
+    rows), one per CU, each over 64 key tiles, so 28 CUs idle.  A split that balanced
+    the work would give every CU 57 tiles.  The kernel is timed on synthetic layers
+    of the same per-workgroup shape (seeded normal K, V and Q; one query group per
+    head; 64 or 57-58 blocks of 64 tokens drawn at random from a 20-chunk history of
+    4680-token chunks, full blocks only): 12 heads x 4680 rows (228 workgroups) and
+    16 heads x 4096 rows (256 workgroups), each run back to back for `secs` with
+    socket power and GFX clock read twice.  The 256-workgroup runs at 57 and 58
+    tiles price the balanced split before any merge of its partial results."""
+    import threading
+
+    import torch
+
+    from paper_2605_30519_amd import omnimem_sparse_attn, synth
+    n, S, d, B = 20, 4680, 128, 64
+    Bpc = -(-S // B)
+    full = torch.tensor([c * Bpc + o for c in range(n) for o in range(Bpc - 1)], dtype=torch.int32)
+    scale = 1.0 / d ** 0.5
+    caches = {}
+    res = {"history": f"{n} chunks of {S} tokens, blocks of {B}", "seconds_per_case": secs}
+    for H, lq, K in ((12, 4680, 64), (12, 4680, 57), (16, 4096, 64), (16, 4096, 57), (16, 4096, 58)):
+        g = torch.Generator(device="cpu").manual_seed(1000 * H + K)
+        if H not in caches:
+            k = torch.randn((n, S, H, d), generator=g).to(torch.bfloat16).to(dev)
+            v = torch.randn((n, S, H, d), generator=g).to(torch.bfloat16).to(dev)
+            caches[H] = synth.page_layer(k, v, B, seed=H)
+            del k, v
+        cache = caches[H]
+        q = torch.randn((lq, H, d), generator=g).to(torch.bfloat16).to(dev)
+        idx = torch.stack([torch.sort(full[torch.randperm(full.numel(), generator=g)[:K]]).values for _ in range(H)])
+        idx = idx.reshape(H, 1, K).contiguous().to(dev)
+        cnt = torch.full((H, 1), K, dtype=torch.int32, device=dev)
+        out = torch.empty_like(q)
+        lse = torch.empty((H, lq), dtype=torch.float32, device=dev)
+
+        def call():
+            omnimem_sparse_attn(cache, q, idx, cnt, lq, scale, out=out, lse=lse)
+        samples = []
+
+        def sampler():
+            for delay in (0.5 * secs, 0.25 * secs):
+                time.sleep(delay)
+                samples.append((float(torch.cuda.power_draw(dev)), float(torch.cuda.clock_rate(dev))))
+        for _ in range(500):
+            call()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        th = threading.Thread(target=sampler)
+        calls, t_stop = 0, time.time() + secs
+        th.start()
+        e0.record()
+        while time.time() < t_stop:
+            for _ in range(500):
+                call()
+            calls += 500
+            torch.cuda.synchronize()
+        e1.record()
+        torch.cuda.synchronize()
+        th.join()
+        us = e0.elapsed_time(e1) / calls * 1e3
+        wgs = H * -(-lq // 256)
+        fl = 4.0 * d * H * lq * K * B
+        name = f"h{H}_rows{lq}_top{K}"
+        res[name] = {"workgroups": wgs, "tiles_per_workgroup": K, "us_per_call": round(us, 1),
+                     "tflops": round(fl / (us * 1e-6) / 1e12, 1), "ns_per_workgroup_tile": round(us * 1e3 / K, 1),
+                     "socket_power_w": [s[0] for s in samples], "gfx_clock_mhz": [s[1] for s in samples]}
+        log(f"{name}: {res[name]}")
+        del q, idx, cnt, out, lse
+    base = res["h12_rows4680_top64"]["us_per_call"]
+    res["balanced_split_bound_speedup"] = round(base / res["h16_rows4096_top57"]["us_per_call"], 4)
+    print(json.dumps({"cu_fill": res}), flush=True)
+
+
 def select_only(dev, calls, warm=100):
     """omnimem_select alone over the bench workload's rotated layer caches (so that K
     is read from HBM, as in the bench), HIP events around each call: a profiling
@@ -325,6 +404,9 @@ def main():
         return
     if args.power_clock:
         power_clock(dev)
+        return
+    if args.cu_fill:
+        cu_fill(dev)
         return
     if args.prob_only:
         prob_only(dev, args.prob_only)
