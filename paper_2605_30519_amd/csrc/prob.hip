@@ -26,7 +26,7 @@
 // key: the sum over a group's rows is a sum over the lane's accumulator rows).
 // The group means become the order-preserving keys that k_topk ranks (0 outside
 // Omega): written by k_prob_partial when its slice holds whole groups, else by
-// k_prob_merge, which sums a group's slices in order.
+// k_prob_merge, which sums a group's slices in a fixed order.
 #include <math.h>
 
 #include "device_common.h"
@@ -391,28 +391,39 @@ __global__ __launch_bounds__(kPThreads, 2) void k_prob_partial(ProbArgs a) {
   }
 }
 
-// Slices that are parts of one group: the group's parts summed in order.
+// Slices that are parts of one group: the group's parts summed, four lanes per
+// pooled key.  Lane j of a key adds parts j, j + 4, j + 8, ... in order, with every
+// load in flight before its adds, and the four sums meet as (s0 + s1) + (s2 + s3):
+// a fixed order, so the result does not depend on timing.
+constexpr int kMergeLanes = 4;
 __global__ __launch_bounds__(kPThreads) void k_prob_merge(const float* __restrict__ part, int nseg, int nb, int nbp,
                                                           int lq, int G, int R, int spg,
                                                           const int32_t* __restrict__ page_table, int64_t pt_stride,
                                                           int64_t num_pages,
                                                           int first_excluded, uint32_t* __restrict__ keys) {
-  const int b = blockIdx.x * kPThreads + threadIdx.x, r = blockIdx.y, h = blockIdx.z;
-  if (b >= nb) return;
+  const int b = blockIdx.x * (kPThreads / kMergeLanes) + static_cast<int>(threadIdx.x) / kMergeLanes;
+  const int j = static_cast<int>(threadIdx.x) % kMergeLanes, r = blockIdx.y, h = blockIdx.z;
   const int rows = min(r * G + G, lq) - r * G;
-  float s = 0.f;
   const int parts = (rows + kPRows - 1) / kPRows;
-  // the parts added in slice order, kBatch loads in flight before their adds
-  constexpr int kBatch = 16;
-  const float* src = part + (static_cast<int64_t>(h) * nseg + r * spg) * nb + b;
-  for (int k0 = 0; k0 < parts; k0 += kBatch) {
-    float v[kBatch];
+  float s = 0.f;
+  if (b < nb) {  // no return before the shuffles: every lane takes part in them
+    constexpr int kBatch = 16;
+    const float* src = part + (static_cast<int64_t>(h) * nseg + r * spg) * nb + b;
+    for (int k0 = j; k0 < parts; k0 += kBatch * kMergeLanes) {
+      float v[kBatch];
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u) v[u] = k0 + u < parts ? src[static_cast<int64_t>(k0 + u) * nb] : 0.f;
+      for (int u = 0; u < kBatch; ++u) {
+        const int k = k0 + kMergeLanes * u;
+        v[u] = k < parts ? src[static_cast<int64_t>(k) * nb] : 0.f;
+      }
 #pragma unroll
-    for (int u = 0; u < kBatch; ++u)
-      if (k0 + u < parts) s += v[u];
+      for (int u = 0; u < kBatch; ++u)
+        if (k0 + kMergeLanes * u < parts) s += v[u];
+    }
   }
+  s += __shfl_xor(s, 1);
+  s += __shfl_xor(s, 2);
+  if (b >= nb || j != 0) return;
   s = s / static_cast<float>(rows);
   const int32_t p = page_table != nullptr ? page_table[static_cast<int64_t>(h) * pt_stride + b] : 0;
   const bool live = b < first_excluded && p >= 0 && (page_table == nullptr || p < num_pages);
@@ -465,7 +476,8 @@ hipError_t launch_prob_typed(const CacheGeom& g, const SelectPlan& p, const void
   else
     st(k_prob_partial<T, D, false>, dim3(p.prob_slices * g.H), dim3(kPThreads), 0, stream, a);
   if (!a.multi) {
-    const dim3 mgrid((g.nb + kPThreads - 1) / kPThreads, p.R, g.H);
+    constexpr int kMergeKeys = kPThreads / kMergeLanes;
+    const dim3 mgrid((g.nb + kMergeKeys - 1) / kMergeKeys, p.R, g.H);
     st(k_prob_merge, mgrid, dim3(kPThreads), 0, stream, part, p.prob_nseg, g.nb, nbp, p.lq, p.G, p.R, p.prob_spg,
        g.page_table, g.pt_stride, g.num_pages, p.first_excluded, keys);
   }
