@@ -23,6 +23,7 @@
 //
 // f32 kernel (k_attn_f32): one lane per query row, fp32 dot products and exact
 // expf-based online softmax, for fp32 inputs.
+#include <limits.h>
 #include <math.h>
 #include <atomic>
 #include <type_traits>
@@ -136,14 +137,15 @@ __device__ __forceinline__ void resolve_list(const AttnArgs& a, int hr, const in
 // LDS: entry i = (page, (sub-tile << 8) | valid keys).  Padding, out-of-range ids and
 // non-resident pages produce no tile; a B = 128 block produces up to two.  One list
 // entry per thread, compacted with a block-wide prefix sum; returns the tile count.
-// Contains barriers: every thread of the workgroup must call it.
+// Contains barriers: every thread of the workgroup must call it.  pre_id, unless
+// INT_MIN, is this thread's list entry, already read by the caller.
 template <int NT>
 __device__ int decode_tiles(const AttnArgs& a, const int32_t* pt, const int32_t* list, int count, int first,
-                            int2* table, int* scan_tmp) {
+                            int2* table, int* scan_tmp, int pre_id = INT_MIN) {
   const int e = first + static_cast<int>(threadIdx.x);
   int ntiles = 0, page = 0, nvb = 0;
   if (e < count) {
-    const int id = list ? list[e] : a.dense_first + e;
+    const int id = pre_id != INT_MIN ? pre_id : list ? list[e] : a.dense_first + e;
     if (id >= 0 && id < a.nb) {
       const int32_t p = pt[id];
       if (p >= 0 && p < a.num_pages) {
@@ -857,6 +859,9 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   resolve_list(a, hr, list, count);
 
   const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
+  // this thread's entry of the first decoded stretch, read without waiting for the
+  // count (the list holds top_k entries)
+  const int id0 = list != nullptr && tid < a.top_k ? list[tid] : INT_MIN;
   const int half = lane / 32;
   const uint16_t* qp = static_cast<const uint16_t*>(a.q);
   const uint16_t* kp = static_cast<const uint16_t*>(a.k_pages);
@@ -901,7 +906,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       ntab = 0;
       ti = 0;
       while (ntab == 0 && next_entry < count) {
-        ntab = decode_tiles<NT>(a, head_table(a, h), list, count, next_entry, table, scan_tmp);
+        ntab = decode_tiles<NT>(a, head_table(a, h), list, count, next_entry, table, scan_tmp,
+                                next_entry == 0 ? id0 : INT_MIN);
         next_entry += NT;
       }
       if (ntab == 0) return make_int2(0, 0);  // past the end: an empty tile
@@ -1246,7 +1252,9 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
   __syncthreads();
 
   // ---- epilogue: normalise, stage O through LDS (one 16 KB stage per wave, chunks
-  // permuted like K), store rows with 16-byte writes
+  // permuted like K), store rows with 16-byte nontemporal writes (each row is written
+  // once, and the L2 then holds no dirty lines of O for the end of the kernel to
+  // write back)
   uint8_t* const stage_o = k_ring + wave * kR64TileBytes;  // 64 rows x 256 B per wave
   auto finish = [&](f32x16 (&o)[DT], float ms, float l, int g) {
     const float l_tot = pair_sum(l);
@@ -1281,8 +1289,8 @@ __global__ __launch_bounds__(kR64Waves* kWave, 1) void k_attn_bf16_r64(AttnArgs 
       const int r = cid / 16, ch = cid % 16;
       const int qrow = wrow + r;
       if (qrow < row_end)
-        *reinterpret_cast<uint4*>(op + (static_cast<int64_t>(qrow) * a.H + h) * D + ch * 8) =
-            *reinterpret_cast<const uint4*>(stage_o + k_pos(r, ch));
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(stage_o + k_pos(r, ch)),
+                                    reinterpret_cast<u32x4*>(op + (static_cast<int64_t>(qrow) * a.H + h) * D + ch * 8));
     }
   }
 }
