@@ -253,34 +253,43 @@ class PagedKVCache:
     def descriptor(self, num_chunks: Optional[int] = None, with_table: bool = True) -> omnimem_kv_cache_t:
         """C descriptor; `num_chunks` < n exposes only the oldest chunks (a shorter history);
         with_table=False passes a NULL page table (selection from pooled keys only)."""
-        if self.k_pages.dtype not in _DTYPES or self.v_pages.dtype != self.k_pages.dtype:
-            raise TypeError(f"unsupported page dtype {self.k_pages.dtype}")
-        for t in (self.k_pages, self.v_pages, self.page_table):
+        kp, vp, pt = self.k_pages, self.v_pages, self.page_table
+        if kp.dtype not in _DTYPES or vp.dtype != kp.dtype:
+            raise TypeError(f"unsupported page dtype {kp.dtype}")
+        for t in (kp, vp, pt):
             if not t.is_contiguous():
                 raise ValueError("cache tensors must be contiguous")
-        if self.page_table.dtype != torch.int32:
+        if pt.dtype != torch.int32:
             raise TypeError("page_table must be int32")
-        if self.k_pages.dim() != 4 or self.v_pages.shape != self.k_pages.shape:
+        if kp.dim() != 4 or vp.shape != kp.shape:
             raise ValueError("k_pages and v_pages must share one [num_pages, H, B, d] shape")
-        if not (self.page_table.dim() == 2 or (self.page_table.dim() == 3 and
-                                               int(self.page_table.shape[0]) == self.num_heads)) \
-                or int(self.page_table.shape[-1]) != self.blocks_per_chunk:
-            raise ValueError(f"page_table must be [n, {self.blocks_per_chunk}] or "
-                             f"[{self.num_heads}, n, {self.blocks_per_chunk}] (blocks per chunk)")
-        _on_gpu(self.k_pages, v_pages=self.v_pages, page_table=self.page_table)
-        n = self.num_chunks if num_chunks is None else int(num_chunks)
-        if n > self.num_chunks:
+        num_pages, H, B, d = (int(x) for x in kp.shape)
+        bpc = -(-self.chunk_tokens // B)
+        pt_shape = tuple(pt.shape)
+        if not (len(pt_shape) == 2 or (len(pt_shape) == 3 and pt_shape[0] == H)) or pt_shape[-1] != bpc:
+            raise ValueError(f"page_table must be [n, {bpc}] or [{H}, n, {bpc}] (blocks per chunk)")
+        _on_gpu(kp, v_pages=vp, page_table=pt)
+        total = pt_shape[-2]
+        n = total if num_chunks is None else int(num_chunks)
+        if n > total:
             raise ValueError("num_chunks exceeds the page table")
         return omnimem_kv_cache_t(
-            _DTYPES[self.k_pages.dtype], self.num_heads, self.head_dim, self.block_size, self.chunk_tokens, n,
-            int(self.k_pages.shape[0]), self.k_pages.data_ptr(), self.v_pages.data_ptr(),
-            self.page_table.data_ptr() if with_table else None,
-            self.num_chunks * self.blocks_per_chunk if self.per_head_tables else 0)
+            _DTYPES[kp.dtype], H, d, B, self.chunk_tokens, n, num_pages, kp.data_ptr(), vp.data_ptr(),
+            pt.data_ptr() if with_table else None, total * bpc if len(pt_shape) == 3 else 0)
+
+
+def _current_raw_stream():
+    """The current device's current stream as a raw handle: torch's own accessor for
+    it when this torch has one (it builds no Stream object), else the public API."""
+    try:
+        return torch._C._cuda_getCurrentRawStream(torch._C._cuda_getDevice())
+    except AttributeError:
+        return torch.cuda.current_stream().cuda_stream
 
 
 def _stream(stream):
     if stream is None:
-        return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        return ctypes.c_void_p(_current_raw_stream())
     if isinstance(stream, torch.cuda.Stream):
         return ctypes.c_void_p(stream.cuda_stream)
     return ctypes.c_void_p(int(stream))
@@ -311,6 +320,10 @@ def _need(cond: bool, msg: str):
 
 def _on_gpu(like: torch.Tensor, like_name: str = "the cache", **tensors):
     """Every given tensor (None = absent) lives on the GPU that holds `like`."""
+    if like.is_cuda:  # the common case, without building any message
+        dev = like.get_device()
+        if all(t is None or (t.is_cuda and t.get_device() == dev) for t in tensors.values()):
+            return
     _need(like.is_cuda, f"{like_name} must live on a GPU")
     for name, t in tensors.items():
         if t is None:
@@ -320,6 +333,8 @@ def _on_gpu(like: torch.Tensor, like_name: str = "the cache", **tensors):
 
 
 def _check_tensor(name: str, t, shape, dtype):
+    if isinstance(t, torch.Tensor) and t.dtype == dtype and tuple(t.shape) == tuple(shape) and t.is_contiguous():
+        return  # the common case, without building any message
     _need(isinstance(t, torch.Tensor), f"{name} must be a tensor")
     _need(tuple(t.shape) == tuple(shape), f"{name} must have shape {tuple(shape)}, not {tuple(t.shape)}")
     _need(t.dtype == dtype, f"{name} must be {dtype}, not {t.dtype}")
