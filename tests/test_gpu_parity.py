@@ -266,9 +266,9 @@ def test_long_sparse_lists(dev):
     """Lists longer than one decoded stretch of the 64-row kernel (256 entries):
     the first stretch's entries are read before the list's count, later ones after
     it.  Padding, non-resident blocks and duplicates sit on both
-    sides of entry 256, and the two heads' counts end the list in the second
-    stretch at different places."""
-    H, d, S, Lq, B, n = 2, 128, 640, 100, 64, 40   # 10 full blocks per chunk, 400 blocks
+    sides of entry 256; the heads' counts end the list in the second stretch at two
+    places, exactly at its start (256), and one head's list is all padding."""
+    H, d, S, Lq, B, n = 4, 128, 640, 100, 64, 40   # 10 full blocks per chunk, 400 blocks
     nb = n * (S // B)
     g = torch.Generator().manual_seed(33)
     q = (0.5 * torch.randn(Lq, H, d, generator=g)).to(torch.bfloat16)
@@ -284,10 +284,10 @@ def test_long_sparse_lists(dev):
     for h in range(H):
         ids = rng.permutation(nb)[:top_k].astype(np.int32)
         ids[[3, 255, 256, 290]] = -1          # padding on both sides of entry 256
-        ids[[100, 258]] = nonres[h]           # non-resident
+        ids[[100, 258]] = nonres[h % 3]       # non-resident
         ids[[200, 259]] = ids[50]             # duplicates of a valid id
-        idx[h, 0] = ids
-    cnt = np.array([[300], [270]], np.int32)
+        idx[h, 0] = ids if h < 3 else -1     # head 3: nothing but padding
+    cnt = np.array([[300], [270], [256], [300]], np.int32)
     idx_d, cnt_d = torch.from_numpy(idx).to(dev), torch.from_numpy(cnt).to(dev)
     out, lse = omnimem_sparse_attn(cache, q.to(dev), idx_d, cnt_d, Lq, scale)
     o_ref, l_ref, hs, qs = oracle.sparse_attn(q, k, v, B, idx, cnt, Lq, scale, resident=resident)
